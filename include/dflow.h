@@ -1,0 +1,238 @@
+/*
+ * dflow.h - C ABI of the MI355X (gfx950) DFlow speculative-decoding round.
+ *
+ * One round of block-diffusion speculative decoding with verifier information
+ * relay (DFlow):
+ *   dflow_draft_block       block drafting: drafter inputs built from the mask
+ *                           embedding and the relayed verifier states
+ *                           (Sec. 4.2, eqs. reject_conditioning, dflow_input),
+ *                           one parallel drafter forward conditioned on fused
+ *                           target features (Sec. 3, eqs. dflash_context,
+ *                           dflash_drafting);
+ *   dflow_verify_block      target forward over the block against the KV cache
+ *                           (Sec. 3, exact-match verification);
+ *   dflow_accept_and_carry  longest-prefix acceptance, bonus token, block
+ *                           partition (Sec. 3, eq. verification_partition),
+ *                           joint W_c projection of the verifier states and
+ *                           the shifted carry record (Sec. 4.2, verifier
+ *                           representation alignment);
+ *   kv_commit               commit of the accepted prefix plus bonus; the
+ *                           rejected positions are rolled back (Sec. 3; Sec. 1
+ *                           on the rejection boundary as the commit boundary).
+ *
+ * Conventions
+ *  - Every data pointer argument is a DEVICE pointer owned by the caller unless
+ *    stated otherwise; the library never frees caller memory.  Weight, cache
+ *    and page-table pointers registered at dflow_create must stay valid until
+ *    dflow_destroy.  The library allocates its own workspace at create.
+ *  - Every call is asynchronous on the given hipStream_t (0 = null stream) and
+ *    performs no host synchronisation, except dflow_read_status.
+ *  - Return value: DFLOW_OK (0) or a negative DFLOW_E* code; the thread-local
+ *    message of the last failure is available from dflow_last_error().  Host-
+ *    checkable errors are reported before any launch.  Conditions that depend
+ *    on device-resident values (a token id out of range, a position past the
+ *    sequence's page table) set bits of the device status word instead and the
+ *    offending writes are skipped; read it with dflow_read_status.
+ *  - Storage type: DFLOW_BF16 (weights, activations and KV in bf16, fp32
+ *    accumulation, fp32 logits) or DFLOW_F32.  Token ids are int32.
+ *  - Shape constraints: d, ffn, relay_hidden, n_heads*head_dim and vocab must
+ *    be multiples of 16; d, ffn and n_heads*head_dim multiples of 32 (bf16) or
+ *    16 (f32); head_dim is 64 or 128; block <= 64.
+ *  - Batch: b sequences (slots 0..b-1), each with the same block size B.
+ *    Per-sequence positions, acceptance lengths and carry sizes are device
+ *    arrays, so sequences may be ragged.
+ *
+ * Layouts
+ *  - Linear weights are [out, in] row-major in the source and must be
+ *    converted with dflow_pack_linear into the library's tile layout (same
+ *    byte size).  The target/drafter QKV weight is the row concatenation
+ *    [Wq; Wk; Wv]; the gate/up weight is [W_gate; W_up] packed with
+ *    gate_up = 1.  Norm gains, biases, embeddings and E_mask stay plain.
+ *  - KV pools, one per layer, consecutive:
+ *      K: [layer][num_pages][n_kv_heads][64 slots][head_dim]
+ *      V: [layer][num_pages][n_kv_heads][head_dim][64 slots]   (transposed)
+ *    Position p of sequence s lives in page page_table[s*max_pages + p/64],
+ *    slot p%64.  The drafter's context cache has the same layout with
+ *    n_draft_layers layers and shares the page table.
+ */
+#ifndef DFLOW_H
+#define DFLOW_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DFLOW_OK 0
+#define DFLOW_EINVAL (-1)       /* null pointer, bad enum value, bad index */
+#define DFLOW_ESHAPE (-2)       /* a dimension violates the shape constraints */
+#define DFLOW_EDTYPE (-3)       /* unsupported storage type */
+#define DFLOW_ECAPACITY (-4)    /* rows/sequences beyond what the context was created for */
+#define DFLOW_EHIP (-5)         /* a HIP runtime call failed */
+#define DFLOW_EUNSUPPORTED (-6) /* valid request the library does not implement */
+
+#define DFLOW_F32 0
+#define DFLOW_BF16 1
+
+/* Which verifier rows are relayed (Sec. 4.2).  SUFFIX: rows a+1..K-1, i.e.
+ * the states that predict the rejected-suffix positions, placed at next-round
+ * block indices 1..K-1-a.  SUFFIX_TAIL: rows a+1..K (also the state after the
+ * last draft). */
+#define DFLOW_CARRY_SUFFIX 0
+#define DFLOW_CARRY_SUFFIX_TAIL 1
+
+/* device status bits */
+#define DFLOW_STATUS_BAD_TOKEN 1
+#define DFLOW_STATUS_CAPACITY 2
+#define DFLOW_STATUS_BAD_PAGE 4
+
+typedef struct dflow_dims {
+  int dtype;              /* DFLOW_F32 or DFLOW_BF16 */
+  int d;                  /* hidden size */
+  int n_layers;           /* target decoder layers */
+  int n_heads;            /* query heads */
+  int n_kv_heads;         /* key/value heads (divides n_heads) */
+  int head_dim;           /* 64 or 128 */
+  int ffn;                /* SwiGLU intermediate size */
+  int vocab;
+  int n_draft_layers;     /* drafter decoder layers (Sec. 5.1: five) */
+  int n_capture;          /* m, number of target layers feeding W_c */
+  int capture_layers[16]; /* 0-based target layer indices, increasing */
+  int relay_hidden;       /* MLP_phi hidden width */
+  int block;              /* B = anchor + K drafted tokens */
+  int max_batch;          /* sequences per call */
+  int max_rows;           /* rows per prefill chunk (>= block) */
+  int max_pages;          /* page-table row length per sequence */
+  int num_pages;          /* pages in each layer pool */
+  int carry_window;       /* DFLOW_CARRY_* */
+  float rope_theta;       /* RoPE base (1e6 for Qwen3) */
+  float rms_eps;          /* RMSNorm epsilon */
+  float ln_eps;           /* relay LayerNorm epsilon */
+} dflow_dims;
+
+typedef struct dflow_layer {
+  const void* attn_norm;  /* [d] */
+  const void* wqkv;       /* packed [(n_heads+2*n_kv_heads)*head_dim, d] */
+  const void* q_norm;     /* [head_dim] */
+  const void* k_norm;     /* [head_dim] */
+  const void* wo;         /* packed [d, n_heads*head_dim] */
+  const void* ffn_norm;   /* [d] */
+  const void* wgu;        /* packed (gate_up=1) [2*ffn, d] */
+  const void* wdown;      /* packed [d, ffn] */
+} dflow_layer;
+
+typedef struct dflow_weights {
+  const void* embed;            /* [vocab, d] plain row-major (shared by target, drafter and relay) */
+  const void* final_norm;       /* [d] target final RMSNorm gain */
+  const void* lm_head;          /* packed [vocab, d] (shared by target and drafter) */
+  const dflow_layer* layers;    /* HOST array [n_layers] */
+  const dflow_layer* draft_layers; /* HOST array [n_draft_layers] */
+  const void* draft_final_norm; /* [d] */
+  const void* e_mask;           /* [d] mask embedding E_mask */
+  const void* w_c;              /* packed [d, n_capture*d] feature projection W_c */
+  const void* g_c;              /* [d] RMSNorm gain after W_c */
+  const void* relay_w1;         /* packed [relay_hidden, 3d] */
+  const void* relay_c1;         /* [relay_hidden] */
+  const void* relay_w2;         /* packed [2d, relay_hidden] -> [beta; gamma] */
+  const void* relay_c2;         /* [2d] */
+  const void* relay_ln_g;       /* [d] LayerNorm gain */
+  const void* relay_ln_b;       /* [d] LayerNorm bias */
+} dflow_weights;
+
+typedef struct dflow_cache {
+  void* k_pool;                 /* target K pools, n_layers consecutive */
+  void* v_pool;                 /* target V pools */
+  void* ck_pool;                /* drafter context K pools, n_draft_layers consecutive */
+  void* cv_pool;                /* drafter context V pools */
+  const int32_t* page_table;    /* [max_batch][max_pages] page ids in [0, num_pages) */
+} dflow_cache;
+
+typedef struct dflow_ctx dflow_ctx;
+
+/* Thread-local description of the last error of this thread ("" if none). */
+const char* dflow_last_error(void);
+
+/* Bytes of one packed linear weight of shape [N, K] (equal to N*K*elt). */
+size_t dflow_packed_bytes(int dtype, int N, int K);
+
+/* Rearranges a row-major [N, K] weight into the tile layout the GEMM kernels
+ * stream.  gate_up = 1 interleaves the 16-row strips of the two halves
+ * [W_gate; W_up].  `w` and `out` are device buffers of dflow_packed_bytes. */
+int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, void* out);
+
+/* Bytes of device workspace that dflow_create allocates for these dims. */
+size_t dflow_workspace_bytes(const dflow_dims* dims);
+
+/* Validates dims, copies the (device) weight/cache pointers, allocates the
+ * workspace and the RoPE table.  *out receives the context. */
+int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache, dflow_ctx** out);
+int dflow_destroy(dflow_ctx* ctx);
+
+/* Prompt processing for sequence slot `seq` (set-up, not part of the round):
+ * target KV for positions 0..len-1, fused features and drafter context K/V
+ * for the same positions, and first_anchor[0] = the target's greedy token
+ * after the prompt.  Clears the slot's carry record.  tok: device [len]. */
+int dflow_prefill(dflow_ctx* ctx, hipStream_t stream, int seq, const int32_t* tok, int len, int32_t* first_anchor);
+
+/* Block drafting (Sec. 3 eq. dflash_drafting; Sec. 4.2 eq. dflow_input).
+ * Block row 0 is anchor_tok[s] at position anchor_pos[s]; rows 1..K start
+ * from E_mask, except rows 1..n_carry[s] of the previous accept_and_carry,
+ * which take E_mask + beta*LN(h) + gamma when carry_on != 0.  Every block row
+ * attends to the drafter context (positions < anchor_pos) and to the whole
+ * block.  Writes draft_tok [b, K] (argmax of rows 1..K) and, if non-null,
+ * block_out [b, B] = [anchor, drafts] and, if non-null, the fp32 drafter
+ * logits of every block row, draft_logits [b*B, vocab] (row 0 unused).
+ * The block's K/V are written to the drafter context cache at
+ * anchor_pos..anchor_pos+K as scratch and are overwritten by kv_commit. */
+int dflow_draft_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* anchor_tok,
+                      const int32_t* anchor_pos, int carry_on, int32_t* draft_tok, int32_t* block_out,
+                      float* draft_logits);
+
+/* Exact-match verification forward (Sec. 3).  block_tok [b, B] holds the
+ * anchor followed by the K proposals, at positions start_pos[s]..+K.  Writes
+ * the target KV of all B positions (speculatively; kv_commit rolls back the
+ * rejected ones), the target argmax per row tgt_argmax [b, B] (lowest id on
+ * ties), optional fp32 logits [b, B, vocab], and the residual outputs of the
+ * capture layers, which accept_and_carry projects (hcap: pass NULL to use
+ * the internal buffer; otherwise a device [b*B, n_capture*d] copy). */
+int dflow_verify_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,
+                       const int32_t* start_pos, int32_t* tgt_argmax, float* logits, void* hcap);
+
+/* Acceptance and relay preparation (Sec. 3 eq. verification_partition;
+ * Sec. 4.2).  a = number of leading proposals equal to the target argmax of
+ * the previous row; bonus = argmax of row a; committed [b, B] = d_1..d_a,
+ * bonus, then -1.  Projects every verified row with the shared W_c + RMSNorm
+ * (rows 0..a become drafter context at kv_commit, rows a+1.. are the relay
+ * source) and records the carry for the next dflow_draft_block.  Launches no
+ * target-layer kernel.  feat (nullable): device [b*B, d] copy of the
+ * projected features. */
+int dflow_accept_and_carry(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,
+                           const int32_t* tgt_argmax, int32_t* accept_len, int32_t* bonus, int32_t* committed,
+                           int32_t* n_carry, void* feat);
+
+/* Commit (rollback = truncation): seq_len[s] += accept_len[s] + 1, where
+ * seq_len[s] must equal the start_pos used by the verify.  Appends the drafter
+ * context K/V of the projected rows 0..accept_len[s] at positions
+ * seq_len..seq_len+accept_len (the name follows the paper's round contract). */
+int kv_commit(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* accept_len, int32_t* seq_len);
+
+/* Measurement construct (not part of the method): builds the verified block
+ * [anchor, forced drafts] from a target trajectory traj [b, traj_stride]
+ * (absolute positions, traj_len valid entries) and this round's plan
+ * mode/tok [b, B]: mode 1 -> traj[t+j], 2 -> (traj[t+j] + 1 + tok) mod vocab,
+ * 0 -> tok, with t = start_pos[s]. */
+int dflow_bench_force_drafts(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* traj, int traj_stride,
+                             int traj_len, const int8_t* mode, const int32_t* tok, const int32_t* anchor,
+                             const int32_t* start_pos, int32_t* block_tok);
+
+/* Synchronises `stream`, copies the device status word to *host_status and,
+ * if clear != 0, resets it. */
+int dflow_read_status(dflow_ctx* ctx, hipStream_t stream, int32_t* host_status, int clear);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DFLOW_H */

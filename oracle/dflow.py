@@ -208,10 +208,13 @@ class OracleDFlow:
         return n, [a + i for i in range(1, n + 1)]
 
     def round(self, s: SeqState, carry_on: bool = True, block: Optional[Sequence[int]] = None,
-              force=None) -> RoundResult:
+              force=None, decide: Optional[Sequence[int]] = None) -> RoundResult:
         """One drafting/verification round.  `block` replaces the verified
         tokens; `force=(traj, mode, tok)` builds them with forced_block.  The
-        drafter runs in full either way."""
+        drafter runs in full either way.  `decide(a, bonus, logits)` may
+        replace the acceptance outcome; parity tests use it to follow the
+        device through a near-tie that the numerical tolerance cannot
+        decide."""
         t = s.t
         d, dlg, x, n_relay = self.draft(s, carry_on)
         if block is None and force is not None:
@@ -223,6 +226,9 @@ class OracleDFlow:
         assert block[0] == s.anchor and len(block) == self.B
         logits, g, hcat, ks, vs = self.verify(s, block)
         a, bonus, committed = self.accept(block, g)
+        if decide is not None:
+            a, bonus = (int(v) for v in decide(a, bonus, logits))
+            committed = [int(x) for x in block[1:a + 1]] + [bonus]
         f = self.m.fuse(hcat)
         # commit: positions t..t+a join the caches; t+a+1.. are rolled back
         for l in range(self.m.dims.n_layers):

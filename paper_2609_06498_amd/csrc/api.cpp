@@ -1,0 +1,551 @@
+// C ABI of the DFlow round: context, workspace and the call sequences of the
+// four round calls (draft, verify, accept-and-carry, commit) plus prefill.
+// Every computation is a HIP kernel launch on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/dflow.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace dflow;
+
+namespace {
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIPCHK(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return fail(DFLOW_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+}  // namespace
+
+struct dflow_ctx {
+  dflow_dims dm;
+  bool bf;
+  size_t elt;
+  int KT;
+  int q_dim, kv_dim, qkv_n;
+  int mmax, rows_round;
+  int G, nsplit, part_items;
+  int lm_groups;
+
+  dflow_weights w;
+  std::vector<dflow_layer> layers, dlayers;
+  dflow_cache c;
+  size_t pool_layer_elems;   // elements of one layer pool (K or V)
+
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  // workspace views
+  void *x, *xn, *qkv, *q, *attn, *act, *hcap, *f, *fpre, *u, *hid;
+  float *fproj, *bg, *part_o, *part_ml;
+  float2* rope;
+  uint64_t* amax;
+  int *row_argmax, *carry_rec, *status, *tmp_pos, *tmp_argmax;
+};
+
+extern "C" const char* dflow_last_error(void) { return g_err.c_str(); }
+
+extern "C" size_t dflow_packed_bytes(int dtype, int N, int K) {
+  return (size_t)N * (size_t)K * (dtype == DFLOW_BF16 ? 2 : 4);
+}
+
+extern "C" int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, void* out) {
+  if (!w || !out) return fail(DFLOW_EINVAL, "pack: null pointer");
+  if (dtype != DFLOW_F32 && dtype != DFLOW_BF16) return fail(DFLOW_EDTYPE, "pack: dtype %d", dtype);
+  const int KT = dtype == DFLOW_BF16 ? 32 : 16;
+  if (N <= 0 || K <= 0 || N % 16 || K % KT || (gate_up && N % 32))
+    return fail(DFLOW_ESHAPE, "pack: N=%d K=%d must be multiples of 16 and %d", N, K, KT);
+  HIPCHK(launch_pack(dtype == DFLOW_BF16, w, N, K, gate_up, out, stream));
+  return DFLOW_OK;
+}
+
+namespace {
+
+int validate(const dflow_dims* d) {
+  if (!d) return fail(DFLOW_EINVAL, "dims is null");
+  if (d->dtype != DFLOW_F32 && d->dtype != DFLOW_BF16) return fail(DFLOW_EDTYPE, "dtype %d", d->dtype);
+  const int KT = d->dtype == DFLOW_BF16 ? 32 : 16;
+  const int qd = d->n_heads * d->head_dim;
+  if (d->head_dim != 64 && d->head_dim != 128) return fail(DFLOW_ESHAPE, "head_dim %d (64 or 128)", d->head_dim);
+  if (d->n_heads <= 0 || d->n_kv_heads <= 0 || d->n_heads % d->n_kv_heads)
+    return fail(DFLOW_ESHAPE, "heads %d / kv heads %d", d->n_heads, d->n_kv_heads);
+  if (d->d <= 0 || d->d % KT || qd % KT || d->ffn <= 0 || d->ffn % KT || d->relay_hidden <= 0 ||
+      d->relay_hidden % KT)
+    return fail(DFLOW_ESHAPE, "d=%d q_dim=%d ffn=%d relay_hidden=%d must be multiples of %d", d->d, qd, d->ffn,
+                d->relay_hidden, KT);
+  if (d->vocab <= 0 || d->vocab % 16) return fail(DFLOW_ESHAPE, "vocab %d must be a multiple of 16", d->vocab);
+  if (d->n_layers <= 0 || d->n_draft_layers <= 0) return fail(DFLOW_ESHAPE, "layer counts");
+  if (d->n_capture < 1 || d->n_capture > 16) return fail(DFLOW_ESHAPE, "n_capture %d", d->n_capture);
+  for (int i = 0; i < d->n_capture; ++i) {
+    if (d->capture_layers[i] < 0 || d->capture_layers[i] >= d->n_layers ||
+        (i && d->capture_layers[i] <= d->capture_layers[i - 1]))
+      return fail(DFLOW_ESHAPE, "capture_layers must be increasing layer indices");
+  }
+  if (d->block < 2 || d->block > 64) return fail(DFLOW_ESHAPE, "block %d (2..64)", d->block);
+  if (d->max_batch < 1 || d->max_batch * d->block > 128)
+    return fail(DFLOW_ECAPACITY, "max_batch*block = %d exceeds 128 rows", d->max_batch * d->block);
+  if (d->max_rows < d->block || d->max_rows > 128) return fail(DFLOW_ECAPACITY, "max_rows %d (block..128)", d->max_rows);
+  if (d->max_pages < 1 || d->num_pages < 1) return fail(DFLOW_ECAPACITY, "page counts");
+  if (d->carry_window != DFLOW_CARRY_SUFFIX && d->carry_window != DFLOW_CARRY_SUFFIX_TAIL)
+    return fail(DFLOW_EINVAL, "carry_window %d", d->carry_window);
+  return DFLOW_OK;
+}
+
+struct Layout {
+  size_t off[32];
+  size_t total;
+};
+
+// Workspace carve-up; identical for dflow_workspace_bytes and dflow_create.
+Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_groups_out) {
+  const size_t elt = d->dtype == DFLOW_BF16 ? 2 : 4;
+  const int qd = d->n_heads * d->head_dim, kvd = d->n_kv_heads * d->head_dim;
+  const int qkvn = qd + 2 * kvd;
+  const int rows_round = d->max_batch * d->block;
+  const int mmax = rows_round > d->max_rows ? rows_round : d->max_rows;
+  const int G = d->n_heads / d->n_kv_heads;
+  const int nsplit = (d->max_pages * PAGE + SPLIT_KEYS - 1) / SPLIT_KEYS;
+  const int rg_round = (d->block * G + 15) / 16, rg_pre = (d->max_rows * G + 15) / 16;
+  int items = d->max_batch * rg_round;
+  if (rg_pre > items) items = rg_pre;
+  const int lm_groups = (d->vocab / 16 + 3) / 4;
+  Layout L;
+  size_t o = 0;
+  int i = 0;
+  auto add = [&](size_t bytes) { L.off[i++] = o; o += align256(bytes); };
+  add((size_t)mmax * d->d * elt);                      // 0 x
+  add((size_t)mmax * 3 * d->d * elt);                  // 1 xn (also relay u rows)
+  add((size_t)mmax * qkvn * elt);                      // 2 qkv
+  add((size_t)mmax * qd * elt);                        // 3 q
+  add((size_t)mmax * qd * elt);                        // 4 attn
+  add((size_t)mmax * (d->ffn > d->relay_hidden ? d->ffn : d->relay_hidden) * elt);  // 5 act / relay hidden
+  add((size_t)mmax * d->n_capture * d->d * elt);       // 6 hcap
+  add((size_t)rows_round * d->d * elt);                // 7 f (projected features of the last verify)
+  add((size_t)mmax * d->d * elt);                      // 8 fpre (prefill features)
+  add((size_t)mmax * d->d * 4);                        // 9 fproj
+  add((size_t)rows_round * 2 * d->d * 4);              // 10 bg
+  add((size_t)items * d->n_kv_heads * nsplit * 16 * d->head_dim * 4);  // 11 part_o
+  add((size_t)items * d->n_kv_heads * nsplit * 32 * 4);               // 12 part_ml
+  add((size_t)d->max_pages * PAGE * (d->head_dim / 2) * sizeof(float2));  // 13 rope
+  add((size_t)lm_groups * mmax * 8);                   // 14 amax
+  add((size_t)mmax * 4);                               // 15 row_argmax
+  add((size_t)d->max_batch * CARRY_REC * 4);           // 16 carry_rec
+  add(4);                                              // 17 status
+  add((size_t)(d->max_batch + 1) * 4);                 // 18 tmp_pos
+  add((size_t)mmax * 4);                               // 19 tmp_argmax
+  L.total = o;
+  if (nsplit_out) *nsplit_out = nsplit;
+  if (part_items_out) *part_items_out = items;
+  if (lm_groups_out) *lm_groups_out = lm_groups;
+  return L;
+}
+
+}  // namespace
+
+extern "C" size_t dflow_workspace_bytes(const dflow_dims* dims) {
+  if (validate(dims) != DFLOW_OK) return 0;
+  return plan(dims, nullptr, nullptr, nullptr).total;
+}
+
+extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache,
+                            dflow_ctx** out) {
+  int rc = validate(dims);
+  if (rc) return rc;
+  if (!w || !cache || !out) return fail(DFLOW_EINVAL, "create: null argument");
+  const void* req[] = {w->embed, w->final_norm, w->lm_head, w->layers, w->draft_layers, w->draft_final_norm,
+                       w->e_mask, w->w_c, w->g_c, w->relay_w1, w->relay_c1, w->relay_w2, w->relay_c2,
+                       w->relay_ln_g, w->relay_ln_b, cache->k_pool, cache->v_pool, cache->ck_pool, cache->cv_pool,
+                       cache->page_table};
+  for (size_t i = 0; i < sizeof(req) / sizeof(req[0]); ++i)
+    if (!req[i]) return fail(DFLOW_EINVAL, "create: required pointer #%zu is null", i);
+  auto chk_layer = [](const dflow_layer& L) {
+    return L.attn_norm && L.wqkv && L.q_norm && L.k_norm && L.wo && L.ffn_norm && L.wgu && L.wdown;
+  };
+  for (int l = 0; l < dims->n_layers; ++l)
+    if (!chk_layer(w->layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in target layer %d", l);
+  for (int l = 0; l < dims->n_draft_layers; ++l)
+    if (!chk_layer(w->draft_layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in drafter layer %d", l);
+
+  dflow_ctx* c = new dflow_ctx();
+  c->dm = *dims;
+  c->bf = dims->dtype == DFLOW_BF16;
+  c->elt = c->bf ? 2 : 4;
+  c->KT = c->bf ? 32 : 16;
+  c->q_dim = dims->n_heads * dims->head_dim;
+  c->kv_dim = dims->n_kv_heads * dims->head_dim;
+  c->qkv_n = c->q_dim + 2 * c->kv_dim;
+  c->rows_round = dims->max_batch * dims->block;
+  c->mmax = c->rows_round > dims->max_rows ? c->rows_round : dims->max_rows;
+  c->G = dims->n_heads / dims->n_kv_heads;
+  c->w = *w;
+  c->layers.assign(w->layers, w->layers + dims->n_layers);
+  c->dlayers.assign(w->draft_layers, w->draft_layers + dims->n_draft_layers);
+  c->w.layers = c->layers.data();
+  c->w.draft_layers = c->dlayers.data();
+  c->c = *cache;
+  c->pool_layer_elems = (size_t)dims->num_pages * dims->n_kv_heads * PAGE * dims->head_dim;
+
+  Layout L = plan(dims, &c->nsplit, &c->part_items, &c->lm_groups);
+  c->ws_bytes = L.total;
+  hipError_t e = hipMalloc(&c->ws, c->ws_bytes);
+  if (e != hipSuccess) {
+    delete c;
+    return fail(DFLOW_EHIP, "workspace hipMalloc(%zu): %s", L.total, hipGetErrorString(e));
+  }
+  char* b = (char*)c->ws;
+  c->x = b + L.off[0];
+  c->xn = b + L.off[1];
+  c->qkv = b + L.off[2];
+  c->q = b + L.off[3];
+  c->attn = b + L.off[4];
+  c->act = b + L.off[5];
+  c->hcap = b + L.off[6];
+  c->f = b + L.off[7];
+  c->fpre = b + L.off[8];
+  c->fproj = (float*)(b + L.off[9]);
+  c->bg = (float*)(b + L.off[10]);
+  c->part_o = (float*)(b + L.off[11]);
+  c->part_ml = (float*)(b + L.off[12]);
+  c->rope = (float2*)(b + L.off[13]);
+  c->amax = (uint64_t*)(b + L.off[14]);
+  c->row_argmax = (int*)(b + L.off[15]);
+  c->carry_rec = (int*)(b + L.off[16]);
+  c->status = (int*)(b + L.off[17]);
+  c->tmp_pos = (int*)(b + L.off[18]);
+  c->tmp_argmax = (int*)(b + L.off[19]);
+  c->u = c->xn;
+  c->hid = c->act;
+
+  // RoPE table: angle p * theta^(-2i/Dh) evaluated in double
+  const int half = dims->head_dim / 2;
+  const size_t npos = (size_t)dims->max_pages * PAGE;
+  std::vector<float2> tab(npos * half);
+  for (int i = 0; i < half; ++i) {
+    const double inv = std::pow((double)dims->rope_theta, -2.0 * i / dims->head_dim);
+    for (size_t p = 0; p < npos; ++p) {
+      const double a = (double)p * inv;
+      tab[p * half + i] = make_float2((float)std::cos(a), (float)std::sin(a));
+    }
+  }
+  e = hipMemset(c->ws, 0, c->ws_bytes);
+  if (e == hipSuccess) e = hipMemcpy(c->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(c->ws);
+    delete c;
+    return fail(DFLOW_EHIP, "create: %s", hipGetErrorString(e));
+  }
+  *out = c;
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_destroy(dflow_ctx* c) {
+  if (!c) return fail(DFLOW_EINVAL, "destroy: null context");
+  hipError_t e = hipFree(c->ws);
+  delete c;
+  if (e != hipSuccess) return fail(DFLOW_EHIP, "destroy: %s", hipGetErrorString(e));
+  return DFLOW_OK;
+}
+
+// ------------------------------------------------------------------ internals
+namespace {
+
+// Byte offset of packed strip `nt` of a weight with `ktiles` tiles per strip.
+inline const void* strip_ptr(const void* W, int nt, int ktiles) {
+  return (const char*)W + (size_t)nt * ktiles * 1024;
+}
+
+hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, const void* W, int M, int N, int K,
+                void* Y, int ldy, const void* R = nullptr, int ldr = 0, void* Y2 = nullptr, int ldy2 = 0,
+                const void* bias = nullptr, float* logits = nullptr, int ldl = 0) {
+  GemmParams p{};
+  p.A = A;
+  p.lda = lda;
+  p.W = W;
+  p.M = M;
+  p.ntiles = N / 16;
+  p.ktiles = K / c->KT;
+  p.Y = Y;
+  p.ldy = ldy;
+  p.R = R;
+  p.ldr = ldr;
+  p.Y2 = Y2;
+  p.ldy2 = ldy2;
+  p.bias = bias;
+  p.amax = c->amax;
+  p.amax_ld = c->mmax;
+  p.logits = logits;
+  p.ldl = ldl;
+  p.col0 = 0;
+  return launch_gemm(c->bf, epi, p, st);
+}
+
+void* pool_layer(dflow_ctx* c, void* pool, int l) { return (char*)pool + (size_t)l * c->pool_layer_elems * c->elt; }
+
+// Attention of `nseq` sequences x Bq rows over one layer's pools.
+hipError_t attention(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const int* start_pos, const int* page_table,
+                     void* kpool, void* vpool, int causal) {
+  AttnParams a{};
+  a.Q = c->q;
+  a.kpool = kpool;
+  a.vpool = vpool;
+  a.page_table = page_table;
+  a.max_pages = c->dm.max_pages;
+  a.start_pos = start_pos;
+  a.nseq = nseq;
+  a.Bq = Bq;
+  a.Hq = c->dm.n_heads;
+  a.Hkv = c->dm.n_kv_heads;
+  a.Dh = c->dm.head_dim;
+  a.causal = causal;
+  a.nsplit = c->nsplit;
+  a.num_pages = c->dm.num_pages;
+  a.rg = (Bq * c->G + 15) / 16;
+  a.part_o = c->part_o;
+  a.part_ml = c->part_ml;
+  a.out = c->attn;
+  return launch_attention(c->bf, a, st);
+}
+
+// QK-norm + RoPE + KV write for rows of `nseq` x Bq.
+hipError_t qk_rope(dflow_ctx* c, hipStream_t st, const dflow_layer& L, const void* qkv, int ld, int nseq, int Bq,
+                   int nq, const int* start_pos, const int* row_limit, const int* page_table, void* kpool,
+                   void* vpool) {
+  RopeParams r{};
+  r.qkv = qkv;
+  r.ld = ld;
+  r.M = nseq * Bq;
+  r.Bq = Bq;
+  r.nq = nq;
+  r.Hkv = c->dm.n_kv_heads;
+  r.Dh = c->dm.head_dim;
+  r.q_norm = L.q_norm;
+  r.k_norm = L.k_norm;
+  r.rope = c->rope;
+  r.start_pos = start_pos;
+  r.row_limit = row_limit;
+  r.q_out = c->q;
+  r.kpool = kpool;
+  r.vpool = vpool;
+  r.page_table = page_table;
+  r.max_pages = c->dm.max_pages;
+  r.num_pages = c->dm.num_pages;
+  r.status = c->status;
+  r.eps = c->dm.rms_eps;
+  return launch_qk_rope_write(c->bf, r, st);
+}
+
+// One Qwen3-style decoder layer over x (M = nseq*Bq rows) in place.
+hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nseq, int Bq, const int* start_pos,
+                         const int* page_table, void* kpool, void* vpool, int causal, void* capture) {
+  const dflow_dims& d = c->dm;
+  const int M = nseq * Bq;
+  hipError_t e;
+  if ((e = launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, L.attn_norm, d.rms_eps, c->xn, d.d, st))) return e;
+  if ((e = gemm(c, st, EPI_STORE_T, c->xn, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n))) return e;
+  if ((e = qk_rope(c, st, L, c->qkv, c->qkv_n, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool)))
+    return e;
+  if ((e = attention(c, st, nseq, Bq, start_pos, page_table, kpool, vpool, causal))) return e;
+  if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d))) return e;
+  if ((e = launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, L.ffn_norm, d.rms_eps, c->xn, d.d, st))) return e;
+  if ((e = gemm(c, st, EPI_SWIGLU, c->xn, d.d, L.wgu, M, 2 * d.ffn, d.d, c->act, d.ffn))) return e;
+  const int capld = d.n_capture * d.d;
+  if ((e = gemm(c, st, EPI_RESID, c->act, d.ffn, L.wdown, M, d.d, d.ffn, c->x, d.d, c->x, d.d, capture, capld)))
+    return e;
+  return hipSuccess;
+}
+
+// Target forward over block rows already embedded in x; argmax of every row into `argmax_out`.
+hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const int* start_pos,
+                          const int* page_table, int* argmax_out, float* logits, int lm_row0 = 0, int lm_rows = -1) {
+  const dflow_dims& d = c->dm;
+  const int M = nseq * Bq;
+  hipError_t e;
+  int ci = 0;
+  for (int l = 0; l < d.n_layers; ++l) {
+    void* cap = nullptr;
+    if (ci < d.n_capture && d.capture_layers[ci] == l) cap = (char*)c->hcap + (size_t)ci++ * d.d * c->elt;
+    if ((e = decoder_layer(c, st, c->layers[l], nseq, Bq, start_pos, page_table, pool_layer(c, c->c.k_pool, l),
+                           pool_layer(c, c->c.v_pool, l), 1, cap)))
+      return e;
+  }
+  if (!argmax_out) return hipSuccess;
+  // LM head over rows lm_row0 .. lm_row0+lm_rows-1 only
+  if (lm_rows < 0) lm_rows = M;
+  const size_t off = (size_t)lm_row0 * d.d * c->elt;
+  if ((e = launch_rmsnorm(c->bf, false, (char*)c->x + off, d.d, lm_rows, d.d, c->w.final_norm, d.rms_eps, c->xn,
+                          d.d, st)))
+    return e;
+  if ((e = gemm(c, st, EPI_ARGMAX, c->xn, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr,
+                0, nullptr, logits, d.vocab)))
+    return e;
+  return launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, lm_rows, argmax_out, st);
+}
+
+// F = RMSNorm(W_c [captured states]) for M rows -> fout (storage type)
+hipError_t project(dflow_ctx* c, hipStream_t st, int M, void* fout) {
+  const dflow_dims& d = c->dm;
+  hipError_t e;
+  const int K = d.n_capture * d.d;
+  if ((e = gemm(c, st, EPI_STORE_F32, c->hcap, K, c->w.w_c, M, d.d, K, c->fproj, d.d))) return e;
+  return launch_rmsnorm(c->bf, true, c->fproj, d.d, M, d.d, c->w.g_c, d.rms_eps, fout, d.d, st);
+}
+
+// Drafter context K/V of feature rows (nseq x Bq) at start_pos + j for rows j <= row_limit[s].
+hipError_t ctx_append(dflow_ctx* c, hipStream_t st, const void* feat, int nseq, int Bq, const int* start_pos,
+                      const int* row_limit, const int* page_table) {
+  const dflow_dims& d = c->dm;
+  const int M = nseq * Bq;
+  const int kt = d.d / c->KT;
+  hipError_t e;
+  for (int l = 0; l < d.n_draft_layers; ++l) {
+    const dflow_layer& L = c->dlayers[l];
+    const void* wkv = strip_ptr(L.wqkv, c->q_dim / 16, kt);
+    if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, wkv, M, 2 * c->kv_dim, d.d, c->qkv, 2 * c->kv_dim))) return e;
+    if ((e = qk_rope(c, st, L, c->qkv, 2 * c->kv_dim, nseq, Bq, 0, start_pos, row_limit, page_table,
+                     pool_layer(c, c->c.ck_pool, l), pool_layer(c, c->c.cv_pool, l))))
+      return e;
+  }
+  return hipSuccess;
+}
+
+int check_nseq(dflow_ctx* c, int nseq) {
+  if (!c) return fail(DFLOW_EINVAL, "null context");
+  if (nseq < 1 || nseq > c->dm.max_batch) return fail(DFLOW_ECAPACITY, "nseq %d outside 1..%d", nseq, c->dm.max_batch);
+  return DFLOW_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ entry points
+extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len,
+                             int32_t* first_anchor) {
+  if (!c || !tok || !first_anchor) return fail(DFLOW_EINVAL, "prefill: null argument");
+  if (seq < 0 || seq >= c->dm.max_batch) return fail(DFLOW_EINVAL, "prefill: seq %d", seq);
+  if (len < 1) return fail(DFLOW_ESHAPE, "prefill: len %d", len);
+  if ((long long)len + c->dm.block > (long long)c->dm.max_pages * PAGE)
+    return fail(DFLOW_ECAPACITY, "prefill: %d tokens exceed the page table (%d)", len, c->dm.max_pages * PAGE);
+  const dflow_dims& d = c->dm;
+  const int* pt = c->c.page_table + (size_t)seq * d.max_pages;
+  for (int p0 = 0; p0 < len; p0 += d.max_rows) {
+    const int n = (len - p0) < d.max_rows ? (len - p0) : d.max_rows;
+    const bool last = p0 + n >= len;
+    HIPCHK(launch_set_int(c->tmp_pos, p0, st));
+    HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, st));
+    HIPCHK(target_forward(c, st, 1, n, c->tmp_pos, pt, last ? c->tmp_argmax : nullptr, nullptr, n - 1, 1));
+    HIPCHK(project(c, st, n, c->fpre));
+    HIPCHK(ctx_append(c, st, c->fpre, 1, n, c->tmp_pos, nullptr, pt));
+    if (last) HIPCHK(hipMemcpyAsync(first_anchor, c->tmp_argmax, 4, hipMemcpyDeviceToDevice, st));
+  }
+  HIPCHK(launch_fill_u32((uint32_t*)(c->carry_rec + (size_t)seq * CARRY_REC), 0u, CARRY_REC, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* anchor_tok,
+                                 const int32_t* anchor_pos, int carry_on, int32_t* draft_tok, int32_t* block_out,
+                                 float* draft_logits) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!anchor_tok || !anchor_pos || (!draft_tok && !block_out))
+    return fail(DFLOW_EINVAL, "draft_block: null argument");
+  const dflow_dims& d = c->dm;
+  const int B = d.block, M = nseq * B;
+  if (carry_on) {
+    HIPCHK(launch_relay_gather(c->bf, 1, c->carry_rec, c->w.embed, c->f, nseq, B, d.d, d.vocab, c->u, st));
+    HIPCHK(gemm(c, st, EPI_BIAS_SILU, c->u, 3 * d.d, c->w.relay_w1, M, d.relay_hidden, 3 * d.d, c->hid,
+                d.relay_hidden, nullptr, 0, nullptr, 0, c->w.relay_c1));
+    HIPCHK(gemm(c, st, EPI_BIAS_F32, c->hid, d.relay_hidden, c->w.relay_w2, M, 2 * d.d, d.relay_hidden, c->bg,
+                2 * d.d, nullptr, 0, nullptr, 0, c->w.relay_c2));
+  }
+  HIPCHK(launch_relay_input(c->bf, carry_on ? 1 : 0, c->carry_rec, anchor_tok, c->w.embed, c->w.e_mask, c->f, c->bg,
+                            c->w.relay_ln_g, c->w.relay_ln_b, d.ln_eps, nseq, B, d.d, d.vocab, c->x, c->status, st));
+  for (int l = 0; l < d.n_draft_layers; ++l)
+    HIPCHK(decoder_layer(c, st, c->dlayers[l], nseq, B, anchor_pos, c->c.page_table, pool_layer(c, c->c.ck_pool, l),
+                         pool_layer(c, c->c.cv_pool, l), 0, nullptr));
+  HIPCHK(launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, c->w.draft_final_norm, d.rms_eps, c->xn, d.d, st));
+  HIPCHK(gemm(c, st, EPI_ARGMAX, c->xn, d.d, c->w.lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
+              nullptr, draft_logits, d.vocab));
+  HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, M, c->row_argmax, st));
+  HIPCHK(launch_draft_assemble(c->row_argmax, anchor_tok, nseq, B, draft_tok, block_out, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* block_tok,
+                                  const int32_t* start_pos, int32_t* tgt_argmax, float* logits, void* hcap) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!block_tok || !start_pos || !tgt_argmax) return fail(DFLOW_EINVAL, "verify_block: null argument");
+  const dflow_dims& d = c->dm;
+  const int B = d.block, M = nseq * B;
+  HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, st));
+  HIPCHK(target_forward(c, st, nseq, B, start_pos, c->c.page_table, tgt_argmax, logits));
+  if (hcap)
+    HIPCHK(hipMemcpyAsync(hcap, c->hcap, (size_t)M * d.n_capture * d.d * c->elt, hipMemcpyDeviceToDevice, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_accept_and_carry(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* block_tok,
+                                      const int32_t* tgt_argmax, int32_t* accept_len, int32_t* bonus,
+                                      int32_t* committed, int32_t* n_carry, void* feat) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!block_tok || !tgt_argmax || !accept_len || !committed)
+    return fail(DFLOW_EINVAL, "accept_and_carry: null argument");
+  const dflow_dims& d = c->dm;
+  const int B = d.block, M = nseq * B;
+  HIPCHK(launch_accept(block_tok, tgt_argmax, nseq, B, d.carry_window, accept_len, bonus, committed, n_carry,
+                       c->carry_rec, st));
+  HIPCHK(project(c, st, M, c->f));
+  if (feat) HIPCHK(hipMemcpyAsync(feat, c->f, (size_t)M * d.d * c->elt, hipMemcpyDeviceToDevice, st));
+  return DFLOW_OK;
+}
+
+extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* accept_len, int32_t* seq_len) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!accept_len || !seq_len) return fail(DFLOW_EINVAL, "kv_commit: null argument");
+  HIPCHK(ctx_append(c, st, c->f, nseq, c->dm.block, seq_len, accept_len, c->c.page_table));
+  HIPCHK(launch_commit(accept_len, nseq, seq_len, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_bench_force_drafts(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* traj,
+                                        int traj_stride, int traj_len, const int8_t* mode, const int32_t* tok,
+                                        const int32_t* anchor, const int32_t* start_pos, int32_t* block_tok) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!traj || !mode || !tok || !anchor || !start_pos || !block_tok)
+    return fail(DFLOW_EINVAL, "force_drafts: null argument");
+  if (traj_len > traj_stride || traj_len < 1) return fail(DFLOW_ESHAPE, "force_drafts: traj_len %d stride %d",
+                                                          traj_len, traj_stride);
+  HIPCHK(launch_force(traj, traj_stride, traj_len, (const signed char*)mode, tok, anchor, start_pos, nseq,
+                      c->dm.block, c->dm.vocab, block_tok, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_read_status(dflow_ctx* c, hipStream_t st, int32_t* host_status, int clear) {
+  if (!c || !host_status) return fail(DFLOW_EINVAL, "read_status: null argument");
+  HIPCHK(hipStreamSynchronize(st));
+  HIPCHK(hipMemcpy(host_status, c->status, 4, hipMemcpyDeviceToHost));
+  if (clear) HIPCHK(hipMemset(c->status, 0, 4));
+  return DFLOW_OK;
+}

@@ -1,0 +1,109 @@
+// Shared device helpers of the DFlow HIP library (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+namespace dflow {
+
+constexpr int WAVE = 64;
+constexpr int PAGE = 64;          // KV page size in tokens (also the attention sub-chunk)
+constexpr int SPLIT_KEYS = 256;   // keys per attention split, at fixed absolute positions
+
+// ------------------------------------------------------------------ bf16 storage
+struct bf16 { uint16_t u; };
+
+__device__ __host__ inline float bf2f(uint16_t u) {
+  union { uint32_t i; float f; } c;
+  c.i = (uint32_t)u << 16;
+  return c.f;
+}
+// round-to-nearest-even; values here are finite
+__device__ __host__ inline uint16_t f2bf(float f) {
+  union { uint32_t i; float f; } c;
+  c.f = f;
+  uint32_t u = c.i;
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Storage-type traits.  A "lane fragment" is the 16 bytes one lane feeds to
+// the matrix core per tile: 8 bf16 or 4 fp32 consecutive k values.
+template <typename T> struct TT;
+template <> struct TT<bf16> {
+  static constexpr int KL = 8;          // elements per 16-byte lane fragment
+  static constexpr int KT = 32;         // k extent of a 16x(KT) weight tile
+  __device__ static inline float ld(const bf16* p, size_t i) { return bf2f(p[i].u); }
+  __device__ static inline void st(bf16* p, size_t i, float v) { p[i].u = f2bf(v); }
+  __device__ static inline float rnd(float v) { return bf2f(f2bf(v)); }
+};
+template <> struct TT<float> {
+  static constexpr int KL = 4;
+  static constexpr int KT = 16;
+  __device__ static inline float ld(const float* p, size_t i) { return p[i]; }
+  __device__ static inline void st(float* p, size_t i, float v) { p[i] = v; }
+  __device__ static inline float rnd(float v) { return v; }
+};
+
+// acc(16x16) += A(16 x k) * B(k x 16) over one 16-byte lane fragment pair.
+// Lane l supplies row (l%16) of A and column (l%16) of B, k-group l/16.
+__device__ inline f32x4_t mma_frag(bf16, const uint4& a, const uint4& b, f32x4_t acc) {
+  bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
+  bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+}
+__device__ inline f32x4_t mma_frag(float, const uint4& a, const uint4& b, f32x4_t acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  return acc;
+}
+
+// Wave reductions (64 lanes)
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide sum with a fixed combination order (wave partials summed 0..n-1).
+__device__ inline float block_sum(float v, float* sh /* >= 32 floats */) {
+  v = wave_sum(v);
+  const int w = threadIdx.x / WAVE, nw = blockDim.x / WAVE;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  float s = 0.f;
+  for (int i = 0; i < nw; ++i) s += sh[i];
+  return s;
+}
+
+// Device status bits (OR-ed by kernels; read by the host after a sync)
+enum : int {
+  ST_BAD_TOKEN = 1,        // token id outside [0, V)
+  ST_CAPACITY = 2,         // a position beyond the sequence's page table
+  ST_BAD_PAGE = 4,         // page id outside the pool
+};
+__device__ inline void set_status(int* status, int bit) { atomicOr(status, bit); }
+
+__device__ inline float silu(float x) { return x / (1.f + __expf(-x)); }
+
+// ordered 64-bit key: larger float first, then lower index
+__device__ inline uint64_t argmax_key(float v, int idx) {
+  uint32_t u = __float_as_uint(v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx);
+}
+__device__ inline int argmax_key_index(uint64_t k) { return (int)(0xFFFFFFFFu - (uint32_t)(k & 0xFFFFFFFFu)); }
+
+}  // namespace dflow

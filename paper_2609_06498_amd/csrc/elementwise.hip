@@ -1,0 +1,364 @@
+// Row-wise and integer kernels of the DFlow round: embedding gather, RMSNorm,
+// fused QK-norm + RoPE + paged KV write, relay gather / reject-conditioned
+// input build, acceptance scan, argmax reduction, KV commit and the
+// measurement-only forced-draft builder.
+#include "common.h"
+#include "kernels.h"
+
+namespace dflow {
+
+// ---------------------------------------------------------------- embedding
+template <typename T>
+__global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, int* status) {
+  const int row = blockIdx.x;
+  int t = tok[row];
+  if (t < 0 || t >= V) {
+    if (threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
+    for (int i = threadIdx.x; i < d; i += blockDim.x) TT<T>::st(out, (size_t)row * d + i, 0.f);
+    return;
+  }
+  for (int i = threadIdx.x; i < d; i += blockDim.x) out[(size_t)row * d + i] = E[(size_t)t * d + i];
+}
+
+hipError_t launch_embed(bool isbf, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
+                        hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (isbf)
+    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(256), 0, s, tok, (const bf16*)E, V, d, (bf16*)out, status);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, tok, (const float*)E, V, d, (float*)out,
+                       status);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- RMSNorm
+template <typename T, typename TI>
+__global__ void rmsnorm_kernel(const TI* x, int ldx, int d, const T* g, float eps, T* out, int ldo) {
+  __shared__ float sh[32];
+  const int row = blockIdx.x;
+  const TI* xr = x + (size_t)row * ldx;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = TT<TI>::ld(xr, i);
+    ss += v * v;
+  }
+  ss = block_sum(ss, sh);
+  const float r = rsqrtf(ss / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    TT<T>::st(out, (size_t)row * ldo + i, TT<TI>::ld(xr, i) * r * TT<T>::ld(g, i));
+}
+
+hipError_t launch_rmsnorm(bool isbf, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
+                          void* out, int ldo, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (isbf && in_f32)
+    hipLaunchKernelGGL((rmsnorm_kernel<bf16, float>), dim3(M), dim3(256), 0, s, (const float*)x, ldx, d,
+                       (const bf16*)g, eps, (bf16*)out, ldo);
+  else if (isbf)
+    hipLaunchKernelGGL((rmsnorm_kernel<bf16, bf16>), dim3(M), dim3(256), 0, s, (const bf16*)x, ldx, d,
+                       (const bf16*)g, eps, (bf16*)out, ldo);
+  else
+    hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(M), dim3(256), 0, s, (const float*)x, ldx, d,
+                       (const float*)g, eps, (float*)out, ldo);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- QK-norm + RoPE + KV write
+// Block (row, head): head < nq is a query head, then Hkv key heads, then Hkv value heads.
+template <typename T>
+__global__ void qk_rope_kernel(RopeParams p) {
+  const int row = blockIdx.x;
+  const int h = blockIdx.y;
+  const int s = row / p.Bq, j = row - s * p.Bq;
+  if (p.row_limit && j > p.row_limit[s]) return;
+  const int Dh = p.Dh, half = Dh / 2;
+  const int pos = p.start_pos[s] + j;
+  const T* src = reinterpret_cast<const T*>(p.qkv) + (size_t)row * p.ld + (size_t)h * Dh;
+  const bool is_q = h < p.nq;
+  const bool is_k = !is_q && h < p.nq + p.Hkv;
+  const int kvh = is_q ? 0 : (is_k ? h - p.nq : h - p.nq - p.Hkv);
+
+  size_t page_base = 0;
+  const int pidx = pos / PAGE;
+  if (pos < 0 || pidx >= p.max_pages) {      // also bounds the RoPE table
+    if (threadIdx.x == 0) set_status(p.status, ST_CAPACITY);
+    return;
+  }
+  if (!is_q) {
+    const int page = p.page_table[(size_t)s * p.max_pages + pidx];
+    if (page < 0 || page >= p.num_pages) {
+      if (threadIdx.x == 0) set_status(p.status, ST_BAD_PAGE);
+      return;
+    }
+    page_base = ((size_t)page * p.Hkv + kvh) * PAGE * Dh;
+  }
+  const int slot = pos % PAGE;
+  const int i = threadIdx.x;   // pair (i, i + half)
+  if (!is_q && !is_k) {        // value head: transposed page layout
+    T* vp = reinterpret_cast<T*>(p.vpool) + page_base;
+    for (int e = i; e < Dh; e += blockDim.x) vp[(size_t)e * PAGE + slot] = src[e];
+    return;
+  }
+  const T* gain = reinterpret_cast<const T*>(is_q ? p.q_norm : p.k_norm);
+  float x1 = 0.f, x2 = 0.f;
+  if (i < half) { x1 = TT<T>::ld(src, i); x2 = TT<T>::ld(src, i + half); }
+  const float ss = wave_sum(x1 * x1 + x2 * x2);
+  const float r = rsqrtf(ss / (float)Dh + p.eps);
+  if (i < half) {
+    const float y1 = x1 * r * TT<T>::ld(gain, i);
+    const float y2 = x2 * r * TT<T>::ld(gain, i + half);
+    const float2 cs = p.rope[(size_t)pos * half + i];
+    const float o1 = y1 * cs.x - y2 * cs.y;
+    const float o2 = y2 * cs.x + y1 * cs.y;
+    if (is_q) {
+      T* q = reinterpret_cast<T*>(p.q_out) + (size_t)row * p.nq * Dh + (size_t)h * Dh;
+      TT<T>::st(q, i, o1);
+      TT<T>::st(q, i + half, o2);
+    } else {
+      T* kp = reinterpret_cast<T*>(p.kpool) + page_base + (size_t)slot * Dh;
+      TT<T>::st(kp, i, o1);
+      TT<T>::st(kp, i + half, o2);
+    }
+  }
+}
+
+hipError_t launch_qk_rope_write(bool isbf, const RopeParams& p, hipStream_t s) {
+  if (p.M <= 0) return hipSuccess;
+  if (p.Dh > 128 || (p.Dh & 1)) return hipErrorInvalidValue;
+  dim3 grid(p.M, p.nq + 2 * p.Hkv);
+  if (isbf) hipLaunchKernelGGL(qk_rope_kernel<bf16>, grid, dim3(64), 0, s, p);
+  else hipLaunchKernelGGL(qk_rope_kernel<float>, grid, dim3(64), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- argmax
+__global__ void argmax_reduce_kernel(const uint64_t* amax, int groups, int ld, int* out) {
+  __shared__ uint64_t sh[256];
+  const int row = blockIdx.x;
+  uint64_t best = 0;
+  for (int g = threadIdx.x; g < groups; g += blockDim.x) {
+    const uint64_t k = amax[(size_t)g * ld + row];
+    best = k > best ? k : best;
+  }
+  sh[threadIdx.x] = best;
+  __syncthreads();
+  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
+    if (threadIdx.x < w) sh[threadIdx.x] = sh[threadIdx.x + w] > sh[threadIdx.x] ? sh[threadIdx.x + w] : sh[threadIdx.x];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[row] = argmax_key_index(sh[0]);
+}
+
+hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int ld, int M, int* out, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(M), dim3(256), 0, s, amax, groups, ld, out);
+  return hipGetLastError();
+}
+
+// draft_tok[s][j-1] = argmax of block row j (j = 1..B-1); block_out = [anchor, drafts]
+__global__ void draft_assemble_kernel(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
+                                      int* block_out) {
+  const int s = blockIdx.x;
+  for (int j = threadIdx.x; j < B; j += blockDim.x) {
+    if (j == 0) {
+      if (block_out) block_out[(size_t)s * B] = anchor[s];
+    } else {
+      const int t = row_argmax[(size_t)s * B + j];
+      if (draft_tok) draft_tok[(size_t)s * (B - 1) + j - 1] = t;
+      if (block_out) block_out[(size_t)s * B + j] = t;
+    }
+  }
+}
+
+hipError_t launch_draft_assemble(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
+                                 int* block_out, hipStream_t s) {
+  hipLaunchKernelGGL(draft_assemble_kernel, dim3(nseq), dim3(64), 0, s, row_argmax, anchor, nseq, B, draft_tok,
+                     block_out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- acceptance scan
+// a = number of leading drafts d_i (block index i) equal to the target argmax of row i-1;
+// bonus = argmax of row a; committed = d_1..d_a, bonus (rest -1).
+// The carried rows are a+1 .. a+n, placed at next-round block indices 1..n.
+__global__ void accept_kernel(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
+                              int* bonus, int* committed, int* n_carry, int* carry_rec) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= nseq) return;
+  const int K = B - 1;
+  const int* blk = block + (size_t)s * B;
+  const int* gs = g + (size_t)s * B;
+  int a = 0;
+  while (a < K && blk[a + 1] == gs[a]) ++a;
+  const int b = gs[a];
+  for (int j = 0; j < B; ++j) committed[(size_t)s * B + j] = j < a ? blk[j + 1] : (j == a ? b : -1);
+  int n = carry_window == 0 ? K - 1 - a : K - a;
+  if (n < 0) n = 0;
+  accept_len[s] = a;
+  if (bonus) bonus[s] = b;
+  if (n_carry) n_carry[s] = n;
+  int* rec = carry_rec + (size_t)s * CARRY_REC;
+  rec[0] = n;
+  rec[1] = a + 1;
+  rec[2] = b;
+  rec[3] = a < K ? blk[a + 1] : -1;
+}
+
+hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
+                         int* bonus, int* committed, int* n_carry, int* carry_rec, hipStream_t s) {
+  hipLaunchKernelGGL(accept_kernel, dim3((nseq + 63) / 64), dim3(64), 0, s, block, g, nseq, B, carry_window,
+                     accept_len, bonus, committed, n_carry, carry_rec);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- relay
+// u[s*B + i] = [E(b); E(y_rej); f[s*B + src + i - 1]] for relayed rows 1..n, else 0.
+template <typename T>
+__global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, const T* f, int B, int d, int V, T* u) {
+  const int row = blockIdx.x;
+  const int s = row / B, i = row - s * B;
+  const int* r = rec + (size_t)s * CARRY_REC;
+  const bool valid = carry_on && i >= 1 && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B &&
+                     r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
+  T* ur = u + (size_t)row * 3 * d;
+  if (!valid) {
+    for (int e = threadIdx.x; e < 3 * d; e += blockDim.x) TT<T>::st(ur, e, 0.f);
+    return;
+  }
+  const T* eb = E + (size_t)r[2] * d;
+  const T* ey = E + (size_t)r[3] * d;
+  const T* h = f + ((size_t)s * B + r[1] + i - 1) * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    ur[e] = eb[e];
+    ur[d + e] = ey[e];
+    ur[2 * d + e] = h[e];
+  }
+}
+
+hipError_t launch_relay_gather(bool isbf, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
+                               int B, int d, int V, void* u, hipStream_t s) {
+  if (isbf)
+    hipLaunchKernelGGL(relay_gather_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec,
+                       (const bf16*)E, (const bf16*)f, B, d, V, (bf16*)u);
+  else
+    hipLaunchKernelGGL(relay_gather_kernel<float>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec,
+                       (const float*)E, (const float*)f, B, d, V, (float*)u);
+  return hipGetLastError();
+}
+
+// x[s*B + 0] = E(anchor); relayed rows: E_mask + beta * LN(h) + gamma; others E_mask.
+template <typename T>
+__global__ void relay_input_kernel(int carry_on, const int* rec, const int* anchor, const T* E, const T* e_mask,
+                                   const T* f, const float* bg, const T* ln_g, const T* ln_b, float ln_eps, int B,
+                                   int d, int V, T* x, int* status) {
+  __shared__ float sh[32];
+  const int row = blockIdx.x;
+  const int s = row / B, i = row - s * B;
+  T* xr = x + (size_t)row * d;
+  if (i == 0) {
+    const int t = anchor[s];
+    if (t < 0 || t >= V) {
+      if (threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
+      for (int e = threadIdx.x; e < d; e += blockDim.x) TT<T>::st(xr, e, 0.f);
+      return;
+    }
+    for (int e = threadIdx.x; e < d; e += blockDim.x) xr[e] = E[(size_t)t * d + e];
+    return;
+  }
+  const int* r = rec + (size_t)s * CARRY_REC;
+  const bool valid = carry_on && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B && r[2] >= 0 &&
+                     r[2] < V && r[3] >= 0 && r[3] < V;
+  if (!valid) {
+    for (int e = threadIdx.x; e < d; e += blockDim.x) xr[e] = e_mask[e];
+    return;
+  }
+  const T* h = f + ((size_t)s * B + r[1] + i - 1) * d;
+  float sm = 0.f;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) sm += TT<T>::ld(h, e);
+  const float mu = block_sum(sm, sh) / (float)d;
+  float sv = 0.f;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    const float c = TT<T>::ld(h, e) - mu;
+    sv += c * c;
+  }
+  const float var = block_sum(sv, sh) / (float)d;
+  const float rs = rsqrtf(var + ln_eps);
+  const float* bgr = bg + (size_t)row * 2 * d;
+  for (int e = threadIdx.x; e < d; e += blockDim.x) {
+    const float ln = (TT<T>::ld(h, e) - mu) * rs * TT<T>::ld(ln_g, e) + TT<T>::ld(ln_b, e);
+    TT<T>::st(xr, e, TT<T>::ld(e_mask, e) + bgr[e] * ln + bgr[d + e]);
+  }
+}
+
+hipError_t launch_relay_input(bool isbf, int carry_on, const int* carry_rec, const int* anchor, const void* E,
+                              const void* e_mask, const void* f, const float* bg, const void* ln_g,
+                              const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
+                              hipStream_t s) {
+  if (isbf)
+    hipLaunchKernelGGL(relay_input_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
+                       (const bf16*)E, (const bf16*)e_mask, (const bf16*)f, bg, (const bf16*)ln_g,
+                       (const bf16*)ln_b, ln_eps, B, d, V, (bf16*)x, status);
+  else
+    hipLaunchKernelGGL(relay_input_kernel<float>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
+                       (const float*)E, (const float*)e_mask, (const float*)f, bg, (const float*)ln_g,
+                       (const float*)ln_b, ln_eps, B, d, V, (float*)x, status);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- commit
+__global__ void commit_kernel(const int* accept_len, int nseq, int* seq_len) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < nseq) seq_len[s] += accept_len[s] + 1;
+}
+
+hipError_t launch_commit(const int* accept_len, int nseq, int* seq_len, hipStream_t s) {
+  hipLaunchKernelGGL(commit_kernel, dim3((nseq + 63) / 64), dim3(64), 0, s, accept_len, nseq, seq_len);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- forced drafts (measurement only)
+__global__ void force_kernel(const int* traj, int stride, int traj_len, const signed char* mode, const int* tok,
+                             const int* anchor, const int* start_pos, int B, int V, int* block_tok) {
+  const int s = blockIdx.x;
+  const int t = start_pos[s];
+  for (int j = threadIdx.x; j < B; j += blockDim.x) {
+    int v;
+    const int m = mode[(size_t)s * B + j];
+    const int u = tok[(size_t)s * B + j];
+    const int p = t + j;
+    const int tv = (p >= 0 && p < traj_len) ? traj[(size_t)s * stride + p] : 0;
+    if (j == 0) v = anchor[s];
+    else if (m == 1) v = tv;
+    else if (m == 2) v = (int)(((long long)tv + 1 + u) % V);
+    else v = u;
+    block_tok[(size_t)s * B + j] = v;
+  }
+}
+
+hipError_t launch_force(const int* traj, int traj_stride, int traj_len, const signed char* mode, const int* tok,
+                        const int* anchor, const int* start_pos, int nseq, int B, int V, int* block_tok,
+                        hipStream_t s) {
+  hipLaunchKernelGGL(force_kernel, dim3(nseq), dim3(64), 0, s, traj, traj_stride, traj_len, mode, tok, anchor,
+                     start_pos, B, V, block_tok);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- small utilities
+__global__ void set_int_kernel(int* dst, int v) { *dst = v; }
+hipError_t launch_set_int(int* dst, int value, hipStream_t s) {
+  hipLaunchKernelGGL(set_int_kernel, dim3(1), dim3(1), 0, s, dst, value);
+  return hipGetLastError();
+}
+__global__ void fill_u32_kernel(uint32_t* dst, uint32_t v, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = v;
+}
+hipError_t launch_fill_u32(uint32_t* dst, uint32_t value, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)blocks), dim3(256), 0, s, dst, value, n);
+  return hipGetLastError();
+}
+
+}  // namespace dflow

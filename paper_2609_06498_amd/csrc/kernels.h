@@ -1,0 +1,108 @@
+// Internal launch interface between the C-ABI layer and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dflow {
+
+enum Epi : int {
+  EPI_STORE_T = 0,   // Y = acc                       (storage type)
+  EPI_STORE_F32,     // Y = acc                       (fp32)
+  EPI_RESID,         // Y = R + acc; optional copy Y2 (storage type)
+  EPI_SWIGLU,        // Y = silu(gate) * up           (gate/up tiles interleaved)
+  EPI_BIAS_SILU,     // Y = silu(acc + bias)          (storage type)
+  EPI_BIAS_F32,      // Y = acc + bias                (fp32)
+  EPI_ARGMAX,        // per-row best (value, lowest index) over the group's columns
+  EPI_COUNT
+};
+
+struct GemmParams {
+  const void* A; int lda;           // activations [M, lda], storage type
+  const void* W;                    // packed weight tiles of this column range
+  int M, ntiles, ktiles;            // ntiles = N/16 of the range, ktiles = K/KT
+  void* Y; int ldy;
+  const void* R; int ldr;
+  void* Y2; int ldy2;
+  const void* bias;
+  uint64_t* amax; int amax_ld;      // [groups][amax_ld] argmax keys
+  float* logits; int ldl;           // optional fp32 logits
+  int col0;                         // first output column of this range (argmax indices, bias)
+};
+
+struct GemmShape { int ng; int waves; int groups; };
+GemmShape gemm_shape(int ntiles, int ktiles, int epi);
+hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
+hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, void* out, hipStream_t s);
+
+}  // namespace dflow
+
+namespace dflow {
+
+// Paged KV layout (per layer pool):
+//   K: [page][kv_head][slot 0..63][Dh]      (key rows contiguous)
+//   V: [page][kv_head][Dh][slot 0..63]      (transposed: keys contiguous per channel)
+struct AttnParams {
+  const void* Q;             // [nseq*Bq, Hq*Dh] storage type, after QK-norm + RoPE
+  const void* kpool;
+  const void* vpool;
+  const int* page_table;     // [nseq][max_pages]
+  int max_pages;
+  const int* start_pos;      // [nseq] absolute position of block row 0
+  int nseq, Bq, Hq, Hkv, Dh;
+  int causal;                // 1: row j sees keys <= start+j; 0: all keys < start+Bq
+  int nsplit;                // split slots per sequence (upper bound)
+  int num_pages;             // pages per layer pool (page ids are checked)
+  int rg;                    // 16-row groups per (seq, kv head)
+  float* part_o;             // [nseq][Hkv][rg][nsplit][16][Dh]
+  float* part_ml;            // [nseq][Hkv][rg][nsplit][16][2]
+  void* out;                 // [nseq*Bq, Hq*Dh] storage type
+};
+hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
+
+}  // namespace dflow
+
+namespace dflow {
+
+struct RopeParams {
+  const void* qkv; int ld;        // rows: [q heads (nq)][k heads][v heads] x Dh, storage type
+  int M, Bq;                      // rows, rows per sequence
+  int nq, Hkv, Dh;                // nq = query heads present (0 for context rows)
+  const void* q_norm;             // [Dh]
+  const void* k_norm;             // [Dh]
+  const float2* rope;             // [max_pos][Dh/2] (cos, sin)
+  const int* start_pos;           // [nseq] position of row 0 of each sequence
+  const int* row_limit;           // nullable [nseq]: only rows j <= row_limit[s] are written
+  void* q_out;                    // [M, nq*Dh]
+  void* kpool; void* vpool;       // this layer's pools
+  const int* page_table; int max_pages; int num_pages;
+  int* status;
+  float eps;
+};
+
+hipError_t launch_embed(bool bf16, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
+                        hipStream_t s);
+hipError_t launch_rmsnorm(bool bf16, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
+                          void* out, int ldo, hipStream_t s);
+hipError_t launch_qk_rope_write(bool bf16, const RopeParams& p, hipStream_t s);
+hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int ld, int M, int* out, hipStream_t s);
+hipError_t launch_draft_assemble(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
+                                 int* block_out, hipStream_t s);
+hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
+                         int* bonus, int* committed, int* n_carry, int* carry_rec, hipStream_t s);
+hipError_t launch_relay_gather(bool bf16, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
+                               int B, int d, int V, void* u, hipStream_t s);
+hipError_t launch_relay_input(bool bf16, int carry_on, const int* carry_rec, const int* anchor, const void* E,
+                              const void* e_mask, const void* f, const float* bg, const void* ln_g,
+                              const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
+                              hipStream_t s);
+hipError_t launch_commit(const int* accept_len, int nseq, int* seq_len, hipStream_t s);
+hipError_t launch_force(const int* traj, int traj_stride, int traj_len, const signed char* mode, const int* tok,
+                        const int* anchor, const int* start_pos, int nseq, int B, int V, int* block_tok,
+                        hipStream_t s);
+hipError_t launch_set_int(int* dst, int value, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* dst, uint32_t value, size_t n, hipStream_t s);
+
+// carry record per sequence: [n_carry, first source row, bonus, first rejected proposal]
+constexpr int CARRY_REC = 4;
+
+}  // namespace dflow

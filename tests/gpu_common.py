@@ -1,0 +1,31 @@
+"""Helpers shared by the GPU tests: build a runtime and an oracle on the same
+seeded inputs, and numeric comparison utilities."""
+import numpy as np
+
+from workload import get_config
+from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_rows(x, ref):
+    x = np.asarray(x, np.float64).reshape(ref.shape[0], -1)
+    ref = np.asarray(ref, np.float64).reshape(ref.shape[0], -1)
+    return np.linalg.norm(x - ref, axis=1) / np.maximum(np.linalg.norm(ref, axis=1), 1e-30)
+
+
+def margin_rel(logits):
+    """(top1 - top2) / max|l| per row."""
+    l = np.asarray(logits, np.float64)
+    part = np.partition(l, -2, axis=-1)
+    return (part[..., -1] - part[..., -2]) / np.abs(l).max(axis=-1)
+
+
+def bf16_bits(t):
+    """torch int16 bit patterns -> float32 numpy."""
+    a = t.cpu().numpy().view(np.uint16).astype(np.uint32) << 16
+    return a.view(np.float32)
+
+
+def dev_values(t, dtype):
+    return bf16_bits(t) if dtype == "bf16" else t.cpu().numpy()

@@ -1,0 +1,71 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/dflow.h, and host-side validation reports errors before
+any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "dflow.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(?:int|size_t|const char\*)\s+(\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_06498_amd.runtime import library_path, load_library
+    if not os.path.exists(library_path()):
+        pytest.skip("libdflow.so not built")
+    return load_library()
+
+
+def test_header_declares_round_calls():
+    names = _declared()
+    for n in ("dflow_verify_block", "dflow_accept_and_carry", "dflow_draft_block", "kv_commit"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for n in _declared():
+        assert hasattr(lib, n), n
+
+
+def test_binding_covers_header():
+    from paper_2609_06498_amd.runtime import EXPORTS
+    assert sorted(EXPORTS) == _declared()
+
+
+def test_validation_errors_without_device(lib):
+    from paper_2609_06498_amd.runtime import Dims
+    d = Dims()
+    d.dtype = 7
+    assert lib.dflow_workspace_bytes(ctypes.byref(d)) == 0
+    assert "dtype" in lib.dflow_last_error().decode()
+    d.dtype = 1
+    d.d, d.n_layers, d.n_heads, d.n_kv_heads, d.head_dim = 512, 2, 8, 2, 96
+    assert lib.dflow_workspace_bytes(ctypes.byref(d)) == 0
+    assert "head_dim" in lib.dflow_last_error().decode()
+    assert lib.dflow_pack_linear(None, 1, None, 16, 32, 0, None) == -1
+    assert lib.dflow_pack_linear(None, 1, ctypes.c_void_p(16), 16, 48, 0, ctypes.c_void_p(16)) == -2
+    assert lib.dflow_create(None, None, None, None) == -1
+    assert lib.dflow_packed_bytes(1, 32, 64) == 32 * 64 * 2
+    assert lib.dflow_packed_bytes(0, 32, 64) == 32 * 64 * 4
+
+
+def test_workspace_bytes_for_8b_shape(lib):
+    from paper_2609_06498_amd.runtime import Dims
+    d = Dims()
+    d.dtype, d.d, d.n_layers, d.n_heads, d.n_kv_heads, d.head_dim = 1, 4096, 36, 32, 8, 128
+    d.ffn, d.vocab, d.n_draft_layers, d.n_capture = 12288, 151936, 5, 5
+    for i, l in enumerate((0, 8, 17, 26, 35)):
+        d.capture_layers[i] = l
+    d.relay_hidden, d.block, d.max_batch, d.max_rows = 4096, 16, 1, 128
+    d.max_pages, d.num_pages, d.carry_window = 100, 100, 0
+    d.rope_theta, d.rms_eps, d.ln_eps = 1e6, 1e-6, 1e-5
+    n = lib.dflow_workspace_bytes(ctypes.byref(d))
+    assert 0 < n < 1 << 30, (n, lib.dflow_last_error())

@@ -103,12 +103,12 @@ CONFIGS = {
     # multiple of the 64-column group, vocab 5008), real head_dim 128, GQA 4,
     # three sequences with ragged contexts spanning several attention chunks.
     "small-bf16": Workload("small-bf16",
-                           ModelDims("bf16", 512, 3, 8, 2, 128, 1360, 5008, 2, (0, 1, 2)),
+                           ModelDims("bf16", 512, 3, 8, 2, 128, 1376, 5008, 2, (0, 1, 2)),
                            block=16, batch=3, ctx=(40, 520), rounds=6,
                            schedule="geometric", sched_param=4.0,
                            description="3-layer d=512 bf16, V=5008, b=3 ragged ctx, B=16"),
     "small-f32": Workload("small-f32",
-                          ModelDims("f32", 512, 3, 8, 2, 128, 1360, 5008, 2, (0, 1, 2)),
+                          ModelDims("f32", 512, 3, 8, 2, 128, 1376, 5008, 2, (0, 1, 2)),
                           block=16, batch=3, ctx=(40, 520), rounds=6,
                           schedule="geometric", sched_param=4.0,
                           description="fp32 twin of small-bf16"),
