@@ -1,0 +1,263 @@
+"""Benchmark of the DFlow round on one MI355X.
+
+A step is one speculative round over the batch: dflow_draft_block (relay +
+drafter), forced-draft construction, dflow_verify_block, dflow_accept_and_carry
+and kv_commit.  The drafter runs in full every round; the block sent to
+verification is forced from the target's own greedy trajectory with a seeded
+geometric acceptance schedule, because a random-init drafter accepts almost
+nothing.  The trajectory is produced beforehand on the GPU by junk-draft
+rounds through the same kernels.  Inputs (weights, KV cache, trajectory,
+schedule) are resident in HBM before the timed region starts.
+
+Prints one JSON line (see README of the metric in the design doc).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "committed tokens/s + ms/round, Qwen3-8B-shape B=16; % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="qwen3-8b")
+    ap.add_argument("--carry", choices=["on", "off"], default="on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--cpu-sample-ctx", type=int, default=48)
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def gemm_bytes(rt, nseq):
+    """Algorithmic bytes of every weight-streaming GEMM launch of one round:
+    each weight byte once, the A operand once, the output once."""
+    dm, B = rt.dims, rt.block
+    elt = 2 if dm.dtype == "bf16" else 4
+    M = nseq * B
+    d, F, V, qd, kvd = dm.d, dm.ffn, dm.vocab, dm.q_dim, dm.kv_dim
+    qkv = qd + 2 * kvd
+
+    def g(N, K, out_elt=elt, n_out=None):
+        return N * K * elt + M * K * elt + M * (N if n_out is None else n_out) * out_elt
+
+    layer = g(qkv, d) + g(d, qd) + g(2 * F, d, n_out=F) + g(d, F)
+    verify = dm.n_layers * layer + g(V, d, 0)
+    draft = dm.n_draft_layers * layer + g(V, d, 0) + g(dm.d_h, 3 * d) + g(2 * d, dm.d_h, 4)
+    accept = g(d, dm.m * d, 4)
+    commit = dm.n_draft_layers * g(2 * kvd, d)
+    launches = (dm.n_layers + dm.n_draft_layers) * 4 + 2 + 2 + 1 + dm.n_draft_layers
+    return verify + draft + accept + commit, launches
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the DFlow round is a single-GPU "
+              f"data-parallel step; multi-GPU sharding is described in DESIGN.md but not run.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_06498_amd import Runtime
+    from paper_2609_06498_amd.session import Session
+    from workload import get_config
+    from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
+
+    wl = get_config(args.workload)
+    dm, B, b = wl.dims, wl.block, wl.batch
+    K = args.steps
+    log(f"workload {wl.name}: {wl.description}; steps {K} warmup {args.warmup}")
+    t = time.time()
+    w = make_weights(dm, wl.seed_w)
+    log(f"weights generated in {time.time() - t:.1f}s")
+    prompts = make_prompts(wl)
+    sched = make_schedule(wl, max(K, args.warmup))
+    need = trajectory_length_needed(wl, sched)
+    max_ctx = max(need) + B
+    t = time.time()
+    rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
+    torch.cuda.synchronize()
+    log(f"runtime created (upload + pack) in {time.time() - t:.1f}s")
+    if args.no_cpu_baseline:
+        del w
+    sess = Session(rt, b)
+
+    # ---- target trajectory T*: junk-draft rounds through the same kernels
+    t = time.time()
+    sess.prefill(prompts)
+    torch.cuda.synchronize()
+    P = [len(p) for p in prompts]
+    first_anchor = sess.anchor.clone()
+    L = max(need)
+    traj = torch.zeros(b, L, dtype=torch.int32, device="cuda")
+    for s in range(b):
+        traj[s, :P[s]] = torch.from_numpy(prompts[s]).cuda()
+    zmode = torch.zeros(b, B, dtype=torch.int8, device="cuda")
+    ztok = torch.zeros(b, B, dtype=torch.int32, device="cuda")
+    hist_com, hist_acc, hist_pos = [], [], []
+    done = 0
+    while done < max(n - p for n, p in zip(need, P)):
+        pos = sess.seq_len.clone()
+        rt.force_drafts(b, traj, 1, zmode, ztok, sess.anchor, sess.seq_len, sess.block)
+        rt.verify_block(b, sess.block, sess.seq_len, sess.tgt)
+        rt.accept_and_carry(b, sess.block, sess.tgt, sess.accept, sess.anchor, sess.committed, sess.n_carry)
+        rt.kv_commit(b, sess.accept, sess.seq_len)
+        hist_com.append(sess.committed.clone())
+        hist_acc.append(sess.accept.clone())
+        hist_pos.append(pos)
+        if len(hist_com) % 64 == 0:
+            done = int((sess.seq_len.cpu().numpy() - np.array(P)).min())
+    torch.cuda.synchronize()
+    traj_h = np.zeros((b, L), np.int32)
+    fa = first_anchor.cpu().numpy()
+    for s in range(b):
+        traj_h[s, :P[s]] = prompts[s]
+        traj_h[s, P[s]] = fa[s]
+    for com, acc, pos in zip(hist_com, hist_acc, hist_pos):
+        com, acc, pos = com.cpu().numpy(), acc.cpu().numpy(), pos.cpu().numpy()
+        for s in range(b):
+            for j in range(acc[s] + 1):
+                p = pos[s] + 1 + j
+                if p < L:
+                    traj_h[s, p] = com[s, j]
+    traj.copy_(torch.from_numpy(traj_h))
+    log(f"trajectory ({len(hist_com)} junk rounds) in {time.time() - t:.1f}s")
+    assert rt.status() == 0
+
+    mode_d = torch.from_numpy(sched["mode"]).cuda()
+    tok_d = torch.from_numpy(sched["tok"]).cuda()
+    carry_on = args.carry == "on"
+
+    def reset():
+        sess.prefill(prompts)
+
+    def run(n):
+        for r in range(n):
+            sess.round(carry_on, force=(traj, L, mode_d[r], tok_d[r]))
+
+    reset()
+    run(args.warmup)
+    torch.cuda.synchronize()
+    reset()
+    torch.cuda.synchronize()
+    len0 = sess.seq_len.cpu().numpy().copy()
+    t0 = time.perf_counter()
+    run(K)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    len1 = sess.seq_len.cpu().numpy()
+    committed = int((len1 - len0).sum())
+    expect = int((sched["accept"][:K] + 1).sum())
+    diverged = committed != expect
+    status = rt.status()
+    tok_s = committed / dt
+    ms_round = dt * 1e3 / K
+    tau = committed / (K * b)
+    log(f"timed {K} rounds: {ms_round:.3f} ms/round, {tok_s:.1f} tok/s, tau {tau:.3f} "
+        f"(schedule {expect / (K * b):.3f}), status {status}")
+
+    # ---- live per-kernel timing with HIP events on the round's stream
+    roofline, kernels = None, None
+    gb, nl = gemm_bytes(rt, b)
+    if not args.no_kernel_timing:
+        kp = min(K, 64)
+        reset()
+        torch.cuda.synchronize()
+        rt.profile(True)
+        run(kp)
+        torch.cuda.synchronize()
+        entries = rt.profile_read()
+        rt.profile(False)
+        gemms = [e for e in entries if e["name"].startswith("gemm")]
+        assert sum(e["launches"] for e in gemms) == kp * nl, (entries, kp, nl)
+        lib_bytes = sum(e["bytes"] for e in gemms)
+        assert abs(lib_bytes - kp * gb) <= 1e-6 * kp * gb, (lib_bytes, kp * gb)
+        kernels = []
+        for e in sorted(entries, key=lambda e: -e["ms"]):
+            avg_us = e["ms"] * 1e3 / e["launches"]
+            k = {"kernel": e["name"], "N": e["N"], "K": e["K"], "M": e["M"], "per_round": e["launches"] / kp,
+                 "avg_us": round(avg_us, 3), "ms_per_round": round(e["ms"] / kp, 4)}
+            if e["bytes"]:
+                k["GB_s"] = round(e["bytes"] / e["launches"] / (avg_us * 1e-6) / 1e9, 1)
+            kernels.append(k)
+        dom = max(gemms, key=lambda e: e["ms"])
+        avg_s = dom["ms"] * 1e-3 / dom["launches"]
+        per_launch = dom["bytes"] / dom["launches"]
+        achieved = per_launch / avg_s / 1e9
+        fam_ms = sum(e["ms"] for e in gemms)
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "kernel": f"{dom['name']} N={dom['N']} K={dom['K']} M={dom['M']}",
+                    "algorithmic_bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_s * 1e6, 3),
+                    "gemm_family_GB_s": round(lib_bytes / (fam_ms * 1e-3) / 1e9, 1),
+                    "gemm_family_ms_per_round": round(fam_ms / kp, 4)}
+        log(f"dominant {roofline['kernel']}: avg {avg_s * 1e6:.2f} us, {achieved:.1f} GB/s; "
+            f"gemm family {roofline['gemm_family_GB_s']} GB/s, {fam_ms / kp:.3f} ms/round")
+        for k in kernels:
+            log(f"  {k}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, w, prompts, tau, args.cpu_sample_ctx)
+
+    out = {"metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+           "warmup": args.warmup, "ms_per_step": round(ms_round, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if dm.dtype == "bf16" else "f32",
+           "data": "synthetic (seeded random-init weights, uniform prompts, forced geometric acceptance)",
+           "config": {"workload": wl.name, "batch": b, "block": B, "ctx": list(wl.ctx), "rounds": K,
+                      "carry": args.carry, "schedule": f"{wl.schedule}({wl.sched_param})",
+                      "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
+                      "parallelism": "single GPU"},
+           "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(wl, w, prompts, tau, ctx_len):
+    """The oracle timed on this host on a bounded sample: one full round
+    (draft + verify + accept/project + commit) of the same model after a
+    short prefill; tokens/s = realised tau of the GPU run / oracle round time."""
+    import threading
+    from oracle import Mode, OracleDFlow, OracleModel
+    dm = wl.dims
+    mode = "bf16" if dm.dtype == "bf16" else "fp32"
+    m = OracleModel(dm, w, Mode(mode), cache=True)
+    o = OracleDFlow(m, wl.block, wl.carry_window)
+    p = prompts[0][:ctx_len]
+    t = time.time()
+    s = o.prefill(p)
+    t_pre = time.time() - t
+    rng = np.random.default_rng(0)
+    o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))  # carry present
+    t = time.perf_counter()
+    o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))
+    t_round = time.perf_counter() - t
+    try:
+        import threadpoolctl
+        info = threadpoolctl.threadpool_info()
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    log(f"oracle: prefill {len(p)} tokens {t_pre:.1f}s, one round {t_round:.2f}s, {threads} BLAS threads")
+    return {"value": round(tau / t_round, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"one {mode} oracle round (draft+verify+accept+commit, relay on) of {wl.name} after a "
+                      f"{len(p)}-token prefill; tokens/s = GPU-realised tau {tau:.3f} / {t_round:.2f} s; "
+                      f"host cpu_count {os.cpu_count()}"}
+
+
+if __name__ == "__main__":
+    main()

@@ -228,6 +228,24 @@ int dflow_bench_force_drafts(dflow_ctx* ctx, hipStream_t stream, int nseq, const
                              int traj_len, const int8_t* mode, const int32_t* tok, const int32_t* anchor,
                              const int32_t* start_pos, int32_t* block_tok);
 
+/* Kernel timing (tracing aid, not part of the method).  While enabled, every
+ * weight-streaming GEMM launch and every attention launch is bracketed by HIP
+ * events recorded on the launch's stream (up to 16384 launches between reads).
+ * dflow_profile_read waits for the recorded events and aggregates them per
+ * kernel class (GEMM epilogue and shape, or attention): summed elapsed
+ * milliseconds, launches and algorithmic bytes (GEMM: each weight, input and
+ * output byte once; attention: 0, its key count is device-resident).  Writes
+ * up to max_entries entries, sets *n_entries, then clears the record. */
+typedef struct dflow_prof_entry {
+  char name[32];   /* "gemm.store", "gemm.resid", "gemm.swiglu", "gemm.argmax", ..., "attention" */
+  int N, K, M;     /* GEMM shape (0 for attention) */
+  int launches;
+  double ms;
+  double bytes;
+} dflow_prof_entry;
+int dflow_profile(dflow_ctx* ctx, int enable);
+int dflow_profile_read(dflow_ctx* ctx, dflow_prof_entry* out, int max_entries, int* n_entries);
+
 /* Synchronises `stream`, copies the device status word to *host_status and,
  * if clear != 0, resets it. */
 int dflow_read_status(dflow_ctx* ctx, hipStream_t stream, int32_t* host_status, int clear);

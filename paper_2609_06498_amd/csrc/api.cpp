@@ -61,7 +61,20 @@ struct dflow_ctx {
   float2* rope;
   uint64_t* amax;
   int *row_argmax, *carry_rec, *status, *tmp_pos, *tmp_argmax;
+
+  // kernel timing record (dflow_profile)
+  bool prof = false;
+  std::vector<hipEvent_t> ev0, ev1;
+  struct Rec { int cls, N, K, M; double bytes; };
+  std::vector<Rec> ev_rec;
+  int n_ev = 0;
 };
+
+static const char* kClassName[] = {"gemm.store", "gemm.store_f32", "gemm.resid", "gemm.swiglu",
+                                   "gemm.bias_silu", "gemm.bias_f32", "gemm.argmax", "attention"};
+static constexpr int CLS_ATTN = 7;
+
+static constexpr int PROF_MAX = 16384;
 
 extern "C" const char* dflow_last_error(void) { return g_err.c_str(); }
 
@@ -260,6 +273,8 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
 
 extern "C" int dflow_destroy(dflow_ctx* c) {
   if (!c) return fail(DFLOW_EINVAL, "destroy: null context");
+  for (auto ev : c->ev0) (void)hipEventDestroy(ev);
+  for (auto ev : c->ev1) (void)hipEventDestroy(ev);
   hipError_t e = hipFree(c->ws);
   delete c;
   if (e != hipSuccess) return fail(DFLOW_EHIP, "destroy: %s", hipGetErrorString(e));
@@ -296,7 +311,21 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
   p.logits = logits;
   p.ldl = ldl;
   p.col0 = 0;
-  return launch_gemm(c->bf, epi, p, st);
+  const bool rec = c->prof && c->n_ev < PROF_MAX;
+  if (rec) {
+    hipError_t e = hipEventRecord(c->ev0[c->n_ev], st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = launch_gemm(c->bf, epi, p, st);
+  if (e != hipSuccess) return e;
+  if (rec) {
+    if ((e = hipEventRecord(c->ev1[c->n_ev], st)) != hipSuccess) return e;
+    const double out_elt = (epi == EPI_ARGMAX) ? 0.0 : ((epi == EPI_STORE_F32 || epi == EPI_BIAS_F32) ? 4.0 : c->elt);
+    const double n_out = (epi == EPI_SWIGLU) ? N / 2.0 : N;
+    c->ev_rec[c->n_ev] = {epi, N, K, M, (double)N * K * c->elt + (double)M * K * c->elt + (double)M * n_out * out_elt};
+    ++c->n_ev;
+  }
+  return hipSuccess;
 }
 
 void* pool_layer(dflow_ctx* c, void* pool, int l) { return (char*)pool + (size_t)l * c->pool_layer_elems * c->elt; }
@@ -323,7 +352,15 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const int* 
   a.part_o = c->part_o;
   a.part_ml = c->part_ml;
   a.out = c->attn;
-  return launch_attention(c->bf, a, st);
+  const bool rec = c->prof && c->n_ev < PROF_MAX;
+  hipError_t e;
+  if (rec && (e = hipEventRecord(c->ev0[c->n_ev], st)) != hipSuccess) return e;
+  if ((e = launch_attention(c->bf, a, st)) != hipSuccess) return e;
+  if (rec) {
+    if ((e = hipEventRecord(c->ev1[c->n_ev], st)) != hipSuccess) return e;
+    c->ev_rec[c->n_ev++] = {CLS_ATTN, 0, 0, nseq * Bq, 0.0};
+  }
+  return hipSuccess;
 }
 
 // QK-norm + RoPE + KV write for rows of `nseq` x Bq.
@@ -539,6 +576,51 @@ extern "C" int dflow_bench_force_drafts(dflow_ctx* c, hipStream_t st, int nseq, 
                                                           traj_len, traj_stride);
   HIPCHK(launch_force(traj, traj_stride, traj_len, (const signed char*)mode, tok, anchor, start_pos, nseq,
                       c->dm.block, c->dm.vocab, block_tok, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_profile(dflow_ctx* c, int enable) {
+  if (!c) return fail(DFLOW_EINVAL, "profile: null context");
+  if (enable && c->ev0.empty()) {
+    c->ev0.resize(PROF_MAX);
+    c->ev1.resize(PROF_MAX);
+    c->ev_rec.resize(PROF_MAX);
+    for (int i = 0; i < PROF_MAX; ++i) {
+      HIPCHK(hipEventCreate(&c->ev0[i]));
+      HIPCHK(hipEventCreate(&c->ev1[i]));
+    }
+  }
+  c->prof = enable != 0;
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_profile_read(dflow_ctx* c, dflow_prof_entry* out, int max_entries, int* n_entries) {
+  if (!c || !n_entries || (max_entries > 0 && !out)) return fail(DFLOW_EINVAL, "profile_read: null argument");
+  std::vector<dflow_prof_entry> agg;
+  for (int i = 0; i < c->n_ev; ++i) {
+    HIPCHK(hipEventSynchronize(c->ev1[i]));
+    float t = 0.f;
+    HIPCHK(hipEventElapsedTime(&t, c->ev0[i], c->ev1[i]));
+    const auto& r = c->ev_rec[i];
+    size_t k = 0;
+    for (; k < agg.size(); ++k)
+      if (!strcmp(agg[k].name, kClassName[r.cls]) && agg[k].N == r.N && agg[k].K == r.K && agg[k].M == r.M) break;
+    if (k == agg.size()) {
+      dflow_prof_entry e{};
+      snprintf(e.name, sizeof(e.name), "%s", kClassName[r.cls]);
+      e.N = r.N;
+      e.K = r.K;
+      e.M = r.M;
+      agg.push_back(e);
+    }
+    agg[k].launches += 1;
+    agg[k].ms += t;
+    agg[k].bytes += r.bytes;
+  }
+  const int n = (int)agg.size() < max_entries ? (int)agg.size() : max_entries;
+  for (int i = 0; i < n; ++i) out[i] = agg[i];
+  *n_entries = (int)agg.size();
+  c->n_ev = 0;
   return DFLOW_OK;
 }
 

@@ -82,7 +82,15 @@ EXPORTS = {
                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_read_status": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                                          ctypes.c_int]),
+    "dflow_profile": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    "dflow_profile_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                          ctypes.POINTER(ctypes.c_int)]),
 }
+
+
+class ProfEntry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("N", ctypes.c_int), ("K", ctypes.c_int), ("M", ctypes.c_int),
+                ("launches", ctypes.c_int), ("ms", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
 def load_library(path: Optional[str] = None):
@@ -257,6 +265,17 @@ class Runtime:
         self._check(self.lib.dflow_read_status(self.ctx, _stream(), ctypes.byref(out), int(clear)),
                     "dflow_read_status")
         return out.value
+
+    def profile(self, enable: bool):
+        self._check(self.lib.dflow_profile(self.ctx, int(bool(enable))), "dflow_profile")
+
+    def profile_read(self):
+        """List of dicts (name, N, K, M, launches, ms, bytes) per kernel class."""
+        buf = (ProfEntry * 64)()
+        n = ctypes.c_int(0)
+        self._check(self.lib.dflow_profile_read(self.ctx, buf, 64, ctypes.byref(n)), "dflow_profile_read")
+        return [{"name": e.name.decode(), "N": e.N, "K": e.K, "M": e.M, "launches": e.launches, "ms": e.ms,
+                 "bytes": e.bytes} for e in buf[:min(n.value, 64)]]
 
     def close(self):
         if getattr(self, "ctx", None):
