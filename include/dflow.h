@@ -159,8 +159,9 @@ const char* dflow_last_error(void);
 size_t dflow_packed_bytes(int dtype, int N, int K);
 
 /* Rearranges a row-major [N, K] weight into the tile layout the GEMM kernels
- * stream.  gate_up = 1 interleaves the 16-row strips of the two halves
- * [W_gate; W_up].  `w` and `out` are device buffers of dflow_packed_bytes. */
+ * stream.  gate_up = 1 treats w as [W_gate; W_up] and makes every packed
+ * 16-row strip hold 8 gate rows followed by the same 8 up rows.  `w` and `out`
+ * are device buffers of dflow_packed_bytes. */
 int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, void* out);
 
 /* Bytes of device workspace that dflow_create allocates for these dims. */

@@ -141,7 +141,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   const int rg_round = (d->block * G + 15) / 16, rg_pre = (d->max_rows * G + 15) / 16;
   int items = d->max_batch * rg_round;
   if (rg_pre > items) items = rg_pre;
-  const int lm_groups = (d->vocab / 16 + 3) / 4;
+  const int lm_groups = (d->vocab / 16 + 1) / 2;   // gemm_shape: two strips per argmax workgroup
   Layout L;
   size_t o = 0;
   int i = 0;

@@ -158,8 +158,9 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
 }
 
 // out[row, head, :] = sum_split e^(m_s - M) O_s / sum_split e^(m_s - M) l_s
+// (split order fixed; the split loads are independent and unrolled)
 template <typename T, int DH>
-__global__ void attn_combine_kernel(AttnParams p) {
+__global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
   const int row = blockIdx.x;           // s*Bq + j
   const int hq = blockIdx.y;
   const int d = threadIdx.x;
@@ -172,14 +173,18 @@ __global__ void attn_combine_kernel(AttnParams p) {
   int ns = (kv_len + SPLIT_KEYS - 1) / SPLIT_KEYS;
   if (ns > p.nsplit) ns = p.nsplit;
   const size_t base = (((size_t)s * p.Hkv + kvh) * p.rg + rgi) * p.nsplit;
+  const float* ml = p.part_ml + base * 32 + 2 * r;
+  const float* po = p.part_o + (base * 16 + r) * DH + d;
   float M = -INFINITY;
-  for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, p.part_ml[(base + sp) * 32 + 2 * r]);
+#pragma unroll 8
+  for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, ml[(size_t)sp * 32]);
   float acc = 0.f, lsum = 0.f;
+#pragma unroll 8
   for (int sp = 0; sp < ns; ++sp) {
-    const float m = p.part_ml[(base + sp) * 32 + 2 * r];
+    const float m = ml[(size_t)sp * 32];
     const float f = (m == -INFINITY) ? 0.f : __expf(m - M);
-    acc += f * p.part_o[((base + sp) * 16 + r) * DH + d];
-    lsum += f * p.part_ml[(base + sp) * 32 + 2 * r + 1];
+    acc += f * po[(size_t)sp * 16 * DH];
+    lsum += f * ml[(size_t)sp * 32 + 1];
   }
   const float v = lsum > 0.f ? acc / lsum : 0.f;
   TT<T>::st(reinterpret_cast<T*>(p.out), (size_t)row * p.Hq * DH + hq * DH + d, v);

@@ -6,6 +6,9 @@
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+// global-address-space view of 16-byte fragments (loads compile to global_load_dwordx4)
+typedef const __attribute__((address_space(1))) u32x4_t gu4;
 
 namespace dflow {
 
@@ -55,6 +58,17 @@ __device__ inline f32x4_t mma_frag(bf16, const uint4& a, const uint4& b, f32x4_t
   bf16x8_t av = __builtin_bit_cast(bf16x8_t, a);
   bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+}
+__device__ inline f32x4_t mma_frag(bf16, const u32x4_t& a, const u32x4_t& b, f32x4_t acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                 acc, 0, 0, 0);
+}
+__device__ inline f32x4_t mma_frag(float, const u32x4_t& a, const u32x4_t& b, f32x4_t acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+  return acc;
 }
 __device__ inline f32x4_t mma_frag(float, const uint4& a, const uint4& b, f32x4_t acc) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);

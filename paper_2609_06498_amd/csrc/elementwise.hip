@@ -32,25 +32,74 @@ hipError_t launch_embed(bool isbf, const int* tok, int M, const void* E, int V, 
 }
 
 // ---------------------------------------------------------------- RMSNorm
+// One block per row.  Each thread keeps up to RV 16-byte input vectors in
+// registers between the sum of squares and the scaled write.
+template <typename TI> struct Vec16;
+template <> struct Vec16<bf16> {
+  static constexpr int N = 8;
+  __device__ static inline void load(const bf16* p, float* v) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { v[2 * i] = bf2f(w[i] & 0xFFFF); v[2 * i + 1] = bf2f(w[i] >> 16); }
+  }
+};
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  __device__ static inline void load(const float* p, float* v) {
+    const float4 u = *reinterpret_cast<const float4*>(p);
+    v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+  }
+};
+
 template <typename T, typename TI>
-__global__ void rmsnorm_kernel(const TI* x, int ldx, int d, const T* g, float eps, T* out, int ldo) {
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const TI* x, int ldx, int d, const T* g, float eps, T* out,
+                                                      int ldo) {
+  constexpr int VN = Vec16<TI>::N;
+  constexpr int RV = 4;                       // vectors held per thread (d <= 256*RV*VN)
   __shared__ float sh[32];
   const int row = blockIdx.x;
   const TI* xr = x + (size_t)row * ldx;
+  const int nv = d / VN;
+  float v[RV][VN];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    const float v = TT<TI>::ld(xr, i);
-    ss += v * v;
+#pragma unroll
+  for (int r = 0; r < RV; ++r) {
+    const int i = threadIdx.x + r * blockDim.x;
+    if (i < nv) {
+      Vec16<TI>::load(xr + (size_t)i * VN, v[r]);
+#pragma unroll
+      for (int e = 0; e < VN; ++e) ss += v[r][e] * v[r][e];
+    }
+  }
+  for (int i = threadIdx.x + RV * blockDim.x; i < nv; i += blockDim.x) {   // rows wider than the register budget
+    float t[VN];
+    Vec16<TI>::load(xr + (size_t)i * VN, t);
+#pragma unroll
+    for (int e = 0; e < VN; ++e) ss += t[e] * t[e];
   }
   ss = block_sum(ss, sh);
-  const float r = rsqrtf(ss / (float)d + eps);
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    TT<T>::st(out, (size_t)row * ldo + i, TT<TI>::ld(xr, i) * r * TT<T>::ld(g, i));
+  const float rs = rsqrtf(ss / (float)d + eps);
+  T* o = out + (size_t)row * ldo;
+#pragma unroll
+  for (int r = 0; r < RV; ++r) {
+    const int i = threadIdx.x + r * blockDim.x;
+    if (i < nv)
+#pragma unroll
+      for (int e = 0; e < VN; ++e) TT<T>::st(o, (size_t)i * VN + e, v[r][e] * rs * TT<T>::ld(g, (size_t)i * VN + e));
+  }
+  for (int i = threadIdx.x + RV * blockDim.x; i < nv; i += blockDim.x) {
+    float t[VN];
+    Vec16<TI>::load(xr + (size_t)i * VN, t);
+#pragma unroll
+    for (int e = 0; e < VN; ++e) TT<T>::st(o, (size_t)i * VN + e, t[e] * rs * TT<T>::ld(g, (size_t)i * VN + e));
+  }
 }
 
 hipError_t launch_rmsnorm(bool isbf, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
                           void* out, int ldo, hipStream_t s) {
   if (M <= 0) return hipSuccess;
+  if ((d & 7) || (ldx & 7)) return hipErrorInvalidValue;   // 16-byte row vectors
   if (isbf && in_f32)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, float>), dim3(M), dim3(256), 0, s, (const float*)x, ldx, d,
                        (const bf16*)g, eps, (bf16*)out, ldo);

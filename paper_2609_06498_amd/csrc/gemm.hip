@@ -14,13 +14,15 @@
 namespace dflow {
 
 template <typename T, int NG, int MT, int EPI>
-__global__ void __launch_bounds__(1024) gemm_kernel(GemmParams p) {
+__global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   constexpr int KL = TT<T>::KL;
   constexpr int KT = TT<T>::KT;
-  constexpr int U = (MT >= 4) ? 1 : (MT == 2 ? 2 : 4);   // k tiles per pipeline stage
+  // k tiles per pipeline stage: 4 fragments of weights per stage and buffer
+  constexpr int U = (MT * NG >= 4) ? 1 : 4 / (MT * NG);
   extern __shared__ float lds[];
   const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  // wave index as a scalar: keeps the k-range bounds and the pipeline control uniform
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nw = blockDim.x >> 6;
   const int g = blockIdx.x;
   const int nt0 = g * NG;
@@ -31,9 +33,10 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmParams p) {
   const int M = p.M;
   const int mtiles = (M + 15) >> 4;
 
-  const uint4* Wp = reinterpret_cast<const uint4*>(p.W);
+  // Explicit global address space: generic (flat) loads would also count
+  // against the LDS counter and defeat the load pipelining below.
+  const gu4* Wp = (const gu4*)(p.W);
   const T* Ap = reinterpret_cast<const T*>(p.A);
-  const uint4 zero = make_uint4(0, 0, 0, 0);
 
   f32x4_t acc[MT][NG];
 #pragma unroll
@@ -41,57 +44,73 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NG; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  size_t wrow[NG];
+  // Out-of-range strips and rows are clamped to valid addresses instead of
+  // being predicated, so the main loop is straight-line code; their results
+  // land in columns/rows the epilogue never stores.
+  const gu4* wrow[NG];
 #pragma unroll
-  for (int j = 0; j < NG; ++j) wrow[j] = (size_t)(nt0 + j) * p.ktiles * 64 + lane;
-  const T* arow[MT];
-  bool aval[MT];
+  for (int j = 0; j < NG; ++j) wrow[j] = Wp + (size_t)min(nt0 + j, p.ntiles - 1) * p.ktiles * 64 + lane;
+  const gu4* arow[MT];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    const int m = i * 16 + (lane & 15);
-    aval[i] = (i < mtiles) && (m < M);
-    arow[i] = Ap + (size_t)(aval[i] ? m : 0) * p.lda + (lane >> 4) * KL;
+    const int m = min(i * 16 + (lane & 15), M - 1);
+    arow[i] = (const gu4*)(Ap + (size_t)m * p.lda + (lane >> 4) * KL);
   }
+  constexpr int AST = KT * (int)sizeof(T) / 16;   // uint4 stride of one k tile along an A row
 
-  uint4 bq[2][U][NG];
-  uint4 aq[2][U][MT];
-  auto load = [&](int st, int kt) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = kt + u;
-      const bool kv = k < ke;
-#pragma unroll
-      for (int j = 0; j < NG; ++j)
-        bq[st][u][j] = (kv && j < nvalid) ? Wp[wrow[j] + (size_t)k * 64] : zero;
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-        aq[st][u][i] = (kv && aval[i]) ? *reinterpret_cast<const uint4*>(arow[i] + (size_t)k * KT) : zero;
+  u32x4_t bq[2][U][NG];
+  u32x4_t aq[2][U][MT];
+#define DFLOW_LOAD(st, kt)                                                             \
+  _Pragma("unroll") for (int u = 0; u < U; ++u) {                                       \
+    _Pragma("unroll") for (int j = 0; j < NG; ++j) bq[st][u][j] = wrow[j][(size_t)((kt) + u) * 64]; \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i) aq[st][u][i] = arow[i][(size_t)((kt) + u) * AST]; \
+  }                                                                                     \
+  __builtin_amdgcn_sched_barrier(0);
+#define DFLOW_COMPUTE(st)                                                              \
+  _Pragma("unroll") for (int u = 0; u < U; ++u)                                         \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i)                                      \
+      _Pragma("unroll") for (int j = 0; j < NG; ++j) acc[i][j] = mma_frag(T(), aq[st][u][i], bq[st][u][j], acc[i][j]);
+
+  // Full stages of U tiles, double-buffered.  Inside the steady-state loop
+  // every load is unconditional, so the compiler's wait before each compute
+  // covers only the stage being consumed, never the prefetch just issued.
+  const int nst = (ke - kb) / U;
+  int kt = kb;
+  if (nst > 0) {
+    DFLOW_LOAD(0, kt);
+    int left = nst;
+    while (left > 2) {
+      DFLOW_LOAD(1, kt + U);
+      DFLOW_COMPUTE(0);
+      DFLOW_LOAD(0, kt + 2 * U);
+      DFLOW_COMPUTE(1);
+      kt += 2 * U;
+      left -= 2;
     }
-  };
-  auto compute = [&](int st) {
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NG; ++j) acc[i][j] = mma_frag(T(), aq[st][u][i], bq[st][u][j], acc[i][j]);
-  };
-
-  if (kb < ke) {
-    load(0, kb);
-    int kt = kb;
-    for (;;) {
-      const int k1 = kt + U;
-      if (k1 < ke) load(1, k1);
-      compute(0);
-      if (k1 >= ke) break;
-      const int k2 = k1 + U;
-      if (k2 < ke) load(0, k2);
-      compute(1);
-      if (k2 >= ke) break;
-      kt = k2;
+    if (left == 2) {
+      DFLOW_LOAD(1, kt + U);
+      DFLOW_COMPUTE(0);
+      DFLOW_COMPUTE(1);
+      kt += 2 * U;
+    } else {
+      DFLOW_COMPUTE(0);
+      kt += U;
     }
   }
+  // ragged tail (fewer than U tiles)
+  for (; kt < ke; ++kt) {
+    u32x4_t b1[NG], a1[MT];
+#pragma unroll
+    for (int j = 0; j < NG; ++j) b1[j] = wrow[j][(size_t)kt * 64];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) a1[i] = arow[i][(size_t)kt * AST];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NG; ++j) acc[i][j] = mma_frag(T(), a1[i], b1[j], acc[i][j]);
+  }
+#undef DFLOW_LOAD
+#undef DFLOW_COMPUTE
 
   // ---- cross-wave reduction in fixed wave order, one m tile at a time
   float* red = lds;                                 // [nw][NG][64][4]
@@ -132,13 +151,14 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmParams p) {
       p.amax[(size_t)g * p.amax_ld + m] = argmax_key(best, colbase + bi);
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
+    // each packed strip holds 8 gate columns followed by the matching 8 up columns
     const int half = ncols / 2;
     const int obase = (p.col0 + nt0 * 16) / 2;
     for (int e = threadIdx.x; e < M * half; e += blockDim.x) {
       const int m = e / half, c = e - m * half;
-      const int pair = c >> 4, cc = c & 15;
-      const float gt = ct[m * CW + pair * 32 + cc];
-      const float up = ct[m * CW + pair * 32 + 16 + cc];
+      const int strip = c >> 3, cc = c & 7;
+      const float gt = ct[m * CW + strip * 16 + cc];
+      const float up = ct[m * CW + strip * 16 + 8 + cc];
       TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + obase + c, silu(gt) * up);
     }
   } else {
@@ -165,16 +185,18 @@ __global__ void __launch_bounds__(1024) gemm_kernel(GemmParams p) {
   }
 }
 
-// Column-strip count per workgroup is tied to the epilogue; the wave count
-// (the K split) depends only on the K extent, never on M.
+// Launch shape from (N, K) only, never from M: one 16-column strip per
+// workgroup (two for the LM head, whose argmax epilogue then scans 32
+// columns), and the smallest power-of-two wave count (2..8) that puts at
+// least 2048 waves in flight while leaving each wave at least 8 k tiles.
+// Chosen from a sweep over the 8B-shape projections at M = 16.
 GemmShape gemm_shape(int ntiles, int ktiles, int epi) {
   GemmShape s;
-  s.ng = (epi == EPI_SWIGLU) ? 2 : (epi == EPI_ARGMAX ? 4 : 1);
-  int waves = ktiles / 16;
-  if (waves < 1) waves = 1;
-  if (waves > 16) waves = 16;
-  s.waves = waves;
+  s.ng = (epi == EPI_ARGMAX) ? 2 : 1;
   s.groups = (ntiles + s.ng - 1) / s.ng;
+  int waves = 2;
+  while (waves < 8 && (long long)s.groups * waves < 2048 && ktiles / (2 * waves) >= 8) waves *= 2;
+  s.waves = waves;
   return s;
 }
 
@@ -202,10 +224,10 @@ static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
     case EPI_STORE_T: return launch_mt<T, 1, EPI_STORE_T>(p, sh, st);
     case EPI_STORE_F32: return launch_mt<T, 1, EPI_STORE_F32>(p, sh, st);
     case EPI_RESID: return launch_mt<T, 1, EPI_RESID>(p, sh, st);
-    case EPI_SWIGLU: return launch_mt<T, 2, EPI_SWIGLU>(p, sh, st);
+    case EPI_SWIGLU: return launch_mt<T, 1, EPI_SWIGLU>(p, sh, st);
     case EPI_BIAS_SILU: return launch_mt<T, 1, EPI_BIAS_SILU>(p, sh, st);
     case EPI_BIAS_F32: return launch_mt<T, 1, EPI_BIAS_F32>(p, sh, st);
-    case EPI_ARGMAX: return launch_mt<T, 4, EPI_ARGMAX>(p, sh, st);
+    case EPI_ARGMAX: return launch_mt<T, 2, EPI_ARGMAX>(p, sh, st);
   }
   return hipErrorInvalidValue;
 }
@@ -217,7 +239,8 @@ hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t st) 
 
 // ------------------------------------------------------------------ packing
 // out tile (nt, kt) lane l element e <- W[src_row(nt, l%16)][kt*KT + (l/16)*KL + e]
-// gate_up: W is [2F, K] = [gate; up]; packed strip 2i is gate strip i, 2i+1 is up strip i.
+// gate_up: W is [2F, K] = [gate; up]; packed strip i holds gate rows 8i..8i+7
+// followed by up rows 8i..8i+7, so one strip yields 8 SwiGLU outputs.
 template <typename T>
 __global__ void pack_kernel(const T* __restrict__ W, int N, int K, int gate_up, T* __restrict__ out) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
@@ -230,9 +253,9 @@ __global__ void pack_kernel(const T* __restrict__ W, int N, int K, int gate_up, 
     const size_t tile = lt / 64;
     const int kt = (int)(tile % ktiles);
     const int nt = (int)(tile / ktiles);
-    int strip = nt;
-    if (gate_up) strip = (nt & 1) ? (N / 32 + (nt >> 1)) : (nt >> 1);
-    const size_t row = (size_t)strip * 16 + (l & 15);
+    const int r16 = l & 15;
+    size_t row = (size_t)nt * 16 + r16;
+    if (gate_up) row = (r16 < 8) ? (size_t)nt * 8 + r16 : (size_t)N / 2 + (size_t)nt * 8 + (r16 - 8);
     const size_t col = (size_t)kt * KT + (l >> 4) * KL + e;
     out[o] = W[row * K + col];
   }
