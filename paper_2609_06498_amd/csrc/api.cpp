@@ -137,7 +137,8 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   const int rows_round = d->max_batch * d->block;
   const int mmax = rows_round > d->max_rows ? rows_round : d->max_rows;
   const int G = d->n_heads / d->n_kv_heads;
-  const int nsplit = (d->max_pages * PAGE + SPLIT_KEYS - 1) / SPLIT_KEYS;
+  const int split_keys = d->dtype == DFLOW_BF16 ? SplitKeys<bf16>::value : SplitKeys<float>::value;
+  const int nsplit = (d->max_pages * PAGE + split_keys - 1) / split_keys;
   const int rg_round = (d->block * G + 15) / 16, rg_pre = (d->max_rows * G + 15) / 16;
   int items = d->max_batch * rg_round;
   if (rg_pre > items) items = rg_pre;

@@ -4,34 +4,37 @@
 // 0..t+j.  Drafting (causal = 0): every block row attends to every key below
 // t+B (committed-context keys followed by the block's own keys).
 //
-// Work item = (sequence, kv head, split of 256 keys at fixed absolute
-// positions, group of 16 attention rows), where the attention rows of a kv
-// head are (block row j, query head g of the group) pairs.  Each of the four
-// waves of a workgroup takes one 64-key page of the split: it computes
-// S^T = K Q^T on the matrix cores (so the softmax'd scores already sit in the
-// A-operand layout of P V), applies the mask, and accumulates P V.  The four
-// waves are merged in LDS in wave order, the splits by the combine kernel in
-// split order: a row's arithmetic depends only on its own visible keys.
+// Workgroup = (sequence, kv head, split of keys at fixed absolute positions:
+// 256 keys for bf16, 128 for fp32).  The split's K and V pages (stored in
+// matrix-core fragment order) are staged into LDS once with 16-byte loads;
+// each wave then owns whole groups of 16 attention rows -- (block row j,
+// query head g of the group) pairs, so the query heads of a group share every
+// K/V byte -- and sweeps the staged pages with an online softmax: S^T = K Q^T
+// on the matrix cores (the exponentiated scores already sit in the A-operand
+// layout of P V), mask, running max/sum, P V.  Splits are merged by the
+// combine kernel in split order, so a row's arithmetic depends only on its
+// own visible keys, at any batch composition.
 #include "common.h"
 #include "kernels.h"
 
 namespace dflow {
 
-template <typename T>
-__device__ inline f32x4_t mma_pv(const float p[4], const void* vrow, f32x4_t acc);
+// Fragment of 4 consecutive keys of one value channel (8 bytes bf16, 16 bytes fp32)
+template <typename T> struct VFrag;
+template <> struct VFrag<bf16> { typedef uint2 type; };
+template <> struct VFrag<float> { typedef float4 type; };
 
-// P (4 consecutive keys of row l%16) times V^T fragment (same 4 keys, channel l%16)
+template <typename T>
+__device__ inline f32x4_t mma_pv_frag(const float p[4], const typename VFrag<T>::type& v, f32x4_t acc);
 template <>
-__device__ inline f32x4_t mma_pv<bf16>(const float p[4], const void* vrow, f32x4_t acc) {
-  const uint2 vb = *reinterpret_cast<const uint2*>(vrow);
+__device__ inline f32x4_t mma_pv_frag<bf16>(const float p[4], const uint2& vb, f32x4_t acc) {
   short4_t a, b;
   a[0] = (short)f2bf(p[0]); a[1] = (short)f2bf(p[1]); a[2] = (short)f2bf(p[2]); a[3] = (short)f2bf(p[3]);
   b[0] = (short)(vb.x & 0xFFFF); b[1] = (short)(vb.x >> 16); b[2] = (short)(vb.y & 0xFFFF); b[3] = (short)(vb.y >> 16);
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc, 0, 0, 0);
 }
 template <>
-__device__ inline f32x4_t mma_pv<float>(const float p[4], const void* vrow, f32x4_t acc) {
-  const float4 vb = *reinterpret_cast<const float4*>(vrow);
+__device__ inline f32x4_t mma_pv_frag<float>(const float p[4], const float4& vb, f32x4_t acc) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(p[0], vb.x, acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(p[1], vb.y, acc, 0, 0, 0);
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(p[2], vb.z, acc, 0, 0, 0);
@@ -42,118 +45,176 @@ __device__ inline f32x4_t mma_pv<float>(const float p[4], const void* vrow, f32x
 template <typename T, int DH>
 __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
-  constexpr int KS = DH / KT;          // k steps of S^T
-  constexpr int DT = DH / 16;          // output channel tiles
-  __shared__ float sh_o[4][16][DH];
-  __shared__ float sh_m[4][16], sh_l[4][16];
+  constexpr int KS = DH / KT;                 // k steps of S^T
+  constexpr int DT = DH / 16;                 // output channel tiles
+  constexpr int NPG = SplitKeys<T>::value / PAGE;   // pages per split
+  constexpr int PG = PAGE * DH;               // elements of one K (or V) page block
+  typedef typename VFrag<T>::type vfrag_t;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* lk = reinterpret_cast<T*>(smem);         // [2][PG] keys, fragment order (double buffer)
+  T* lv = lk + (size_t)2 * PG;                // [2][PG] values, fragment order
+  __shared__ int s_page[NPG];
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  // XCD-aware item mapping: the row groups of one (seq, head, split) share an XCD (and its L2).
-  const int L = blockIdx.x;
-  const int xcd = L & 7, slot = L >> 3;
-  const int rgi = slot % p.rg;
-  const int item = xcd + 8 * (slot / p.rg);
-  const int n_items = p.nseq * p.Hkv * p.nsplit;
-  if (item >= n_items) return;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int item = blockIdx.x;                // (seq, kv head, split), split fastest
   const int split = item % p.nsplit;
   const int kvh = (item / p.nsplit) % p.Hkv;
   const int s = item / (p.nsplit * p.Hkv);
-
-  const int t0 = p.start_pos[s];
-  const int kv_len = t0 + p.Bq;
-  if (split * SPLIT_KEYS >= kv_len) return;
   const int G = p.Hq / p.Hkv;
   const int R = p.Bq * G;
   const float scale = rsqrtf((float)DH);
+  const int key0 = split * SplitKeys<T>::value;
+  const int t0 = p.start_pos[s];
+  const int kv_len = t0 + p.Bq;
+  if (key0 >= kv_len) return;                 // uniform over the workgroup
 
-  // this lane's attention row (as column of S^T / B operand)
-  const int ar = rgi * 16 + (lane & 15);
-  const bool row_ok = ar < R;
-  const int jrow = row_ok ? ar / G : 0;
-  const int grow = row_ok ? ar % G : 0;
-  const int pos_row = t0 + jrow;
-  const T* qrow = reinterpret_cast<const T*>(p.Q) + ((size_t)(s * p.Bq + jrow) * p.Hq + kvh * G + grow) * DH;
-  uint4 qf[KS];
-#pragma unroll
-  for (int k = 0; k < KS; ++k)
-    qf[k] = row_ok ? *reinterpret_cast<const uint4*>(qrow + k * KT + (lane >> 4) * KL) : make_uint4(0, 0, 0, 0);
-
-  const int kp0 = split * SPLIT_KEYS + w * PAGE;   // first key of this wave's page
-  float mrow = -INFINITY, lrow = 0.f;
-  f32x4_t o[DT];
-#pragma unroll
-  for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  const int pidx = kp0 / PAGE;
-  const int page = (kp0 < kv_len && pidx < p.max_pages) ? p.page_table[(size_t)s * p.max_pages + pidx] : -1;
-  if (page >= 0 && page < p.num_pages) {
-    const T* kb = reinterpret_cast<const T*>(p.kpool) + ((size_t)page * p.Hkv + kvh) * PAGE * DH;
-    const T* vb = reinterpret_cast<const T*>(p.vpool) + ((size_t)page * p.Hkv + kvh) * DH * PAGE;
-    float sc[4][4];
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt) {
-      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      const T* krow = kb + (size_t)(kt * 16 + (lane & 15)) * DH + (lane >> 4) * KL;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) acc = mma_frag(T(), *reinterpret_cast<const uint4*>(krow + k * KT), qf[k], acc);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
-        const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
-        sc[kt][r] = vis ? acc[r] * scale : -INFINITY;
-      }
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    float ls = 0.f;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float e = (mx == -INFINITY || sc[kt][r] == -INFINITY) ? 0.f : __expf(sc[kt][r] - mx);
-        sc[kt][r] = e;
-        ls += e;
-      }
-    ls += __shfl_xor(ls, 16, 64);
-    ls += __shfl_xor(ls, 32, 64);
-    mrow = mx;
-    lrow = ls;
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const T* vrow = vb + (size_t)(dt * 16 + (lane & 15)) * PAGE + kt * 16 + 4 * (lane >> 4);
-        o[dt] = mma_pv<T>(sc[kt], vrow, o[dt]);
-      }
+  // ---- pages stream through two LDS buffers: page i+1 is fetched into
+  // registers while page i is used, then stored into the other buffer.
+  if (threadIdx.x < NPG) {
+    const int pidx = min(key0 / PAGE + (int)threadIdx.x, p.max_pages - 1);
+    const int pg = p.page_table[(size_t)s * p.max_pages + pidx];
+    s_page[threadIdx.x] = (key0 + (int)threadIdx.x * PAGE < kv_len && pg >= 0 && pg < p.num_pages) ? pg : -1;
   }
-
-  // ---- merge the four waves (fixed order)
-  if (lane < 16) { sh_m[w][lane] = mrow; sh_l[w][lane] = lrow; }
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) sh_o[w][4 * (lane >> 4) + r][dt * 16 + (lane & 15)] = o[dt][r];
   __syncthreads();
-  const size_t pi = (((size_t)s * p.Hkv + kvh) * p.rg + rgi) * p.nsplit + split;
-  float* po = p.part_o + pi * 16 * DH;
-  float* pml = p.part_ml + pi * 32;
-  for (int e = threadIdx.x; e < 16 * DH; e += blockDim.x) {
-    const int r = e / DH, d = e - r * DH;
-    float M = -INFINITY;
-    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, sh_m[ww][r]);
-    float acc = 0.f, lsum = 0.f;
-    for (int ww = 0; ww < 4; ++ww) {
-      const float f = (sh_m[ww][r] == -INFINITY) ? 0.f : __expf(sh_m[ww][r] - M);
-      acc += f * sh_o[ww][r][d];
-      lsum += f * sh_l[ww][r];
+  constexpr int V16 = PG * (int)sizeof(T) / 16;       // 16-byte vectors per page block
+  constexpr int PER = V16 / 256;                      // per thread, K and V each
+  static_assert(V16 % 256 == 0, "page staging assumes 256 threads");
+  u32x4_t kr[PER], vr[PER];
+  // absent pages read page 0 of the pool (always valid); their copy is never used
+  auto fetch = [&](int pi) {
+    const int pg = max(s_page[pi], 0);
+    const size_t off = ((size_t)pg * p.Hkv + kvh) * PG;
+    const gu4* gk = (const gu4*)(reinterpret_cast<const T*>(p.kpool) + off);
+    const gu4* gv = (const gu4*)(reinterpret_cast<const T*>(p.vpool) + off);
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      kr[it] = gk[threadIdx.x + it * 256];
+      vr[it] = gv[threadIdx.x + it * 256];
     }
-    po[e] = acc;
-    if (d == 0) { pml[2 * r] = M; pml[2 * r + 1] = lsum; }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      reinterpret_cast<u32x4_t*>(lk + (size_t)buf * PG)[threadIdx.x + it * 256] = kr[it];
+      reinterpret_cast<u32x4_t*>(lv + (size_t)buf * PG)[threadIdx.x + it * 256] = vr[it];
+    }
+  };
+  // ---- each wave owns up to RGW whole 16-row groups per pass over the pages.
+  // The pass and page loops are uniform over the workgroup: every thread
+  // stages every page and reaches every barrier, with or without rows.
+  constexpr int RGW = 2;
+  const int nrg = (R + 15) / 16;
+  const int npass = (nrg + 4 * RGW - 1) / (4 * RGW);
+  for (int pass = 0; pass < npass; ++pass) {
+    int rgs[RGW];
+    bool rgv[RGW];
+    u32x4_t qf[RGW][KS];
+    float mrow[RGW], lrow[RGW];
+    f32x4_t o[RGW][DT];
+#pragma unroll
+    for (int g = 0; g < RGW; ++g) {
+      rgs[g] = pass * 4 * RGW + 4 * g + w;
+      rgv[g] = rgs[g] < nrg;
+      const int ar = min(rgs[g], nrg - 1) * 16 + (lane & 15);
+      const int jrow = ar < R ? ar / G : 0, grow = ar < R ? ar % G : 0;
+      const T* qrow = reinterpret_cast<const T*>(p.Q) + ((size_t)(s * p.Bq + jrow) * p.Hq + kvh * G + grow) * DH;
+#pragma unroll
+      for (int k = 0; k < KS; ++k) qf[g][k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
+      mrow[g] = -INFINITY;
+      lrow[g] = 0.f;
+#pragma unroll
+      for (int i = 0; i < DT; ++i) o[g][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    fetch(0);
+    __syncthreads();                          // buffer 0 is free (previous pass finished with it)
+    store(0);
+    __syncthreads();
+    for (int pi = 0; pi < NPG; ++pi) {
+      const int buf = pi & 1;
+      if (pi + 1 < NPG) fetch(pi + 1);        // uniform; lands while this page is used
+      if (s_page[pi] >= 0) {                  // uniform
+        const int kp0 = key0 + pi * PAGE;
+        const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)buf * PG);
+        const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)buf * PG);
+#pragma unroll
+        for (int g = 0; g < RGW; ++g) {
+          if (!rgv[g]) continue;              // uniform per wave; no barrier inside
+          const int ar = rgs[g] * 16 + (lane & 15);
+          const bool row_ok = ar < R;
+          const int pos_row = t0 + (row_ok ? ar / G : 0);
+          float sc[4][4];
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt) {
+            f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[g][k], acc);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
+              const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
+              sc[kt][r] = vis ? acc[r] * scale : -INFINITY;
+            }
+          }
+          float mx = -INFINITY;
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
+          mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+          // rows with nothing visible so far keep m = -inf, l = 0 and a zero output;
+          // control flow stays uniform (the matrix-core ops and shuffles need all lanes)
+          const float mnew = fmaxf(mrow[g], mx);
+          const float alpha = (mrow[g] == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : __expf(mrow[g] - mnew);
+          float ls = 0.f;
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float e = (sc[kt][r] == -INFINITY) ? 0.f : __expf(sc[kt][r] - mnew);
+              sc[kt][r] = e;
+              ls += e;
+            }
+          ls += __shfl_xor(ls, 16, 64);
+          ls += __shfl_xor(ls, 32, 64);
+          lrow[g] = lrow[g] * alpha + ls;
+          mrow[g] = mnew;
+          float al[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o[g][dt][r] *= al[r];
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[g][dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[g][dt]);
+        }
+      }
+      if (pi + 1 < NPG) {
+        // the other buffer was last read in iteration pi-1, which every wave
+        // finished before the barrier that ended that iteration
+        store(buf ^ 1);
+        __syncthreads();
+      }
+    }
+    // ---- this split's partials of the wave's row groups
+#pragma unroll
+    for (int g = 0; g < RGW; ++g) {
+      if (!rgv[g]) continue;
+      const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + rgs[g]) * p.nsplit + split;
+      float* po = p.part_o + pidx * 16 * DH;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) po[(4 * (lane >> 4) + r) * DH + dt * 16 + (lane & 15)] = o[g][dt][r];
+      if (lane < 16) {
+        p.part_ml[pidx * 32 + 2 * lane] = mrow[g];
+        p.part_ml[pidx * 32 + 2 * lane + 1] = lrow[g];
+      }
+    }
   }
 }
 
@@ -170,7 +231,7 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
   const int ar = j * G + g;
   const int rgi = ar >> 4, r = ar & 15;
   const int kv_len = p.start_pos[s] + p.Bq;
-  int ns = (kv_len + SPLIT_KEYS - 1) / SPLIT_KEYS;
+  int ns = (kv_len + SplitKeys<T>::value - 1) / SplitKeys<T>::value;
   if (ns > p.nsplit) ns = p.nsplit;
   const size_t base = (((size_t)s * p.Hkv + kvh) * p.rg + rgi) * p.nsplit;
   const float* ml = p.part_ml + base * 32 + 2 * r;
@@ -192,9 +253,17 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
-  const int n_items = p.nseq * p.Hkv * p.nsplit;
-  const int blocks = ((n_items + 7) / 8) * 8 * p.rg;
-  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(blocks), dim3(256), 0, st, p);
+  const int blocks = p.nseq * p.Hkv * p.nsplit;
+  const size_t lds = 2 * 2 * (size_t)PAGE * DH * sizeof(T);   // two page buffers, K and V
+  if (lds > 160 * 1024) return hipErrorInvalidConfiguration;
+  static bool lds_set = false;   // allow more than the default dynamic LDS once per instantiation
+  if (!lds_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    lds_set = true;
+  }
+  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(blocks), dim3(256), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(p.nseq * p.Bq, p.Hq), dim3(DH), 0, st, p);

@@ -14,7 +14,10 @@ namespace dflow {
 
 constexpr int WAVE = 64;
 constexpr int PAGE = 64;          // KV page size in tokens (also the attention sub-chunk)
-constexpr int SPLIT_KEYS = 256;   // keys per attention split, at fixed absolute positions
+// keys per attention split (fixed absolute positions): 4 pages bf16, 2 pages fp32,
+// so the staged K+V pages of a split fit the 160 KB LDS of a CU
+template <typename T> struct SplitKeys;
+template <> struct SplitKeys<float> { static constexpr int value = 128; };
 
 // ------------------------------------------------------------------ bf16 storage
 struct bf16 { uint16_t u; };
@@ -33,6 +36,8 @@ __device__ __host__ inline uint16_t f2bf(float f) {
   u += 0x7FFFu + ((u >> 16) & 1u);
   return (uint16_t)(u >> 16);
 }
+
+template <> struct SplitKeys<bf16> { static constexpr int value = 256; };
 
 // Storage-type traits.  A "lane fragment" is the 16 bytes one lane feeds to
 // the matrix core per tile: 8 bf16 or 4 fp32 consecutive k values.

@@ -143,11 +143,19 @@ __global__ void qk_rope_kernel(RopeParams p) {
   }
   const int slot = pos % PAGE;
   const int i = threadIdx.x;   // pair (i, i + half)
-  if (!is_q && !is_k) {        // value head: transposed page layout
+  constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
+  const int KS = Dh / KT, DT = Dh / 16;
+  if (!is_q && !is_k) {        // value head, fragment order (see kernels.h)
     T* vp = reinterpret_cast<T*>(p.vpool) + page_base;
-    for (int e = i; e < Dh; e += blockDim.x) vp[(size_t)e * PAGE + slot] = src[e];
+    const int kt = slot / 16, q = (slot % 16) / 4, r = slot % 4;
+    for (int e = i; e < Dh; e += blockDim.x)
+      vp[((size_t)(kt * DT + e / 16) * 64 + q * 16 + e % 16) * 4 + r] = src[e];
     return;
   }
+  // key element d of this slot, fragment order (see kernels.h)
+  auto koff = [&](int d) -> size_t {
+    return ((size_t)((slot / 16) * KS + d / KT) * 64 + ((d % KT) / KL) * 16 + slot % 16) * KL + d % KL;
+  };
   const T* gain = reinterpret_cast<const T*>(is_q ? p.q_norm : p.k_norm);
   float x1 = 0.f, x2 = 0.f;
   if (i < half) { x1 = TT<T>::ld(src, i); x2 = TT<T>::ld(src, i + half); }
@@ -164,9 +172,9 @@ __global__ void qk_rope_kernel(RopeParams p) {
       TT<T>::st(q, i, o1);
       TT<T>::st(q, i + half, o2);
     } else {
-      T* kp = reinterpret_cast<T*>(p.kpool) + page_base + (size_t)slot * Dh;
-      TT<T>::st(kp, i, o1);
-      TT<T>::st(kp, i + half, o2);
+      T* kp = reinterpret_cast<T*>(p.kpool) + page_base;
+      TT<T>::st(kp, koff(i), o1);
+      TT<T>::st(kp, koff(i + half), o2);
     }
   }
 }

@@ -38,9 +38,13 @@ hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, void
 
 namespace dflow {
 
-// Paged KV layout (per layer pool):
-//   K: [page][kv_head][slot 0..63][Dh]      (key rows contiguous)
-//   V: [page][kv_head][Dh][slot 0..63]      (transposed: keys contiguous per channel)
+// Paged KV layout (per layer pool): [page][kv_head][64 keys x Dh] where the
+// 64 x Dh block of a page is stored in matrix-core fragment order:
+//   K element (key, d): ((kt*KS + ks)*64 + q*16 + key%16)*KL + d%KL
+//       with kt = key/16, ks = d/KT, q = (d%KT)/KL, KS = Dh/KT
+//   V element (key, d): ((kt*DT + dt)*64 + q*16 + d%16)*4 + key%4
+//       with kt = key/16, q = (key%16)/4, dt = d/16, DT = Dh/16
+// (KL, KT: 8, 32 for bf16 and 4, 16 for fp32.)
 struct AttnParams {
   const void* Q;             // [nseq*Bq, Hq*Dh] storage type, after QK-norm + RoPE
   const void* kpool;
