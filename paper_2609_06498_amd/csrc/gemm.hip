@@ -185,17 +185,19 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   }
 }
 
-// Launch shape from (N, K) only, never from M: one 16-column strip per
-// workgroup (two for the LM head, whose argmax epilogue then scans 32
-// columns), and the smallest power-of-two wave count (2..8) that puts at
-// least 2048 waves in flight while leaving each wave at least 8 k tiles.
-// Chosen from a sweep over the 8B-shape projections at M = 16.
+// Launch shape from (N, K) only, never from M.  Wide weights (>= 1024
+// strips) and the LM head take two 16-column strips per workgroup (the A
+// fragments are reused across both); narrower ones take one so that enough
+// workgroups exist.  The wave count (the K split) is the smallest power of
+// two in 2..8 that puts at least 1024 waves in flight while leaving each wave
+// at least 8 k tiles.  Chosen from a sweep over the 8B-shape projections at
+// M = 16 with weights streamed from HBM.
 GemmShape gemm_shape(int ntiles, int ktiles, int epi) {
   GemmShape s;
-  s.ng = (epi == EPI_ARGMAX) ? 2 : 1;
+  s.ng = (epi == EPI_ARGMAX || ntiles >= 1024) ? 2 : 1;
   s.groups = (ntiles + s.ng - 1) / s.ng;
   int waves = 2;
-  while (waves < 8 && (long long)s.groups * waves < 2048 && ktiles / (2 * waves) >= 8) waves *= 2;
+  while (waves < 8 && (long long)s.groups * waves < 1024 && ktiles / (2 * waves) >= 8) waves *= 2;
   s.waves = waves;
   return s;
 }
@@ -217,16 +219,21 @@ static hipError_t launch_mt(const GemmParams& p, const GemmShape& sh, hipStream_
   return hipErrorInvalidValue;
 }
 
+template <typename T, int EPI>
+static hipError_t launch_ng(const GemmParams& p, const GemmShape& sh, hipStream_t st) {
+  return sh.ng == 2 ? launch_mt<T, 2, EPI>(p, sh, st) : launch_mt<T, 1, EPI>(p, sh, st);
+}
+
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi);
   switch (epi) {
-    case EPI_STORE_T: return launch_mt<T, 1, EPI_STORE_T>(p, sh, st);
-    case EPI_STORE_F32: return launch_mt<T, 1, EPI_STORE_F32>(p, sh, st);
-    case EPI_RESID: return launch_mt<T, 1, EPI_RESID>(p, sh, st);
-    case EPI_SWIGLU: return launch_mt<T, 1, EPI_SWIGLU>(p, sh, st);
-    case EPI_BIAS_SILU: return launch_mt<T, 1, EPI_BIAS_SILU>(p, sh, st);
-    case EPI_BIAS_F32: return launch_mt<T, 1, EPI_BIAS_F32>(p, sh, st);
+    case EPI_STORE_T: return launch_ng<T, EPI_STORE_T>(p, sh, st);
+    case EPI_STORE_F32: return launch_ng<T, EPI_STORE_F32>(p, sh, st);
+    case EPI_RESID: return launch_ng<T, EPI_RESID>(p, sh, st);
+    case EPI_SWIGLU: return launch_ng<T, EPI_SWIGLU>(p, sh, st);
+    case EPI_BIAS_SILU: return launch_ng<T, EPI_BIAS_SILU>(p, sh, st);
+    case EPI_BIAS_F32: return launch_ng<T, EPI_BIAS_F32>(p, sh, st);
     case EPI_ARGMAX: return launch_mt<T, 2, EPI_ARGMAX>(p, sh, st);
   }
   return hipErrorInvalidValue;
