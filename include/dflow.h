@@ -47,13 +47,23 @@
  *    converted with dflow_pack_linear into the library's tile layout (same
  *    byte size).  The target/drafter QKV weight is the row concatenation
  *    [Wq; Wk; Wv]; the gate/up weight is [W_gate; W_up] packed with
- *    gate_up = 1.  Norm gains, biases, embeddings and E_mask stay plain.
- *  - KV pools, one per layer, consecutive:
- *      K: [layer][num_pages][n_kv_heads][64 slots][head_dim]
- *      V: [layer][num_pages][n_kv_heads][head_dim][64 slots]   (transposed)
- *    Position p of sequence s lives in page page_table[s*max_pages + p/64],
- *    slot p%64.  The drafter's context cache has the same layout with
- *    n_draft_layers layers and shares the page table.
+ *    gate_up = 1.  A projection that reads RMSNorm(x) (QKV after the
+ *    attention norm, gate/up after the FFN norm, the LM heads after the
+ *    final norms) is packed with that norm's gain as col_gain: the library
+ *    applies the per-row 1/rms scale itself and never materialises the
+ *    normalised rows.  QK-norm gains, g_c, biases, embeddings and E_mask
+ *    stay plain.
+ *  - KV pools, one per layer, consecutive: [layer][num_pages][n_kv_heads]
+ *    [64 x head_dim block].  Position p of sequence s lives in page
+ *    page_table[s*max_pages + p/64], slot p%64.  Inside a block the keys and
+ *    values are stored in matrix-core fragment order (KL, KT = 8, 32 for
+ *    bf16; 4, 16 for f32):
+ *      K (slot, e): ((slot/16 * head_dim/KT + e/KT) * 64 + (e%KT)/KL * 16
+ *                    + slot%16) * KL + e%KL
+ *      V (slot, e): ((slot/16 * head_dim/16 + e/16) * 64 + (slot%16)/4 * 16
+ *                    + e%16) * 4 + slot%4
+ *    The drafter's context cache has the same layout with n_draft_layers
+ *    layers and shares the page table.
  */
 #ifndef DFLOW_H
 #define DFLOW_H
@@ -114,23 +124,22 @@ typedef struct dflow_dims {
 } dflow_dims;
 
 typedef struct dflow_layer {
-  const void* attn_norm;  /* [d] */
-  const void* wqkv;       /* packed [(n_heads+2*n_kv_heads)*head_dim, d] */
+  const void* wqkv;       /* packed [(n_heads+2*n_kv_heads)*head_dim, d], col_gain = attention-norm gain */
   const void* q_norm;     /* [head_dim] */
   const void* k_norm;     /* [head_dim] */
   const void* wo;         /* packed [d, n_heads*head_dim] */
-  const void* ffn_norm;   /* [d] */
-  const void* wgu;        /* packed (gate_up=1) [2*ffn, d] */
+  const void* wgu;        /* packed (gate_up=1) [2*ffn, d], col_gain = FFN-norm gain */
   const void* wdown;      /* packed [d, ffn] */
+  const void* wkv_ctx;    /* drafter layers only: packed [Wk; Wv] [2*n_kv_heads*head_dim, d]
+                             without gain, projecting the context features F (Sec. 4.1) */
 } dflow_layer;
 
 typedef struct dflow_weights {
   const void* embed;            /* [vocab, d] plain row-major (shared by target, drafter and relay) */
-  const void* final_norm;       /* [d] target final RMSNorm gain */
-  const void* lm_head;          /* packed [vocab, d] (shared by target and drafter) */
+  const void* lm_head;          /* packed [vocab, d], col_gain = target final-norm gain */
   const dflow_layer* layers;    /* HOST array [n_layers] */
   const dflow_layer* draft_layers; /* HOST array [n_draft_layers] */
-  const void* draft_final_norm; /* [d] */
+  const void* draft_lm_head;    /* the shared LM head packed with col_gain = drafter final-norm gain */
   const void* e_mask;           /* [d] mask embedding E_mask */
   const void* w_c;              /* packed [d, n_capture*d] feature projection W_c */
   const void* g_c;              /* [d] RMSNorm gain after W_c */
@@ -160,9 +169,13 @@ size_t dflow_packed_bytes(int dtype, int N, int K);
 
 /* Rearranges a row-major [N, K] weight into the tile layout the GEMM kernels
  * stream.  gate_up = 1 treats w as [W_gate; W_up] and makes every packed
- * 16-row strip hold 8 gate rows followed by the same 8 up rows.  `w` and `out`
- * are device buffers of dflow_packed_bytes. */
-int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, void* out);
+ * 16-row strip hold 8 gate rows followed by the same 8 up rows.  col_gain
+ * (nullable, device [K] in the storage type) multiplies column k by
+ * col_gain[k] (fp32 product rounded once to the storage type): the gain of
+ * the RMSNorm that precedes the projection.  `w` and `out` are device buffers
+ * of dflow_packed_bytes. */
+int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, const void* col_gain,
+                      void* out);
 
 /* Bytes of device workspace that dflow_create allocates for these dims. */
 size_t dflow_workspace_bytes(const dflow_dims* dims);

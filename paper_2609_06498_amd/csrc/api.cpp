@@ -61,6 +61,7 @@ struct dflow_ctx {
   float2* rope;
   uint64_t* amax;
   int *row_argmax, *carry_rec, *status, *tmp_pos, *tmp_argmax;
+  float* ssq;   // [mmax][SSQ_LD] sums of squares of x per 16-column strip (RMSNorm row scales)
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -82,13 +83,14 @@ extern "C" size_t dflow_packed_bytes(int dtype, int N, int K) {
   return (size_t)N * (size_t)K * (dtype == DFLOW_BF16 ? 2 : 4);
 }
 
-extern "C" int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, void* out) {
+extern "C" int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up,
+                                 const void* col_gain, void* out) {
   if (!w || !out) return fail(DFLOW_EINVAL, "pack: null pointer");
   if (dtype != DFLOW_F32 && dtype != DFLOW_BF16) return fail(DFLOW_EDTYPE, "pack: dtype %d", dtype);
   const int KT = dtype == DFLOW_BF16 ? 32 : 16;
   if (N <= 0 || K <= 0 || N % 16 || K % KT || (gate_up && N % 32))
     return fail(DFLOW_ESHAPE, "pack: N=%d K=%d must be multiples of 16 and %d", N, K, KT);
-  HIPCHK(launch_pack(dtype == DFLOW_BF16, w, N, K, gate_up, out, stream));
+  HIPCHK(launch_pack(dtype == DFLOW_BF16, w, N, K, gate_up, col_gain, out, stream));
   return DFLOW_OK;
 }
 
@@ -107,6 +109,7 @@ int validate(const dflow_dims* d) {
     return fail(DFLOW_ESHAPE, "d=%d q_dim=%d ffn=%d relay_hidden=%d must be multiples of %d", d->d, qd, d->ffn,
                 d->relay_hidden, KT);
   if (d->vocab <= 0 || d->vocab % 16) return fail(DFLOW_ESHAPE, "vocab %d must be a multiple of 16", d->vocab);
+  if (d->d > 16 * SSQ_LD) return fail(DFLOW_ESHAPE, "d = %d: RMSNorm row scales support d <= %d", d->d, 16 * SSQ_LD);
   if (d->n_layers <= 0 || d->n_draft_layers <= 0) return fail(DFLOW_ESHAPE, "layer counts");
   if (d->n_capture < 1 || d->n_capture > 16) return fail(DFLOW_ESHAPE, "n_capture %d", d->n_capture);
   for (int i = 0; i < d->n_capture; ++i) {
@@ -167,6 +170,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add(4);                                              // 17 status
   add((size_t)(d->max_batch + 1) * 4);                 // 18 tmp_pos
   add((size_t)mmax * 4);                               // 19 tmp_argmax
+  add((size_t)mmax * SSQ_LD * 4);                      // 20 ssq: per-strip sums of squares of the residual rows
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -186,19 +190,20 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   int rc = validate(dims);
   if (rc) return rc;
   if (!w || !cache || !out) return fail(DFLOW_EINVAL, "create: null argument");
-  const void* req[] = {w->embed, w->final_norm, w->lm_head, w->layers, w->draft_layers, w->draft_final_norm,
+  const void* req[] = {w->embed, w->lm_head, w->layers, w->draft_layers, w->draft_lm_head,
                        w->e_mask, w->w_c, w->g_c, w->relay_w1, w->relay_c1, w->relay_w2, w->relay_c2,
                        w->relay_ln_g, w->relay_ln_b, cache->k_pool, cache->v_pool, cache->ck_pool, cache->cv_pool,
                        cache->page_table};
   for (size_t i = 0; i < sizeof(req) / sizeof(req[0]); ++i)
     if (!req[i]) return fail(DFLOW_EINVAL, "create: required pointer #%zu is null", i);
-  auto chk_layer = [](const dflow_layer& L) {
-    return L.attn_norm && L.wqkv && L.q_norm && L.k_norm && L.wo && L.ffn_norm && L.wgu && L.wdown;
+  auto chk_layer = [](const dflow_layer& L, bool draft) {
+    return L.wqkv && L.q_norm && L.k_norm && L.wo && L.wgu && L.wdown && (!draft || L.wkv_ctx);
   };
   for (int l = 0; l < dims->n_layers; ++l)
-    if (!chk_layer(w->layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in target layer %d", l);
+    if (!chk_layer(w->layers[l], false)) return fail(DFLOW_EINVAL, "create: null pointer in target layer %d", l);
   for (int l = 0; l < dims->n_draft_layers; ++l)
-    if (!chk_layer(w->draft_layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in drafter layer %d", l);
+    if (!chk_layer(w->draft_layers[l], true))
+      return fail(DFLOW_EINVAL, "create: null pointer in drafter layer %d", l);
 
   dflow_ctx* c = new dflow_ctx();
   c->dm = *dims;
@@ -247,6 +252,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->status = (int*)(b + L.off[17]);
   c->tmp_pos = (int*)(b + L.off[18]);
   c->tmp_argmax = (int*)(b + L.off[19]);
+  c->ssq = (float*)(b + L.off[20]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -285,15 +291,24 @@ extern "C" int dflow_destroy(dflow_ctx* c) {
 // ------------------------------------------------------------------ internals
 namespace {
 
-// Byte offset of packed strip `nt` of a weight with `ktiles` tiles per strip.
-inline const void* strip_ptr(const void* W, int nt, int ktiles) {
-  return (const char*)W + (size_t)nt * ktiles * 1024;
-}
+struct NormIn {            // RMSNorm of the A rows: per-strip sums of squares; the gain is in the packed weight
+  const float* ssq = nullptr;
+};
 
 hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, const void* W, int M, int N, int K,
                 void* Y, int ldy, const void* R = nullptr, int ldr = 0, void* Y2 = nullptr, int ldy2 = 0,
-                const void* bias = nullptr, float* logits = nullptr, int ldl = 0) {
+                const void* bias = nullptr, float* logits = nullptr, int ldl = 0, NormIn nin = NormIn(),
+                float* ssq_out = nullptr) {
   GemmParams p{};
+  if (nin.ssq) {
+    p.norm = 1;
+    p.ssq = nin.ssq;
+    p.ssq_ld = SSQ_LD;
+    p.ssq_parts = c->dm.d / 16;
+    p.eps = c->dm.rms_eps;
+  }
+  p.ssq_out = ssq_out;
+  p.ssq_out_ld = SSQ_LD;
   p.A = A;
   p.lda = lda;
   p.W = W;
@@ -398,16 +413,28 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   const dflow_dims& d = c->dm;
   const int M = nseq * Bq;
   hipError_t e;
-  if ((e = launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, L.attn_norm, d.rms_eps, c->xn, d.d, st))) return e;
-  if ((e = gemm(c, st, EPI_STORE_T, c->xn, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n))) return e;
+  // The attention and FFN RMSNorms are applied by the QKV and gate/up
+  // projections (gain folded into the packed weight, 1/rms from the sums of
+  // squares that the producer of x -- embedding, relay input or the residual
+  // epilogue -- left in c->ssq).
+  NormIn attn_n, ffn_n;
+  attn_n.ssq = c->ssq;
+  ffn_n.ssq = c->ssq;
+  if ((e = gemm(c, st, EPI_STORE_T, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
+                nullptr, nullptr, 0, attn_n)))
+    return e;
   if ((e = qk_rope(c, st, L, c->qkv, c->qkv_n, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool)))
     return e;
   if ((e = attention(c, st, nseq, Bq, start_pos, page_table, kpool, vpool, causal))) return e;
-  if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d))) return e;
-  if ((e = launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, L.ffn_norm, d.rms_eps, c->xn, d.d, st))) return e;
-  if ((e = gemm(c, st, EPI_SWIGLU, c->xn, d.d, L.wgu, M, 2 * d.ffn, d.d, c->act, d.ffn))) return e;
+  if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d, nullptr, 0,
+                nullptr, nullptr, 0, NormIn(), c->ssq)))
+    return e;
+  if ((e = gemm(c, st, EPI_SWIGLU, c->x, d.d, L.wgu, M, 2 * d.ffn, d.d, c->act, d.ffn, nullptr, 0, nullptr, 0,
+                nullptr, nullptr, 0, ffn_n)))
+    return e;
   const int capld = d.n_capture * d.d;
-  if ((e = gemm(c, st, EPI_RESID, c->act, d.ffn, L.wdown, M, d.d, d.ffn, c->x, d.d, c->x, d.d, capture, capld)))
+  if ((e = gemm(c, st, EPI_RESID, c->act, d.ffn, L.wdown, M, d.d, d.ffn, c->x, d.d, c->x, d.d, capture, capld,
+                nullptr, nullptr, 0, NormIn(), c->ssq)))
     return e;
   return hipSuccess;
 }
@@ -427,14 +454,13 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
       return e;
   }
   if (!argmax_out) return hipSuccess;
-  // LM head over rows lm_row0 .. lm_row0+lm_rows-1 only
+  // LM head (final RMSNorm folded in) over rows lm_row0 .. lm_row0+lm_rows-1 only
   if (lm_rows < 0) lm_rows = M;
   const size_t off = (size_t)lm_row0 * d.d * c->elt;
-  if ((e = launch_rmsnorm(c->bf, false, (char*)c->x + off, d.d, lm_rows, d.d, c->w.final_norm, d.rms_eps, c->xn,
-                          d.d, st)))
-    return e;
-  if ((e = gemm(c, st, EPI_ARGMAX, c->xn, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr,
-                0, nullptr, logits, d.vocab)))
+  NormIn fin;
+  fin.ssq = c->ssq + (size_t)lm_row0 * SSQ_LD;
+  if ((e = gemm(c, st, EPI_ARGMAX, (char*)c->x + off, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr,
+                0, nullptr, 0, nullptr, logits, d.vocab, fin)))
     return e;
   return launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, lm_rows, argmax_out, st);
 }
@@ -453,12 +479,10 @@ hipError_t ctx_append(dflow_ctx* c, hipStream_t st, const void* feat, int nseq, 
                       const int* row_limit, const int* page_table) {
   const dflow_dims& d = c->dm;
   const int M = nseq * Bq;
-  const int kt = d.d / c->KT;
   hipError_t e;
   for (int l = 0; l < d.n_draft_layers; ++l) {
     const dflow_layer& L = c->dlayers[l];
-    const void* wkv = strip_ptr(L.wqkv, c->q_dim / 16, kt);
-    if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, wkv, M, 2 * c->kv_dim, d.d, c->qkv, 2 * c->kv_dim))) return e;
+    if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, L.wkv_ctx, M, 2 * c->kv_dim, d.d, c->qkv, 2 * c->kv_dim))) return e;
     if ((e = qk_rope(c, st, L, c->qkv, 2 * c->kv_dim, nseq, Bq, 0, start_pos, row_limit, page_table,
                      pool_layer(c, c->c.ck_pool, l), pool_layer(c, c->c.cv_pool, l))))
       return e;
@@ -488,7 +512,7 @@ extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_
     const int n = (len - p0) < d.max_rows ? (len - p0) : d.max_rows;
     const bool last = p0 + n >= len;
     HIPCHK(launch_set_int(c->tmp_pos, p0, st));
-    HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, st));
+    HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
     HIPCHK(target_forward(c, st, 1, n, c->tmp_pos, pt, last ? c->tmp_argmax : nullptr, nullptr, n - 1, 1));
     HIPCHK(project(c, st, n, c->fpre));
     HIPCHK(ctx_append(c, st, c->fpre, 1, n, c->tmp_pos, nullptr, pt));
@@ -515,13 +539,15 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
                 2 * d.d, nullptr, 0, nullptr, 0, c->w.relay_c2));
   }
   HIPCHK(launch_relay_input(c->bf, carry_on ? 1 : 0, c->carry_rec, anchor_tok, c->w.embed, c->w.e_mask, c->f, c->bg,
-                            c->w.relay_ln_g, c->w.relay_ln_b, d.ln_eps, nseq, B, d.d, d.vocab, c->x, c->status, st));
+                            c->w.relay_ln_g, c->w.relay_ln_b, d.ln_eps, nseq, B, d.d, d.vocab, c->x, c->status,
+                            c->ssq, SSQ_LD, st));
   for (int l = 0; l < d.n_draft_layers; ++l)
     HIPCHK(decoder_layer(c, st, c->dlayers[l], nseq, B, anchor_pos, c->c.page_table, pool_layer(c, c->c.ck_pool, l),
                          pool_layer(c, c->c.cv_pool, l), 0, nullptr));
-  HIPCHK(launch_rmsnorm(c->bf, false, c->x, d.d, M, d.d, c->w.draft_final_norm, d.rms_eps, c->xn, d.d, st));
-  HIPCHK(gemm(c, st, EPI_ARGMAX, c->xn, d.d, c->w.lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
-              nullptr, draft_logits, d.vocab));
+  NormIn fin;
+  fin.ssq = c->ssq;
+  HIPCHK(gemm(c, st, EPI_ARGMAX, c->x, d.d, c->w.draft_lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
+              nullptr, draft_logits, d.vocab, fin));
   HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, M, c->row_argmax, st));
   HIPCHK(launch_draft_assemble(c->row_argmax, anchor_tok, nseq, B, draft_tok, block_out, st));
   return DFLOW_OK;
@@ -534,7 +560,7 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
   if (!block_tok || !start_pos || !tgt_argmax) return fail(DFLOW_EINVAL, "verify_block: null argument");
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, st));
+  HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
   HIPCHK(target_forward(c, st, nseq, B, start_pos, c->c.page_table, tgt_argmax, logits));
   if (hcap)
     HIPCHK(hipMemcpyAsync(hcap, c->hcap, (size_t)M * d.n_capture * d.d * c->elt, hipMemcpyDeviceToDevice, st));

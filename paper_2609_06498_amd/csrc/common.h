@@ -9,11 +9,13 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 // global-address-space view of 16-byte fragments (loads compile to global_load_dwordx4)
 typedef const __attribute__((address_space(1))) u32x4_t gu4;
+typedef const __attribute__((address_space(1))) float gf32;
 
 namespace dflow {
 
 constexpr int WAVE = 64;
 constexpr int PAGE = 64;          // KV page size in tokens (also the attention sub-chunk)
+constexpr int SSQ_LD = 512;       // row stride of the RMSNorm partial sums [row][strip] (d <= 16 * SSQ_LD)
 // keys per attention split (fixed absolute positions): 4 pages bf16, 2 pages fp32,
 // so the staged K+V pages of a split fit the 160 KB LDS of a CU
 template <typename T> struct SplitKeys;

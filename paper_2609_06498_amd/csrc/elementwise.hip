@@ -8,26 +8,37 @@
 namespace dflow {
 
 // ---------------------------------------------------------------- embedding
+// Also writes the per-16-column-strip sums of squares of the row (the
+// RMSNorm row scale of the next projection), ssq[row * ssq_ld + c].
 template <typename T>
-__global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, int* status) {
+__global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, int* status, float* ssq, int ssq_ld) {
   const int row = blockIdx.x;
   int t = tok[row];
-  if (t < 0 || t >= V) {
-    if (threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
-    for (int i = threadIdx.x; i < d; i += blockDim.x) TT<T>::st(out, (size_t)row * d + i, 0.f);
-    return;
+  const bool ok = t >= 0 && t < V;
+  if (!ok && threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
+  for (int c = threadIdx.x; c < d / 16; c += blockDim.x) {
+    float sq = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const size_t i = (size_t)c * 16 + e;
+      const float v = ok ? TT<T>::ld(E, (size_t)t * d + i) : 0.f;
+      TT<T>::st(out, (size_t)row * d + i, v);
+      sq += v * v;
+    }
+    if (ssq) ssq[(size_t)row * ssq_ld + c] = sq;
   }
-  for (int i = threadIdx.x; i < d; i += blockDim.x) out[(size_t)row * d + i] = E[(size_t)t * d + i];
 }
 
 hipError_t launch_embed(bool isbf, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
-                        hipStream_t s) {
+                        float* ssq, int ssq_ld, hipStream_t s) {
   if (M <= 0) return hipSuccess;
+  if (d % 16) return hipErrorInvalidValue;
   if (isbf)
-    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(256), 0, s, tok, (const bf16*)E, V, d, (bf16*)out, status);
+    hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(256), 0, s, tok, (const bf16*)E, V, d, (bf16*)out, status,
+                       ssq, ssq_ld);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, tok, (const float*)E, V, d, (float*)out,
-                       status);
+                       status, ssq, ssq_ld);
   return hipGetLastError();
 }
 
@@ -304,61 +315,72 @@ hipError_t launch_relay_gather(bool isbf, int carry_on, const int* carry_rec, co
 }
 
 // x[s*B + 0] = E(anchor); relayed rows: E_mask + beta * LN(h) + gamma; others E_mask.
+// Also writes the per-16-column-strip sums of squares of the stored row.
 template <typename T>
 __global__ void relay_input_kernel(int carry_on, const int* rec, const int* anchor, const T* E, const T* e_mask,
                                    const T* f, const float* bg, const T* ln_g, const T* ln_b, float ln_eps, int B,
-                                   int d, int V, T* x, int* status) {
+                                   int d, int V, T* x, int* status, float* ssq, int ssq_ld) {
   __shared__ float sh[32];
   const int row = blockIdx.x;
   const int s = row / B, i = row - s * B;
   T* xr = x + (size_t)row * d;
-  if (i == 0) {
-    const int t = anchor[s];
-    if (t < 0 || t >= V) {
-      if (threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
-      for (int e = threadIdx.x; e < d; e += blockDim.x) TT<T>::st(xr, e, 0.f);
-      return;
-    }
-    for (int e = threadIdx.x; e < d; e += blockDim.x) xr[e] = E[(size_t)t * d + e];
-    return;
-  }
   const int* r = rec + (size_t)s * CARRY_REC;
-  const bool valid = carry_on && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B && r[2] >= 0 &&
+  const bool relay = i > 0 && carry_on && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B && r[2] >= 0 &&
                      r[2] < V && r[3] >= 0 && r[3] < V;
-  if (!valid) {
-    for (int e = threadIdx.x; e < d; e += blockDim.x) xr[e] = e_mask[e];
-    return;
+  int src_tok = -1;                  // row 0: the anchor's embedding
+  if (i == 0) {
+    src_tok = anchor[s];
+    if (src_tok < 0 || src_tok >= V) {
+      if (threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
+      src_tok = -2;                  // zero row
+    }
   }
-  const T* h = f + ((size_t)s * B + r[1] + i - 1) * d;
-  float sm = 0.f;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) sm += TT<T>::ld(h, e);
-  const float mu = block_sum(sm, sh) / (float)d;
-  float sv = 0.f;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) {
-    const float c = TT<T>::ld(h, e) - mu;
-    sv += c * c;
+  float mu = 0.f, rs = 0.f;
+  const T* h = nullptr;
+  if (relay) {                       // LayerNorm statistics of the carried state (two passes)
+    h = f + ((size_t)s * B + r[1] + i - 1) * d;
+    float sm = 0.f;
+    for (int e = threadIdx.x; e < d; e += blockDim.x) sm += TT<T>::ld(h, e);
+    mu = block_sum(sm, sh) / (float)d;
+    float sv = 0.f;
+    for (int e = threadIdx.x; e < d; e += blockDim.x) {
+      const float c = TT<T>::ld(h, e) - mu;
+      sv += c * c;
+    }
+    rs = rsqrtf(block_sum(sv, sh) / (float)d + ln_eps);
   }
-  const float var = block_sum(sv, sh) / (float)d;
-  const float rs = rsqrtf(var + ln_eps);
   const float* bgr = bg + (size_t)row * 2 * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) {
-    const float ln = (TT<T>::ld(h, e) - mu) * rs * TT<T>::ld(ln_g, e) + TT<T>::ld(ln_b, e);
-    TT<T>::st(xr, e, TT<T>::ld(e_mask, e) + bgr[e] * ln + bgr[d + e]);
+  for (int c = threadIdx.x; c < d / 16; c += blockDim.x) {
+    float sq = 0.f;
+#pragma unroll
+    for (int e16 = 0; e16 < 16; ++e16) {
+      const int e = c * 16 + e16;
+      float v;
+      if (i == 0) v = src_tok >= 0 ? TT<T>::ld(E, (size_t)src_tok * d + e) : 0.f;
+      else if (relay) {
+        const float ln = (TT<T>::ld(h, e) - mu) * rs * TT<T>::ld(ln_g, e) + TT<T>::ld(ln_b, e);
+        v = TT<T>::rnd(TT<T>::ld(e_mask, e) + bgr[e] * ln + bgr[d + e]);
+      } else v = TT<T>::ld(e_mask, e);
+      TT<T>::st(xr, e, v);
+      sq += v * v;
+    }
+    if (ssq) ssq[(size_t)row * ssq_ld + c] = sq;
   }
 }
 
 hipError_t launch_relay_input(bool isbf, int carry_on, const int* carry_rec, const int* anchor, const void* E,
                               const void* e_mask, const void* f, const float* bg, const void* ln_g,
                               const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
-                              hipStream_t s) {
+                              float* ssq, int ssq_ld, hipStream_t s) {
+  if (d % 16) return hipErrorInvalidValue;
   if (isbf)
     hipLaunchKernelGGL(relay_input_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
                        (const bf16*)E, (const bf16*)e_mask, (const bf16*)f, bg, (const bf16*)ln_g,
-                       (const bf16*)ln_b, ln_eps, B, d, V, (bf16*)x, status);
+                       (const bf16*)ln_b, ln_eps, B, d, V, (bf16*)x, status, ssq, ssq_ld);
   else
     hipLaunchKernelGGL(relay_input_kernel<float>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
                        (const float*)E, (const float*)e_mask, (const float*)f, bg, (const float*)ln_g,
-                       (const float*)ln_b, ln_eps, B, d, V, (float*)x, status);
+                       (const float*)ln_b, ln_eps, B, d, V, (float*)x, status, ssq, ssq_ld);
   return hipGetLastError();
 }
 

@@ -13,7 +13,7 @@
 
 namespace dflow {
 
-template <typename T, int NG, int MT, int EPI>
+template <typename T, int NG, int MT, int EPI, bool NORM>
 __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   constexpr int KL = TT<T>::KL;
   constexpr int KT = TT<T>::KT;
@@ -71,13 +71,38 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                      \
       _Pragma("unroll") for (int j = 0; j < NG; ++j) acc[i][j] = mma_frag(T(), aq[st][u][i], bq[st][u][j], acc[i][j]);
 
+  // RMSNorm row scales.  The norm gain is folded into the packed weight, so
+  // the normalised projection is rs[m] * (x W'^T) and the scale is applied in
+  // the epilogue.  rs comes from the per-strip sums of squares ssq[m][c] that
+  // the producer of x left behind: lane q of a 16-lane group sums strips
+  // c = q (mod 16) in increasing c, then a fixed butterfly over the group --
+  // the same order for every row, batch and launch shape.  Group g owns rows
+  // g + k * ngrp; the partials of strips c < 256 for its first two rows are
+  // loaded here, ahead of the weights, and consumed after the main loop, so
+  // the reduction costs no latency on the critical path.
+  constexpr int EL = 16;                  // early partials per lane and row
+  const int q16 = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
+  float ea[NORM ? EL : 1], eb[NORM ? EL : 1];
+  if constexpr (NORM) {
+    // rows of a group are clamped to valid rows and strips read the padded
+    // row (ssq_ld >= 256 entries), so every load is unconditional
+    gf32* ra = (gf32*)(p.ssq) + (size_t)min(grp, M - 1) * p.ssq_ld + q16;
+    gf32* rb = (gf32*)(p.ssq) + (size_t)min(grp + ngrp, M - 1) * p.ssq_ld + q16;
+#pragma unroll
+    for (int it = 0; it < EL; ++it) {
+      ea[it] = ra[16 * it];
+      eb[it] = rb[16 * it];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
   // Full stages of U tiles, double-buffered.  Inside the steady-state loop
   // every load is unconditional, so the compiler's wait before each compute
   // covers only the stage being consumed, never the prefetch just issued.
   const int nst = (ke - kb) / U;
   int kt = kb;
+  if (nst > 0) { DFLOW_LOAD(0, kt); }
   if (nst > 0) {
-    DFLOW_LOAD(0, kt);
     int left = nst;
     while (left > 2) {
       DFLOW_LOAD(1, kt + U);
@@ -112,6 +137,51 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
 #undef DFLOW_LOAD
 #undef DFLOW_COMPUTE
 
+  __shared__ float s_rs[NORM ? MT * 16 : 1];
+  if constexpr (NORM) {
+    const int np = p.ssq_parts;
+    for (int m0 = grp; m0 < MT * 16; m0 += 2 * ngrp) {
+      const int ma = min(m0, M - 1), mb = min(m0 + ngrp, M - 1);
+      float sa = 0.f, sb = 0.f;
+      if (m0 == grp) {
+#pragma unroll
+        for (int it = 0; it < EL; ++it) {
+          const bool ok = q16 + 16 * it < np;
+          sa += ok ? ea[it] : 0.f;
+          sb += ok ? eb[it] : 0.f;
+        }
+      } else {
+        gf32* ra = (gf32*)(p.ssq) + (size_t)ma * p.ssq_ld + q16;
+        gf32* rb = (gf32*)(p.ssq) + (size_t)mb * p.ssq_ld + q16;
+        float la[EL], lb[EL];
+#pragma unroll
+        for (int it = 0; it < EL; ++it) {
+          la[it] = ra[16 * it];
+          lb[it] = rb[16 * it];
+        }
+#pragma unroll
+        for (int it = 0; it < EL; ++it) {
+          const bool ok = q16 + 16 * it < np;
+          sa += ok ? la[it] : 0.f;
+          sb += ok ? lb[it] : 0.f;
+        }
+      }
+      for (int c = q16 + 16 * EL; c < np; c += 16) {   // strips beyond the early window (d > 4096)
+        sa += p.ssq[(size_t)ma * p.ssq_ld + c];
+        sb += p.ssq[(size_t)mb * p.ssq_ld + c];
+      }
+#pragma unroll
+      for (int x = 8; x >= 1; x >>= 1) {
+        sa += __shfl_xor(sa, x, 16);
+        sb += __shfl_xor(sb, x, 16);
+      }
+      if (q16 == 0) {
+        s_rs[m0] = rsqrtf(sa / (float)(np * 16) + p.eps);
+        if (m0 + ngrp < MT * 16) s_rs[m0 + ngrp] = rsqrtf(sb / (float)(np * 16) + p.eps);
+      }
+    }
+  }
+
   // ---- cross-wave reduction in fixed wave order, one m tile at a time
   float* red = lds;                                 // [nw][NG][64][4]
   constexpr int CW = NG * 16 + 1;                   // padded C-tile row
@@ -139,8 +209,11 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   if constexpr (EPI == EPI_ARGMAX) {
     for (int e = threadIdx.x; e < M * ncols; e += blockDim.x) {
       const int m = e / ncols, n = e - m * ncols;
-      if (p.logits) p.logits[(size_t)m * p.ldl + colbase + n] = ct[m * CW + n];
+      float v = ct[m * CW + n];
+      if constexpr (NORM) ct[m * CW + n] = v = v * s_rs[m];
+      if (p.logits) p.logits[(size_t)m * p.ldl + colbase + n] = v;
     }
+    __syncthreads();
     for (int m = threadIdx.x; m < M; m += blockDim.x) {
       float best = ct[m * CW];
       int bi = 0;
@@ -157,8 +230,12 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
     for (int e = threadIdx.x; e < M * half; e += blockDim.x) {
       const int m = e / half, c = e - m * half;
       const int strip = c >> 3, cc = c & 7;
-      const float gt = ct[m * CW + strip * 16 + cc];
-      const float up = ct[m * CW + strip * 16 + 8 + cc];
+      float gt = ct[m * CW + strip * 16 + cc];
+      float up = ct[m * CW + strip * 16 + 8 + cc];
+      if constexpr (NORM) {
+        gt *= s_rs[m];
+        up *= s_rs[m];
+      }
       TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + obase + c, silu(gt) * up);
     }
   } else {
@@ -166,20 +243,37 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
       const int m = e / ncols, n = e - m * ncols;
       const int col = colbase + n;
       float v = ct[m * CW + n];
+      if constexpr (NORM) v *= s_rs[m];
       if constexpr (EPI == EPI_STORE_T) {
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
       } else if constexpr (EPI == EPI_STORE_F32) {
         reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
       } else if constexpr (EPI == EPI_RESID) {
-        v += TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col);
+        v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col));
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
         if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), (size_t)m * p.ldy2 + col, v);
+        ct[m * CW + n] = v;
       } else if constexpr (EPI == EPI_BIAS_SILU) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, silu(v));
       } else if constexpr (EPI == EPI_BIAS_F32) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
+      }
+    }
+    if constexpr (EPI == EPI_RESID) {
+      if (p.ssq_out) {   // sum of squares of the stored values, per row and 16-column strip
+        __syncthreads();
+        for (int e = threadIdx.x; e < M * nvalid; e += blockDim.x) {
+          const int m = e / nvalid, j = e - m * nvalid;
+          float sq = 0.f;
+#pragma unroll
+          for (int c = 0; c < 16; ++c) {
+            const float v = ct[m * CW + j * 16 + c];
+            sq += v * v;
+          }
+          p.ssq_out[(size_t)m * p.ssq_out_ld + nt0 + j] = sq;
+        }
       }
     }
   }
@@ -202,8 +296,8 @@ GemmShape gemm_shape(int ntiles, int ktiles, int epi) {
   return s;
 }
 
-template <typename T, int NG, int EPI>
-static hipError_t launch_mt(const GemmParams& p, const GemmShape& sh, hipStream_t st) {
+template <typename T, int NG, int EPI, bool NORM>
+static hipError_t launch_mtn(const GemmParams& p, const GemmShape& sh, hipStream_t st) {
   const int mt = (p.M + 15) / 16;
   const int cw = NG * 16 + 1;
   auto go = [&](auto kern, int MTv) {
@@ -212,11 +306,24 @@ static hipError_t launch_mt(const GemmParams& p, const GemmShape& sh, hipStream_
     hipLaunchKernelGGL(kern, dim3(sh.groups), dim3(sh.waves * 64), lds, st, p);
     return hipGetLastError();
   };
-  if (mt <= 1) return go(gemm_kernel<T, NG, 1, EPI>, 1);
-  if (mt <= 2) return go(gemm_kernel<T, NG, 2, EPI>, 2);
-  if (mt <= 4) return go(gemm_kernel<T, NG, 4, EPI>, 4);
-  if (mt <= 8) return go(gemm_kernel<T, NG, 8, EPI>, 8);
+  if (mt <= 1) return go(gemm_kernel<T, NG, 1, EPI, NORM>, 1);
+  if (mt <= 2) return go(gemm_kernel<T, NG, 2, EPI, NORM>, 2);
+  if (mt <= 4) return go(gemm_kernel<T, NG, 4, EPI, NORM>, 4);
+  if (mt <= 8) return go(gemm_kernel<T, NG, 8, EPI, NORM>, 8);
   return hipErrorInvalidValue;
+}
+
+// The RMSNorm row scale is instantiated only for the projections that follow a norm.
+template <int EPI> struct HasNorm { static constexpr bool value = EPI == EPI_STORE_T || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX; };
+
+template <typename T, int NG, int EPI>
+static hipError_t launch_mt(const GemmParams& p, const GemmShape& sh, hipStream_t st) {
+  if constexpr (HasNorm<EPI>::value) {
+    if (p.norm) return launch_mtn<T, NG, EPI, true>(p, sh, st);
+  } else {
+    if (p.norm) return hipErrorInvalidValue;
+  }
+  return launch_mtn<T, NG, EPI, false>(p, sh, st);
 }
 
 template <typename T, int EPI>
@@ -245,11 +352,14 @@ hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t st) 
 }
 
 // ------------------------------------------------------------------ packing
-// out tile (nt, kt) lane l element e <- W[src_row(nt, l%16)][kt*KT + (l/16)*KL + e]
+// out tile (nt, kt) lane l element e <- W[src_row(nt, l%16)][kt*KT + (l/16)*KL + e] * gain[col]
 // gate_up: W is [2F, K] = [gate; up]; packed strip i holds gate rows 8i..8i+7
-// followed by up rows 8i..8i+7, so one strip yields 8 SwiGLU outputs.
+// followed by up rows 8i..8i+7, so one strip yields 8 SwiGLU outputs.  The
+// optional column gain (the RMSNorm gain of the rows this weight multiplies)
+// is applied in fp32 and rounded once to the storage type.
 template <typename T>
-__global__ void pack_kernel(const T* __restrict__ W, int N, int K, int gate_up, T* __restrict__ out) {
+__global__ void pack_kernel(const T* __restrict__ W, int N, int K, int gate_up, const T* __restrict__ gain,
+                            T* __restrict__ out) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
   const int ktiles = K / KT;
   const size_t total = (size_t)N * K;
@@ -264,21 +374,25 @@ __global__ void pack_kernel(const T* __restrict__ W, int N, int K, int gate_up, 
     size_t row = (size_t)nt * 16 + r16;
     if (gate_up) row = (r16 < 8) ? (size_t)nt * 8 + r16 : (size_t)N / 2 + (size_t)nt * 8 + (r16 - 8);
     const size_t col = (size_t)kt * KT + (l >> 4) * KL + e;
-    out[o] = W[row * K + col];
+    if (gain)
+      TT<T>::st(out, o, TT<T>::ld(W, row * K + col) * TT<T>::ld(gain, col));
+    else
+      out[o] = W[row * K + col];
   }
 }
 
-hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, void* out, hipStream_t s) {
+hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
+                       hipStream_t s) {
   const int threads = 256;
   const size_t total = (size_t)N * K;
   int blocks = (int)((total + threads - 1) / threads);
   if (blocks > 65536) blocks = 65536;
   if (bf16)
-    hipLaunchKernelGGL(pack_kernel<dflow::bf16>, dim3(blocks), dim3(threads), 0, s,
-                       (const dflow::bf16*)w, N, K, gate_up, (dflow::bf16*)out);
+    hipLaunchKernelGGL(pack_kernel<dflow::bf16>, dim3(blocks), dim3(threads), 0, s, (const dflow::bf16*)w, N, K,
+                       gate_up, (const dflow::bf16*)col_gain, (dflow::bf16*)out);
   else
     hipLaunchKernelGGL(pack_kernel<float>, dim3(blocks), dim3(threads), 0, s, (const float*)w, N, K, gate_up,
-                       (float*)out);
+                       (const float*)col_gain, (float*)out);
   return hipGetLastError();
 }
 

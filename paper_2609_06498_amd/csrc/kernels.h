@@ -27,12 +27,22 @@ struct GemmParams {
   uint64_t* amax; int amax_ld;      // [groups][amax_ld] argmax keys
   float* logits; int ldl;           // optional fp32 logits
   int col0;                         // first output column of this range (argmax indices, bias)
+  // RMSNorm row scale (norm = 1): A rows are the raw x, the norm gain is
+  // folded into W, and every output of row m is scaled by rs[m] =
+  // (sum_c ssq[m * ssq_ld + c] / (16 ssq_parts) + eps)^(-1/2).  Rows are
+  // padded: ssq_ld >= max(256, ssq_parts) entries are readable.
+  int norm;
+  const float* ssq; int ssq_ld; int ssq_parts;
+  float eps;
+  // EPI_RESID: per-16-column-strip sums of squares of the stored rows, [m * ssq_out_ld + strip]
+  float* ssq_out; int ssq_out_ld;
 };
 
 struct GemmShape { int ng; int waves; int groups; };
 GemmShape gemm_shape(int ntiles, int ktiles, int epi);
 hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
-hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, void* out, hipStream_t s);
+hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
+                       hipStream_t s);
 
 }  // namespace dflow
 
@@ -84,7 +94,7 @@ struct RopeParams {
 };
 
 hipError_t launch_embed(bool bf16, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
-                        hipStream_t s);
+                        float* ssq, int ssq_ld, hipStream_t s);
 hipError_t launch_rmsnorm(bool bf16, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
                           void* out, int ldo, hipStream_t s);
 hipError_t launch_qk_rope_write(bool bf16, const RopeParams& p, hipStream_t s);
@@ -98,7 +108,7 @@ hipError_t launch_relay_gather(bool bf16, int carry_on, const int* carry_rec, co
 hipError_t launch_relay_input(bool bf16, int carry_on, const int* carry_rec, const int* anchor, const void* E,
                               const void* e_mask, const void* f, const float* bg, const void* ln_g,
                               const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
-                              hipStream_t s);
+                              float* ssq, int ssq_ld, hipStream_t s);
 hipError_t launch_commit(const int* accept_len, int nseq, int* seq_len, hipStream_t s);
 hipError_t launch_force(const int* traj, int traj_stride, int traj_len, const signed char* mode, const int* tok,
                         const int* anchor, const int* start_pos, int nseq, int B, int V, int* block_tok,

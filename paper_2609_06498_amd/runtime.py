@@ -40,13 +40,13 @@ class Dims(ctypes.Structure):
 
 class Layer(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
-                ("attn_norm", "wqkv", "q_norm", "k_norm", "wo", "ffn_norm", "wgu", "wdown")]
+                ("wqkv", "q_norm", "k_norm", "wo", "wgu", "wdown", "wkv_ctx")]
 
 
 class Weights(ctypes.Structure):
-    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
+    _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
                 ("layers", ctypes.POINTER(Layer)), ("draft_layers", ctypes.POINTER(Layer)),
-                ("draft_final_norm", ctypes.c_void_p), ("e_mask", ctypes.c_void_p), ("w_c", ctypes.c_void_p),
+                ("draft_lm_head", ctypes.c_void_p), ("e_mask", ctypes.c_void_p), ("w_c", ctypes.c_void_p),
                 ("g_c", ctypes.c_void_p), ("relay_w1", ctypes.c_void_p), ("relay_c1", ctypes.c_void_p),
                 ("relay_w2", ctypes.c_void_p), ("relay_c2", ctypes.c_void_p), ("relay_ln_g", ctypes.c_void_p),
                 ("relay_ln_b", ctypes.c_void_p)]
@@ -61,7 +61,7 @@ EXPORTS = {
     "dflow_last_error": (ctypes.c_char_p, []),
     "dflow_packed_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "dflow_pack_linear": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
-                                         ctypes.c_int, ctypes.c_void_p]),
+                                         ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Dims)]),
     "dflow_create": (ctypes.c_int, [ctypes.POINTER(Dims), ctypes.POINTER(Weights), ctypes.POINTER(Cache),
                                     ctypes.POINTER(ctypes.c_void_p)]),
@@ -157,14 +157,14 @@ class Runtime:
         up = self._upload
         W = Weights()
         W.embed = up(weights["embed"])
-        W.final_norm = up(weights["final_norm"])
-        W.lm_head = self._packed(weights["lm_head"])
+        # RMSNorm gains that precede a projection are folded into its packed weight
+        W.lm_head = self._packed(weights["lm_head"], gain=weights["final_norm"])
         self.layers = (Layer * dims.n_layers)(*[self._layer(weights, f"layers.{l}") for l in range(dims.n_layers)])
         self.dlayers = (Layer * dims.n_draft_layers)(
-            *[self._layer(weights, f"draft.layers.{l}") for l in range(dims.n_draft_layers)])
+            *[self._layer(weights, f"draft.layers.{l}", draft=True) for l in range(dims.n_draft_layers)])
         W.layers = self.layers
         W.draft_layers = self.dlayers
-        W.draft_final_norm = up(weights["draft.final_norm"])
+        W.draft_lm_head = self._packed(weights["lm_head"], gain=weights["draft.final_norm"])
         W.e_mask = up(weights["draft.e_mask"])
         W.w_c = self._packed(weights["draft.w_c"])
         W.g_c = up(weights["draft.g_c"])
@@ -205,27 +205,31 @@ class Runtime:
             return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(self.device)
         return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.device)
 
-    def _packed(self, a: np.ndarray, gate_up: int = 0):
+    def _packed(self, a: np.ndarray, gate_up: int = 0, gain: Optional[np.ndarray] = None):
         N, K = a.shape
         src = self._to_dev(a)
+        g = self._to_dev(gain) if gain is not None else None
         out = self.torch.empty_like(src)
         self._check(self.lib.dflow_pack_linear(_stream(), self.dtype_code, src.data_ptr(), N, K, gate_up,
-                                               out.data_ptr()), "dflow_pack_linear")
+                                               g.data_ptr() if g is not None else None, out.data_ptr()),
+                    "dflow_pack_linear")
         self.torch.cuda.current_stream().synchronize()
-        del src
+        del src, g
         self._keep.append(out)
         return out.data_ptr()
 
-    def _layer(self, w, p) -> Layer:
+    def _layer(self, w, p, draft: bool = False) -> Layer:
         L = Layer()
-        L.attn_norm = self._upload(w[f"{p}.attn_norm"])
-        L.wqkv = self._packed(np.concatenate([w[f"{p}.wq"], w[f"{p}.wk"], w[f"{p}.wv"]]))
+        L.wqkv = self._packed(np.concatenate([w[f"{p}.wq"], w[f"{p}.wk"], w[f"{p}.wv"]]),
+                              gain=w[f"{p}.attn_norm"])
         L.q_norm = self._upload(w[f"{p}.q_norm"])
         L.k_norm = self._upload(w[f"{p}.k_norm"])
         L.wo = self._packed(w[f"{p}.wo"])
-        L.ffn_norm = self._upload(w[f"{p}.ffn_norm"])
-        L.wgu = self._packed(np.concatenate([w[f"{p}.w_gate"], w[f"{p}.w_up"]]), gate_up=1)
+        L.wgu = self._packed(np.concatenate([w[f"{p}.w_gate"], w[f"{p}.w_up"]]), gate_up=1,
+                             gain=w[f"{p}.ffn_norm"])
         L.wdown = self._packed(w[f"{p}.w_down"])
+        if draft:   # the context features F enter K/V without the layer's attention norm
+            L.wkv_ctx = self._packed(np.concatenate([w[f"{p}.wk"], w[f"{p}.wv"]]))
         return L
 
     # ------------------------------------------------------------ calls

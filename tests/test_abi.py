@@ -50,8 +50,8 @@ def test_validation_errors_without_device(lib):
     d.d, d.n_layers, d.n_heads, d.n_kv_heads, d.head_dim = 512, 2, 8, 2, 96
     assert lib.dflow_workspace_bytes(ctypes.byref(d)) == 0
     assert "head_dim" in lib.dflow_last_error().decode()
-    assert lib.dflow_pack_linear(None, 1, None, 16, 32, 0, None) == -1
-    assert lib.dflow_pack_linear(None, 1, ctypes.c_void_p(16), 16, 48, 0, ctypes.c_void_p(16)) == -2
+    assert lib.dflow_pack_linear(None, 1, None, 16, 32, 0, None, None) == -1
+    assert lib.dflow_pack_linear(None, 1, ctypes.c_void_p(16), 16, 48, 0, None, ctypes.c_void_p(16)) == -2
     assert lib.dflow_create(None, None, None, None) == -1
     assert lib.dflow_packed_bytes(1, 32, 64) == 32 * 64 * 2
     assert lib.dflow_packed_bytes(0, 32, 64) == 32 * 64 * 4
