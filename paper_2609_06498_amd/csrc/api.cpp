@@ -62,6 +62,8 @@ struct dflow_ctx {
   uint64_t* amax;
   int *row_argmax, *carry_rec, *status, *tmp_pos, *tmp_argmax;
   float* ssq;   // [mmax][SSQ_LD] sums of squares of x per 16-column strip (RMSNorm row scales)
+  uint64_t* amax_part;   // [ARGMAX_SPLITS][mmax]
+  unsigned* counters;    // arrival counters of last-workgroup reductions; every launch leaves them at 0
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -164,13 +166,15 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)items * d->n_kv_heads * nsplit * 16 * d->head_dim * 4);  // 11 part_o
   add((size_t)items * d->n_kv_heads * nsplit * 32 * 4);               // 12 part_ml
   add((size_t)d->max_pages * PAGE * (d->head_dim / 2) * sizeof(float2));  // 13 rope
-  add((size_t)lm_groups * mmax * 8);                   // 14 amax
+  add((size_t)lm_groups * mmax * 8);                   // 14 amax: [lm_groups][rows] argmax keys
   add((size_t)mmax * 4);                               // 15 row_argmax
   add((size_t)d->max_batch * CARRY_REC * 4);           // 16 carry_rec
   add(4);                                              // 17 status
   add((size_t)(d->max_batch + 1) * 4);                 // 18 tmp_pos
   add((size_t)mmax * 4);                               // 19 tmp_argmax
   add((size_t)mmax * SSQ_LD * 4);                      // 20 ssq: per-strip sums of squares of the residual rows
+  add((size_t)ARGMAX_SPLITS * mmax * 8);               // 21 amax_part: [split][row] partial argmax keys
+  add(256);                                            // 22 counters (zero between launches)
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -253,6 +257,8 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->tmp_pos = (int*)(b + L.off[18]);
   c->tmp_argmax = (int*)(b + L.off[19]);
   c->ssq = (float*)(b + L.off[20]);
+  c->amax_part = (uint64_t*)(b + L.off[21]);
+  c->counters = (unsigned*)(b + L.off[22]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -323,7 +329,7 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
   p.ldy2 = ldy2;
   p.bias = bias;
   p.amax = c->amax;
-  p.amax_ld = c->mmax;
+  p.amax_ld = M;   // keys [group][row], compact for this launch
   p.logits = logits;
   p.ldl = ldl;
   p.col0 = 0;
@@ -462,7 +468,7 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
   if ((e = gemm(c, st, EPI_ARGMAX, (char*)c->x + off, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr,
                 0, nullptr, 0, nullptr, logits, d.vocab, fin)))
     return e;
-  return launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, lm_rows, argmax_out, st);
+  return launch_argmax_reduce(c->amax, c->lm_groups, lm_rows, c->amax_part, c->counters, argmax_out, st);
 }
 
 // F = RMSNorm(W_c [captured states]) for M rows -> fout (storage type)
@@ -548,7 +554,7 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   fin.ssq = c->ssq;
   HIPCHK(gemm(c, st, EPI_ARGMAX, c->x, d.d, c->w.draft_lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
               nullptr, draft_logits, d.vocab, fin));
-  HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, c->mmax, M, c->row_argmax, st));
+  HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, M, c->amax_part, c->counters, c->row_argmax, st));
   HIPCHK(launch_draft_assemble(c->row_argmax, anchor_tok, nseq, B, draft_tok, block_out, st));
   return DFLOW_OK;
 }

@@ -59,6 +59,46 @@ template <> struct TT<float> {
   __device__ static inline float rnd(float v) { return v; }
 };
 
+// 16 consecutive elements (16-byte aligned) <-> fp32, stores rounded to the storage type
+template <typename T> struct Row16;
+template <> struct Row16<bf16> {
+  __device__ static inline void load(const bf16* p, float* v) {
+    const uint4* q = reinterpret_cast<const uint4*>(p);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint4 u = q[h];
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { v[8 * h + 2 * i] = bf2f(w[i] & 0xFFFF); v[8 * h + 2 * i + 1] = bf2f(w[i] >> 16); }
+    }
+  }
+  __device__ static inline void store(bf16* p, const float* v) {
+    uint4* q = reinterpret_cast<uint4*>(p);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[8 * h + 2 * i]) | ((uint32_t)f2bf(v[8 * h + 2 * i + 1]) << 16);
+      q[h] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  }
+};
+template <> struct Row16<float> {
+  __device__ static inline void load(const float* p, float* v) {
+    const float4* q = reinterpret_cast<const float4*>(p);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const float4 u = q[h];
+      v[4 * h] = u.x; v[4 * h + 1] = u.y; v[4 * h + 2] = u.z; v[4 * h + 3] = u.w;
+    }
+  }
+  __device__ static inline void store(float* p, const float* v) {
+    float4* q = reinterpret_cast<float4*>(p);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) q[h] = make_float4(v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]);
+  }
+};
+
 // acc(16x16) += A(16 x k) * B(k x 16) over one 16-byte lane fragment pair.
 // Lane l supplies row (l%16) of A and column (l%16) of B, k-group l/16.
 __device__ inline f32x4_t mma_frag(bf16, const uint4& a, const uint4& b, f32x4_t acc) {

@@ -200,26 +200,72 @@ hipError_t launch_qk_rope_write(bool isbf, const RopeParams& p, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------- argmax
-__global__ void argmax_reduce_kernel(const uint64_t* amax, int groups, int ld, int* out) {
-  __shared__ uint64_t sh[256];
-  const int row = blockIdx.x;
-  uint64_t best = 0;
-  for (int g = threadIdx.x; g < groups; g += blockDim.x) {
-    const uint64_t k = amax[(size_t)g * ld + row];
-    best = k > best ? k : best;
-  }
-  sh[threadIdx.x] = best;
-  __syncthreads();
-  for (int w = blockDim.x / 2; w > 0; w >>= 1) {
-    if (threadIdx.x < w) sh[threadIdx.x] = sh[threadIdx.x + w] > sh[threadIdx.x] ? sh[threadIdx.x + w] : sh[threadIdx.x];
+// Keys are [group][M].  Workgroup b takes a contiguous range of groups; its
+// lane t reads row t%16 (+16 per row batch) of groups t/16, t/16 + 16, ...,
+// so 16 consecutive lanes read one contiguous 128-byte run.  Each workgroup
+// leaves its per-row maxima in part[b][m]; the last workgroup to arrive
+// (device-scope counter, reset by that workgroup) reduces the partials and
+// writes the indices.  Max is order-independent, so the result does not
+// depend on arrival order.
+__global__ void __launch_bounds__(256) argmax_reduce_kernel(const uint64_t* amax, int groups, int M, uint64_t* part,
+                                                            unsigned* counter, int* out) {
+  __shared__ uint64_t sh[16][17];
+  __shared__ bool s_last;
+  const int r16 = threadIdx.x & 15, slice = threadIdx.x >> 4;
+  const int per = (groups + gridDim.x - 1) / gridDim.x;
+  const int g0 = blockIdx.x * per, g1 = min(groups, g0 + per);
+  for (int m0 = 0; m0 < M; m0 += 16) {
+    const int m = m0 + r16, mc = min(m, M - 1);
+    uint64_t best = 0;
+#pragma unroll 4
+    for (int g = g0 + slice; g < g1; g += 16) {
+      const uint64_t k = amax[(size_t)g * M + mc];
+      best = k > best ? k : best;
+    }
+    sh[slice][r16] = best;
+    __syncthreads();
+    if (threadIdx.x < 16 && m < M) {
+      uint64_t b = sh[0][r16];
+      for (int i = 1; i < 16; ++i) b = sh[i][r16] > b ? sh[i][r16] : b;
+      part[(size_t)blockIdx.x * M + m] = b;
+    }
     __syncthreads();
   }
-  if (threadIdx.x == 0) out[row] = argmax_key_index(sh[0]);
+  // publish this workgroup's partials, then count arrivals
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(counter, 1u) == gridDim.x - 1;
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  // lane (slice, r16) folds partials of workgroups slice, slice + 16, ... (independent loads)
+  for (int m0 = 0; m0 < M; m0 += 16) {
+    const int m = m0 + r16, mc = min(m, M - 1);
+    uint64_t best = 0;
+#pragma unroll
+    for (int w = slice; w < ARGMAX_SPLITS; w += 16) {
+      if (w < (int)gridDim.x) {
+        const uint64_t k = __hip_atomic_load(part + (size_t)w * M + mc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        best = k > best ? k : best;
+      }
+    }
+    sh[slice][r16] = best;
+    __syncthreads();
+    if (threadIdx.x < 16 && m < M) {
+      uint64_t b = sh[0][r16];
+      for (int i = 1; i < 16; ++i) b = sh[i][r16] > b ? sh[i][r16] : b;
+      out[m] = argmax_key_index(b);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int ld, int M, int* out, hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(M), dim3(256), 0, s, amax, groups, ld, out);
+hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_t* part, unsigned* counter, int* out,
+                                hipStream_t s) {
+  if (M <= 0 || groups <= 0) return hipSuccess;
+  const int nb = groups < ARGMAX_SPLITS ? groups : ARGMAX_SPLITS;
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(nb), dim3(256), 0, s, amax, groups, M, part, counter, out);
   return hipGetLastError();
 }
 
@@ -281,48 +327,53 @@ hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int ca
 
 // ---------------------------------------------------------------- relay
 // u[s*B + i] = [E(b); E(y_rej); f[s*B + src + i - 1]] for relayed rows 1..n, else 0.
+// One workgroup per (row, segment), 16-byte copies (d * sizeof(T) is a multiple of 16).
 template <typename T>
 __global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, const T* f, int B, int d, int V, T* u) {
-  const int row = blockIdx.x;
+  const int row = blockIdx.x, seg = blockIdx.y;
   const int s = row / B, i = row - s * B;
   const int* r = rec + (size_t)s * CARRY_REC;
   const bool valid = carry_on && i >= 1 && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B &&
                      r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
-  T* ur = u + (size_t)row * 3 * d;
+  uint4* dst = reinterpret_cast<uint4*>(u + ((size_t)row * 3 + seg) * d);
+  const int nvec = d * (int)sizeof(T) / 16;
   if (!valid) {
-    for (int e = threadIdx.x; e < 3 * d; e += blockDim.x) TT<T>::st(ur, e, 0.f);
+    for (int v = threadIdx.x; v < nvec; v += blockDim.x) dst[v] = make_uint4(0u, 0u, 0u, 0u);
     return;
   }
-  const T* eb = E + (size_t)r[2] * d;
-  const T* ey = E + (size_t)r[3] * d;
-  const T* h = f + ((size_t)s * B + r[1] + i - 1) * d;
-  for (int e = threadIdx.x; e < d; e += blockDim.x) {
-    ur[e] = eb[e];
-    ur[d + e] = ey[e];
-    ur[2 * d + e] = h[e];
-  }
+  const T* src = seg == 0 ? E + (size_t)r[2] * d : seg == 1 ? E + (size_t)r[3] * d
+                                                            : f + ((size_t)s * B + r[1] + i - 1) * d;
+  const uint4* sv = reinterpret_cast<const uint4*>(src);
+  for (int v = threadIdx.x; v < nvec; v += blockDim.x) dst[v] = sv[v];
 }
 
 hipError_t launch_relay_gather(bool isbf, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
                                int B, int d, int V, void* u, hipStream_t s) {
+  if (d % 16) return hipErrorInvalidValue;
   if (isbf)
-    hipLaunchKernelGGL(relay_gather_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec,
+    hipLaunchKernelGGL(relay_gather_kernel<bf16>, dim3(nseq * B, 3), dim3(256), 0, s, carry_on, carry_rec,
                        (const bf16*)E, (const bf16*)f, B, d, V, (bf16*)u);
   else
-    hipLaunchKernelGGL(relay_gather_kernel<float>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec,
+    hipLaunchKernelGGL(relay_gather_kernel<float>, dim3(nseq * B, 3), dim3(256), 0, s, carry_on, carry_rec,
                        (const float*)E, (const float*)f, B, d, V, (float*)u);
   return hipGetLastError();
 }
 
 // x[s*B + 0] = E(anchor); relayed rows: E_mask + beta * LN(h) + gamma; others E_mask.
 // Also writes the per-16-column-strip sums of squares of the stored row.
+// Thread t owns the 16-column chunks t, t + 256, ... (d <= 16 * 256 * RC);
+// the carried state is read once and kept in registers for both LayerNorm passes.
 template <typename T>
-__global__ void relay_input_kernel(int carry_on, const int* rec, const int* anchor, const T* E, const T* e_mask,
-                                   const T* f, const float* bg, const T* ln_g, const T* ln_b, float ln_eps, int B,
-                                   int d, int V, T* x, int* status, float* ssq, int ssq_ld) {
+__global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const int* rec, const int* anchor, const T* E,
+                                                          const T* e_mask, const T* f,
+                                                          const float* bg, const T* ln_g, const T* ln_b, float ln_eps,
+                                                          int B, int d, int V, T* x, int* status, float* ssq,
+                                                          int ssq_ld) {
+  constexpr int RC = 2;
   __shared__ float sh[32];
   const int row = blockIdx.x;
   const int s = row / B, i = row - s * B;
+  const int nc = d / 16;
   T* xr = x + (size_t)row * d;
   const int* r = rec + (size_t)s * CARRY_REC;
   const bool relay = i > 0 && carry_on && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B && r[2] >= 0 &&
@@ -335,35 +386,71 @@ __global__ void relay_input_kernel(int carry_on, const int* rec, const int* anch
       src_tok = -2;                  // zero row
     }
   }
+  float hv[RC][16];
   float mu = 0.f, rs = 0.f;
   const T* h = nullptr;
-  if (relay) {                       // LayerNorm statistics of the carried state (two passes)
+  if (relay) {                       // LayerNorm statistics of the carried state (uniform per workgroup)
     h = f + ((size_t)s * B + r[1] + i - 1) * d;
     float sm = 0.f;
-    for (int e = threadIdx.x; e < d; e += blockDim.x) sm += TT<T>::ld(h, e);
+#pragma unroll
+    for (int k = 0; k < RC; ++k) {
+      const int c = threadIdx.x + 256 * k;
+      if (c < nc) {
+        Row16<T>::load(h + (size_t)c * 16, hv[k]);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sm += hv[k][e];
+      }
+    }
     mu = block_sum(sm, sh) / (float)d;
     float sv = 0.f;
-    for (int e = threadIdx.x; e < d; e += blockDim.x) {
-      const float c = TT<T>::ld(h, e) - mu;
-      sv += c * c;
+#pragma unroll
+    for (int k = 0; k < RC; ++k) {
+      const int c = threadIdx.x + 256 * k;
+      if (c < nc)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float t = hv[k][e] - mu;
+          sv += t * t;
+        }
     }
     rs = rsqrtf(block_sum(sv, sh) / (float)d + ln_eps);
   }
   const float* bgr = bg + (size_t)row * 2 * d;
-  for (int c = threadIdx.x; c < d / 16; c += blockDim.x) {
+#pragma unroll
+  for (int k = 0; k < RC; ++k) {
+    const int c = threadIdx.x + 256 * k;
+    if (c >= nc) continue;
+    float v[16];
+    if (i == 0) {
+      if (src_tok >= 0) Row16<T>::load(E + (size_t)src_tok * d + (size_t)c * 16, v);
+      else
+#pragma unroll
+        for (int e = 0; e < 16; ++e) v[e] = 0.f;
+    } else {
+      Row16<T>::load(e_mask + (size_t)c * 16, v);
+      if (relay) {
+        float g[16], b[16];
+        Row16<T>::load(ln_g + (size_t)c * 16, g);
+        Row16<T>::load(ln_b + (size_t)c * 16, b);
+        const float4* be = reinterpret_cast<const float4*>(bgr + (size_t)c * 16);
+        const float4* ga = reinterpret_cast<const float4*>(bgr + d + (size_t)c * 16);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 bq = be[q], gq = ga[q];
+          const float bb[4] = {bq.x, bq.y, bq.z, bq.w}, gg[4] = {gq.x, gq.y, gq.z, gq.w};
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4) {
+            const int e = 4 * q + e4;
+            const float ln = (hv[k][e] - mu) * rs * g[e] + b[e];
+            v[e] = TT<T>::rnd(v[e] + bb[e4] * ln + gg[e4]);
+          }
+        }
+      }
+    }
+    Row16<T>::store(xr + (size_t)c * 16, v);
     float sq = 0.f;
 #pragma unroll
-    for (int e16 = 0; e16 < 16; ++e16) {
-      const int e = c * 16 + e16;
-      float v;
-      if (i == 0) v = src_tok >= 0 ? TT<T>::ld(E, (size_t)src_tok * d + e) : 0.f;
-      else if (relay) {
-        const float ln = (TT<T>::ld(h, e) - mu) * rs * TT<T>::ld(ln_g, e) + TT<T>::ld(ln_b, e);
-        v = TT<T>::rnd(TT<T>::ld(e_mask, e) + bgr[e] * ln + bgr[d + e]);
-      } else v = TT<T>::ld(e_mask, e);
-      TT<T>::st(xr, e, v);
-      sq += v * v;
-    }
+    for (int e = 0; e < 16; ++e) sq += v[e] * v[e];
     if (ssq) ssq[(size_t)row * ssq_ld + c] = sq;
   }
 }
@@ -372,7 +459,7 @@ hipError_t launch_relay_input(bool isbf, int carry_on, const int* carry_rec, con
                               const void* e_mask, const void* f, const float* bg, const void* ln_g,
                               const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
                               float* ssq, int ssq_ld, hipStream_t s) {
-  if (d % 16) return hipErrorInvalidValue;
+  if (d % 16 || d > 16 * 256 * 2) return hipErrorInvalidValue;
   if (isbf)
     hipLaunchKernelGGL(relay_input_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
                        (const bf16*)E, (const bf16*)e_mask, (const bf16*)f, bg, (const bf16*)ln_g,

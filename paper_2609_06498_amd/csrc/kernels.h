@@ -24,7 +24,7 @@ struct GemmParams {
   const void* R; int ldr;
   void* Y2; int ldy2;
   const void* bias;
-  uint64_t* amax; int amax_ld;      // [groups][amax_ld] argmax keys
+  uint64_t* amax; int amax_ld;      // [workgroup][amax_ld] argmax keys
   float* logits; int ldl;           // optional fp32 logits
   int col0;                         // first output column of this range (argmax indices, bias)
   // RMSNorm row scale (norm = 1): A rows are the raw x, the norm gain is
@@ -98,7 +98,9 @@ hipError_t launch_embed(bool bf16, const int* tok, int M, const void* E, int V, 
 hipError_t launch_rmsnorm(bool bf16, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
                           void* out, int ldo, hipStream_t s);
 hipError_t launch_qk_rope_write(bool bf16, const RopeParams& p, hipStream_t s);
-hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int ld, int M, int* out, hipStream_t s);
+constexpr int ARGMAX_SPLITS = 32;   // workgroups of the argmax reduction
+hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_t* part, unsigned* counter, int* out,
+                                hipStream_t s);
 hipError_t launch_draft_assemble(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
                                  int* block_out, hipStream_t s);
 hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
