@@ -352,11 +352,21 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
 
 void* pool_layer(dflow_ctx* c, void* pool, int l) { return (char*)pool + (size_t)l * c->pool_layer_elems * c->elt; }
 
-// Attention of `nseq` sequences x Bq rows over one layer's pools.
-hipError_t attention(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const int* start_pos, const int* page_table,
-                     void* kpool, void* vpool, int causal) {
+// Attention of `nseq` sequences x Bq rows over one layer's pools.  With
+// `fused`, from the raw QKV projection rows (QK-norm, RoPE and the block's
+// KV-cache write happen inside); otherwise from c->q after qk_rope.
+hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nseq, int Bq, const int* start_pos,
+                     const int* page_table, void* kpool, void* vpool, int causal, bool fused) {
   AttnParams a{};
-  a.Q = c->q;
+  a.fused = fused ? 1 : 0;
+  a.q = c->q;
+  a.qkv = c->qkv;
+  a.ld_qkv = c->qkv_n;
+  a.q_norm = L.q_norm;
+  a.k_norm = L.k_norm;
+  a.rope = c->rope;
+  a.eps = c->dm.rms_eps;
+  a.status = c->status;
   a.kpool = kpool;
   a.vpool = vpool;
   a.page_table = page_table;
@@ -429,9 +439,11 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   if ((e = gemm(c, st, EPI_STORE_T, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
                 nullptr, nullptr, 0, attn_n)))
     return e;
-  if ((e = qk_rope(c, st, L, c->qkv, c->qkv_n, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool)))
+  const bool fused = attention_fuses_rope(c->bf, Bq, c->G, d.head_dim);
+  if (!fused &&
+      (e = qk_rope(c, st, L, c->qkv, c->qkv_n, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool)))
     return e;
-  if ((e = attention(c, st, nseq, Bq, start_pos, page_table, kpool, vpool, causal))) return e;
+  if ((e = attention(c, st, L, nseq, Bq, start_pos, page_table, kpool, vpool, causal, fused))) return e;
   if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d, nullptr, 0,
                 nullptr, nullptr, 0, NormIn(), c->ssq)))
     return e;

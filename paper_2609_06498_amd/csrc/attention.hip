@@ -1,19 +1,15 @@
-// Block attention over the paged KV cache with split-KV and GQA row packing.
+// Block attention over the paged KV cache with split-KV and GQA row packing,
+// fused with QK-norm + RoPE of the block's queries and keys and the KV-cache
+// write of the block's rows.
 //
 // Verification (causal = 1): block row j at position t+j attends to keys
 // 0..t+j.  Drafting (causal = 0): every block row attends to every key below
 // t+B (committed-context keys followed by the block's own keys).
 //
-// Workgroup = (sequence, kv head, split of keys at fixed absolute positions:
-// 256 keys for bf16, 128 for fp32).  The split's K and V pages (stored in
-// matrix-core fragment order) are staged into LDS once with 16-byte loads;
-// each wave then owns whole groups of 16 attention rows -- (block row j,
-// query head g of the group) pairs, so the query heads of a group share every
-// K/V byte -- and sweeps the staged pages with an online softmax: S^T = K Q^T
-// on the matrix cores (the exponentiated scores already sit in the A-operand
-// layout of P V), mask, running max/sum, P V.  Splits are merged by the
-// combine kernel in split order, so a row's arithmetic depends only on its
-// own visible keys, at any batch composition.
+// Attention rows are (block row j, query head g of a kv group) pairs packed
+// 16 to a matrix-core tile, so the query heads of a group share every K/V
+// byte.  Splits are merged by the combine kernel in split order, so a row's
+// arithmetic depends only on its own visible keys, at any batch composition.
 #include "common.h"
 #include "kernels.h"
 
@@ -28,10 +24,9 @@ template <typename T>
 __device__ inline f32x4_t mma_pv_frag(const float p[4], const typename VFrag<T>::type& v, f32x4_t acc);
 template <>
 __device__ inline f32x4_t mma_pv_frag<bf16>(const float p[4], const uint2& vb, f32x4_t acc) {
-  short4_t a, b;
-  a[0] = (short)f2bf(p[0]); a[1] = (short)f2bf(p[1]); a[2] = (short)f2bf(p[2]); a[3] = (short)f2bf(p[3]);
-  b[0] = (short)(vb.x & 0xFFFF); b[1] = (short)(vb.x >> 16); b[2] = (short)(vb.y & 0xFFFF); b[3] = (short)(vb.y >> 16);
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc, 0, 0, 0);
+  const uint2 pa = make_uint2(f2bf2(p[0], p[1]), f2bf2(p[2], p[3]));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, pa), __builtin_bit_cast(short4_t, vb),
+                                                  acc, 0, 0, 0);
 }
 template <>
 __device__ inline f32x4_t mma_pv_frag<float>(const float p[4], const float4& vb, f32x4_t acc) {
@@ -42,17 +37,42 @@ __device__ inline f32x4_t mma_pv_frag<float>(const float p[4], const float4& vb,
   return acc;
 }
 
-template <typename T, int DH>
-__global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
+// One workgroup of NW waves per (sequence, kv head, split of SplitKeys keys at
+// fixed absolute positions).
+//  1. The split's K/V pages are staged into LDS, all loads in flight at once.
+//     Meanwhile the waves apply QK-norm + RoPE to the group's R = Bq * G query
+//     rows (one row per wave and pass, one rotate-half pair per lane) into an
+//     LDS query tile, and to the block's own key rows that fall into this
+//     split (V copied).
+//  2. The block rows' keys and values are written into the staged tiles and
+//     into the paged cache.
+//  3. Work units are (16-row group, page subset): with nrg row groups, WPR =
+//     min(pages, NW / nrg) waves share a row group and take pages part,
+//     part + WPR, ... with an online softmax (S^T = K Q^T on the matrix cores,
+//     mask, running max/sum, P V).  Their partials are merged through LDS in
+//     part order and written as this split's partial (m, l, O); with WPR = 1
+//     each wave owns whole row groups and writes directly.
+// WPR depends only on (Bq, G), so a row's arithmetic does not depend on the
+// batch it is part of.
+template <typename T, int DH, int NW, bool FUSED>
+__global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
   constexpr int KS = DH / KT;                 // k steps of S^T
   constexpr int DT = DH / 16;                 // output channel tiles
-  constexpr int NPG = SplitKeys<T>::value / PAGE;   // pages per split
+  constexpr int SK = SplitKeys<T>::value;
+  constexpr int NPG = SK / PAGE;              // pages per split
   constexpr int PG = PAGE * DH;               // elements of one K (or V) page block
+  constexpr int NT = NW * 64;
+  constexpr int HALF = DH / 2;
   typedef typename VFrag<T>::type vfrag_t;
+  constexpr int QLD = DH + KL;                // padded row of the query tile
+  constexpr int MAXB = 4;                     // block rows per wave held in registers (Bq <= 64)
   extern __shared__ __align__(16) unsigned char smem[];
-  T* lk = reinterpret_cast<T*>(smem);         // [2][PG] keys, fragment order (double buffer)
-  T* lv = lk + (size_t)2 * PG;                // [2][PG] values, fragment order
+  T* lk = reinterpret_cast<T*>(smem);         // [NPG][PG] keys, fragment order
+  T* lv = lk + (size_t)NPG * PG;              // [NPG][PG] values, fragment order
+  T* lq = lv + (size_t)NPG * PG;              // [R][QLD] queries after QK-norm + RoPE
+  float* mo = reinterpret_cast<float*>(smem); // merge area [NW][16][DH], reuses the K/V tiles after use
+  float* s_ml = reinterpret_cast<float*>(lq); // merge (m, l) [NW][16][2], reuses the query tile after use
   __shared__ int s_page[NPG];
 
   const int lane = threadIdx.x & 63;
@@ -63,157 +83,304 @@ __global__ void __launch_bounds__(256) attn_kernel(AttnParams p) {
   const int s = item / (p.nsplit * p.Hkv);
   const int G = p.Hq / p.Hkv;
   const int R = p.Bq * G;
+  const int nrg = (R + 15) / 16;
   const float scale = rsqrtf((float)DH);
-  const int key0 = split * SplitKeys<T>::value;
+  const int key0 = split * SK;
   const int t0 = p.start_pos[s];
   const int kv_len = t0 + p.Bq;
+  const int cap = p.max_pages * PAGE;
+  if (threadIdx.x == 0 && split == 0 && kv_len > cap) set_status(p.status, ST_CAPACITY);
   if (key0 >= kv_len) return;                 // uniform over the workgroup
 
-  // ---- pages stream through two LDS buffers: page i+1 is fetched into
-  // registers while page i is used, then stored into the other buffer.
   if (threadIdx.x < NPG) {
     const int pidx = min(key0 / PAGE + (int)threadIdx.x, p.max_pages - 1);
     const int pg = p.page_table[(size_t)s * p.max_pages + pidx];
     s_page[threadIdx.x] = (key0 + (int)threadIdx.x * PAGE < kv_len && pg >= 0 && pg < p.num_pages) ? pg : -1;
   }
   __syncthreads();
-  constexpr int V16 = PG * (int)sizeof(T) / 16;       // 16-byte vectors per page block
-  constexpr int PER = V16 / 256;                      // per thread, K and V each
-  static_assert(V16 % 256 == 0, "page staging assumes 256 threads");
+
+  // ---- 1. stage all pages (absent pages read page 0 of the pool; never used) ...
+  constexpr int V16 = PG * (int)sizeof(T) / 16;   // 16-byte vectors per page block
+  constexpr int PER = NPG * V16 / NT;             // per thread, K and V each
+  static_assert((NPG * V16) % NT == 0, "page staging assumes whole vectors per thread");
   u32x4_t kr[PER], vr[PER];
-  // absent pages read page 0 of the pool (always valid); their copy is never used
-  auto fetch = [&](int pi) {
-    const int pg = max(s_page[pi], 0);
-    const size_t off = ((size_t)pg * p.Hkv + kvh) * PG;
-    const gu4* gk = (const gu4*)(reinterpret_cast<const T*>(p.kpool) + off);
-    const gu4* gv = (const gu4*)(reinterpret_cast<const T*>(p.vpool) + off);
 #pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      kr[it] = gk[threadIdx.x + it * 256];
-      vr[it] = gv[threadIdx.x + it * 256];
+  for (int it = 0; it < PER; ++it) {
+    const int idx = threadIdx.x + it * NT;
+    const int pi = idx / V16, vi = idx - pi * V16;
+    const size_t off = ((size_t)max(s_page[pi], 0) * p.Hkv + kvh) * PG;
+    kr[it] = ((const gu4*)(reinterpret_cast<const T*>(p.kpool) + off))[vi];
+    vr[it] = ((const gu4*)(reinterpret_cast<const T*>(p.vpool) + off))[vi];
+  }
+  // ... while the query rows get QK-norm + RoPE (lane i < DH/2 owns channels i, i + DH/2)
+  const T* qkv = reinterpret_cast<const T*>(p.qkv);
+  if constexpr (FUSED) {
+    const T* gq = reinterpret_cast<const T*>(p.q_norm);
+    for (int rr = w; rr < R; rr += NW) {       // uniform per wave
+      const int j = rr / G, g = rr - j * G;
+      const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH;
+      float x1 = 0.f, x2 = 0.f;
+      if (lane < HALF) { x1 = TT<T>::ld(src, lane); x2 = TT<T>::ld(src, lane + HALF); }
+      const float r = rsqrtf(wave_sum(x1 * x1 + x2 * x2) / (float)DH + p.eps);
+      if (lane < HALF) {
+        const int pos = min(t0 + j, cap - 1);   // past capacity: status set above
+        const float2 c = p.rope[(size_t)pos * HALF + lane];
+        const float y1 = x1 * r * TT<T>::ld(gq, lane);
+        const float y2 = x2 * r * TT<T>::ld(gq, lane + HALF);
+        TT<T>::st(lq, (size_t)rr * QLD + lane, y1 * c.x - y2 * c.y);
+        TT<T>::st(lq, (size_t)rr * QLD + lane + HALF, y2 * c.x + y1 * c.y);
+      }
     }
-  };
-  auto store = [&](int buf) {
+  }
+  // ... and the block's own key rows in this split (wave w: rows jlo + w + NW * b)
+  const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SK - t0);
+  float nk1[MAXB], nk2[MAXB], nv1[MAXB], nv2[MAXB];
+  if constexpr (FUSED) {
+    const T* gk = reinterpret_cast<const T*>(p.k_norm);
 #pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      reinterpret_cast<u32x4_t*>(lk + (size_t)buf * PG)[threadIdx.x + it * 256] = kr[it];
-      reinterpret_cast<u32x4_t*>(lv + (size_t)buf * PG)[threadIdx.x + it * 256] = vr[it];
+    for (int b = 0; b < MAXB; ++b) {
+      const int j = jlo + w + NW * b;
+      if (j >= jhi) break;                     // uniform per wave
+      const int pos = min(t0 + j, cap - 1);
+      const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)p.Hq * DH + (size_t)kvh * DH;
+      const T* vsrc = src + (size_t)p.Hkv * DH;
+      float x1 = 0.f, x2 = 0.f;
+      if (lane < HALF) { x1 = TT<T>::ld(src, lane); x2 = TT<T>::ld(src, lane + HALF); }
+      const float r = rsqrtf(wave_sum(x1 * x1 + x2 * x2) / (float)DH + p.eps);
+      nk1[b] = nk2[b] = 0.f;
+      if (lane < HALF) {
+        const float2 c = p.rope[(size_t)pos * HALF + lane];
+        const float y1 = x1 * r * TT<T>::ld(gk, lane);
+        const float y2 = x2 * r * TT<T>::ld(gk, lane + HALF);
+        nk1[b] = y1 * c.x - y2 * c.y;
+        nk2[b] = y2 * c.x + y1 * c.y;
+      }
+      nv1[b] = TT<T>::ld(vsrc, lane);
+      nv2[b] = lane + 64 < DH ? TT<T>::ld(vsrc, lane + 64) : 0.f;
     }
-  };
-  // ---- each wave owns up to RGW whole 16-row groups per pass over the pages.
-  // The pass and page loops are uniform over the workgroup: every thread
-  // stages every page and reaches every barrier, with or without rows.
-  constexpr int RGW = 2;
-  const int nrg = (R + 15) / 16;
-  const int npass = (nrg + 4 * RGW - 1) / (4 * RGW);
-  for (int pass = 0; pass < npass; ++pass) {
-    int rgs[RGW];
-    bool rgv[RGW];
-    u32x4_t qf[RGW][KS];
-    float mrow[RGW], lrow[RGW];
-    f32x4_t o[RGW][DT];
+  }
 #pragma unroll
-    for (int g = 0; g < RGW; ++g) {
-      rgs[g] = pass * 4 * RGW + 4 * g + w;
-      rgv[g] = rgs[g] < nrg;
-      const int ar = min(rgs[g], nrg - 1) * 16 + (lane & 15);
-      const int jrow = ar < R ? ar / G : 0, grow = ar < R ? ar % G : 0;
-      const T* qrow = reinterpret_cast<const T*>(p.Q) + ((size_t)(s * p.Bq + jrow) * p.Hq + kvh * G + grow) * DH;
+  for (int it = 0; it < PER; ++it) {
+    const int idx = threadIdx.x + it * NT;
+    reinterpret_cast<u32x4_t*>(lk)[idx] = kr[it];
+    reinterpret_cast<u32x4_t*>(lv)[idx] = vr[it];
+  }
+  __syncthreads();
+
+  // ---- 2. the block rows' keys and values into the staged tiles and the cache
 #pragma unroll
-      for (int k = 0; k < KS; ++k) qf[g][k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
-      mrow[g] = -INFINITY;
-      lrow[g] = 0.f;
-#pragma unroll
-      for (int i = 0; i < DT; ++i) o[g][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < (FUSED ? MAXB : 0); ++b) {
+    const int j = jlo + w + NW * b;
+    if (j >= jhi) break;                       // uniform per wave
+    const int pos = t0 + j;
+    if (pos >= cap) continue;                  // status set above
+    const int pi = (pos - key0) / PAGE, slot = pos % PAGE;
+    const int gpage = s_page[pi];
+    if (lane == 0 && gpage < 0) set_status(p.status, ST_BAD_PAGE);
+    T* kt_l = lk + (size_t)pi * PG;
+    T* vt_l = lv + (size_t)pi * PG;
+    T* kt_g = gpage >= 0 ? reinterpret_cast<T*>(p.kpool) + ((size_t)gpage * p.Hkv + kvh) * PG : nullptr;
+    T* vt_g = gpage >= 0 ? reinterpret_cast<T*>(p.vpool) + ((size_t)gpage * p.Hkv + kvh) * PG : nullptr;
+    auto koff = [&](int d) -> int {
+      return (((slot / 16) * KS + d / KT) * 64 + ((d % KT) / KL) * 16 + slot % 16) * KL + d % KL;
+    };
+    auto voff = [&](int e) -> int {
+      return (((slot / 16) * DT + e / 16) * 64 + ((slot % 16) / 4) * 16 + e % 16) * 4 + slot % 4;
+    };
+    if (lane < HALF) {
+      TT<T>::st(kt_l, koff(lane), nk1[b]);
+      TT<T>::st(kt_l, koff(lane + HALF), nk2[b]);
+      if (kt_g) {
+        TT<T>::st(kt_g, koff(lane), nk1[b]);
+        TT<T>::st(kt_g, koff(lane + HALF), nk2[b]);
+      }
     }
-    fetch(0);
-    __syncthreads();                          // buffer 0 is free (previous pass finished with it)
-    store(0);
-    __syncthreads();
-    for (int pi = 0; pi < NPG; ++pi) {
-      const int buf = pi & 1;
-      if (pi + 1 < NPG) fetch(pi + 1);        // uniform; lands while this page is used
-      if (s_page[pi] >= 0) {                  // uniform
-        const int kp0 = key0 + pi * PAGE;
-        const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)buf * PG);
-        const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)buf * PG);
+    TT<T>::st(vt_l, voff(lane), nv1[b]);
+    if (vt_g) TT<T>::st(vt_g, voff(lane), nv1[b]);
+    if (lane + 64 < DH) {
+      TT<T>::st(vt_l, voff(lane + 64), nv2[b]);
+      if (vt_g) TT<T>::st(vt_g, voff(lane + 64), nv2[b]);
+    }
+  }
+  __syncthreads();
+
+  // ---- 3. row groups x page subsets
+  int wpr = 1;
+  while (wpr * 2 <= NPG && wpr * 2 * nrg <= NW) wpr *= 2;
+  const int units = nrg * wpr;                 // waves with work in a pass (merge) or row groups (wpr = 1)
+  auto run_unit = [&](int rg, int part, u32x4_t (&qf)[KS], float& mrow, float& lrow, f32x4_t (&o)[DT]) {
+    {
+      const int qr = min(rg * 16 + (lane & 15), R - 1);
+      if constexpr (FUSED) {
 #pragma unroll
-        for (int g = 0; g < RGW; ++g) {
-          if (!rgv[g]) continue;              // uniform per wave; no barrier inside
-          const int ar = rgs[g] * 16 + (lane & 15);
-          const bool row_ok = ar < R;
-          const int pos_row = t0 + (row_ok ? ar / G : 0);
-          float sc[4][4];
+        for (int k = 0; k < KS; ++k)
+          qf[k] = *reinterpret_cast<const u32x4_t*>(lq + (size_t)qr * QLD + k * KT + (lane >> 4) * KL);
+      } else {
+        const int j = qr / G, g = qr - j * G;
+        const T* qrow = reinterpret_cast<const T*>(p.q) + ((size_t)(s * p.Bq + j) * p.Hq + kvh * G + g) * DH;
 #pragma unroll
-          for (int kt = 0; kt < 4; ++kt) {
-            f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < KS; ++k) qf[k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
+      }
+    }
+    mrow = -INFINITY;
+    lrow = 0.f;
 #pragma unroll
-            for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[g][k], acc);
+    for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int ar = rg * 16 + (lane & 15);
+    const bool row_ok = ar < R;
+    const int pos_row = t0 + (row_ok ? ar / G : 0);
+    for (int pi = part; pi < NPG; pi += wpr) {
+      if (s_page[pi] < 0) continue;          // uniform
+      const int kp0 = key0 + pi * PAGE;
+      const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)pi * PG);
+      const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
+      // every key of the page precedes the block and every row is valid: no mask
+      const bool full = kp0 + PAGE <= t0 && rg * 16 + 16 <= R;   // uniform
+      float sc[4][4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
-              const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
-              sc[kt][r] = vis ? acc[r] * scale : -INFINITY;
-            }
+      for (int kt = 0; kt < 4; ++kt) {
+        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[k], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sc[kt][r] = acc[r] * scale;
+      }
+      if (!full) {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
+            const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
+            if (!vis) sc[kt][r] = -INFINITY;
           }
-          float mx = -INFINITY;
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
-          mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-          // rows with nothing visible so far keep m = -inf, l = 0 and a zero output;
-          // control flow stays uniform (the matrix-core ops and shuffles need all lanes)
-          const float mnew = fmaxf(mrow[g], mx);
-          const float alpha = (mrow[g] == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : __expf(mrow[g] - mnew);
-          float ls = 0.f;
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float e = (sc[kt][r] == -INFINITY) ? 0.f : __expf(sc[kt][r] - mnew);
-              sc[kt][r] = e;
-              ls += e;
-            }
-          ls += __shfl_xor(ls, 16, 64);
-          ls += __shfl_xor(ls, 32, 64);
-          lrow[g] = lrow[g] * alpha + ls;
-          mrow[g] = mnew;
-          float al[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) o[g][dt][r] *= al[r];
-#pragma unroll
-          for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) o[g][dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[g][dt]);
-        }
       }
-      if (pi + 1 < NPG) {
-        // the other buffer was last read in iteration pi-1, which every wave
-        // finished before the barrier that ended that iteration
-        store(buf ^ 1);
-        __syncthreads();
-      }
-    }
-    // ---- this split's partials of the wave's row groups
+      float mx = -INFINITY;
 #pragma unroll
-    for (int g = 0; g < RGW; ++g) {
-      if (!rgv[g]) continue;
-      const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + rgs[g]) * p.nsplit + split;
-      float* po = p.part_o + pidx * 16 * DH;
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      // rows with nothing visible so far keep m = -inf, l = 0 and a zero output;
+      // control flow stays uniform (the matrix-core ops and shuffles need all lanes)
+      const float mnew = fmaxf(mrow, mx);
+      const float alpha = (mrow == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : __expf(mrow - mnew);
+      float ls = 0.f;
+      if (full) {                              // mnew is finite and no score is masked
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            sc[kt][r] = __expf(sc[kt][r] - mnew);
+            ls += sc[kt][r];
+          }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = (sc[kt][r] == -INFINITY) ? 0.f : __expf(sc[kt][r] - mnew);
+            sc[kt][r] = e;
+            ls += e;
+          }
+      }
+      ls += __shfl_xor(ls, 16, 64);
+      ls += __shfl_xor(ls, 32, 64);
+      lrow = lrow * alpha + ls;
+      mrow = mnew;
+      float al[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) po[(4 * (lane >> 4) + r) * DH + dt * 16 + (lane & 15)] = o[g][dt][r];
-      if (lane < 16) {
-        p.part_ml[pidx * 32 + 2 * lane] = mrow[g];
-        p.part_ml[pidx * 32 + 2 * lane + 1] = lrow[g];
+        for (int r = 0; r < 4; ++r) o[dt][r] *= al[r];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
+    }
+  };
+  auto write_partial = [&](int rg, float mrow, float lrow, const f32x4_t (&o)[DT]) {
+    const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + rg) * p.nsplit + split;
+    float* po = p.part_o + pidx * 16 * DH;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) po[(4 * (lane >> 4) + r) * DH + dt * 16 + (lane & 15)] = o[dt][r];
+    if (lane < 16) {
+      p.part_ml[pidx * 32 + 2 * lane] = mrow;
+      p.part_ml[pidx * 32 + 2 * lane + 1] = lrow;
+    }
+  };
+
+  u32x4_t qf[KS];
+  float mrow, lrow;
+  f32x4_t o[DT];
+  if (wpr == 1) {
+    for (int rg = w; rg < nrg; rg += NW) {     // uniform per wave; no barrier inside
+      run_unit(rg, 0, qf, mrow, lrow, o);
+      write_partial(rg, mrow, lrow, o);
+    }
+    return;
+  }
+  const bool active = w < units;
+  const int rg = w % nrg, part = w / nrg;
+  if (active) run_unit(rg, part, qf, mrow, lrow, o);
+  __syncthreads();                             // every wave is done with the K/V tiles
+  if (active) {
+    float* mw = mo + (size_t)w * 16 * DH;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)   // 16-column blocks XOR-swizzled by row/4: conflict-free stores
+        mw[(4 * (lane >> 4) + r) * DH + ((dt * 16 + (lane & 15)) ^ ((lane >> 4) << 4))] = o[dt][r];
+    if (lane < 16) {
+      s_ml[(w * 16 + lane) * 2] = mrow;
+      s_ml[(w * 16 + lane) * 2 + 1] = lrow;
+    }
+  }
+  __syncthreads();
+  // merge the wpr partials of each row group in part order; lane handles 4
+  // consecutive channels, all partial loads in flight together
+  for (int e4 = threadIdx.x; e4 < nrg * 4 * DH; e4 += NT) {
+    const int e = e4 * 4;
+    const int g = e / (16 * DH), rem = e - g * 16 * DH, row = rem / DH, dd = rem - row * DH;
+    float mq[NPG], lq4[NPG];
+    float4 oq[NPG];
+#pragma unroll
+    for (int q = 0; q < NPG; ++q) {
+      if (q < wpr) {                               // uniform
+        const int u = q * nrg + g;
+        mq[q] = s_ml[(u * 16 + row) * 2];
+        lq4[q] = s_ml[(u * 16 + row) * 2 + 1];
+        oq[q] = *reinterpret_cast<const float4*>(mo + ((size_t)u * 16 + row) * DH + (dd ^ (((row >> 2) & 3) << 4)));
+      } else {
+        mq[q] = -INFINITY;
+        lq4[q] = 0.f;
+        oq[q] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < NPG; ++q) M = fmaxf(M, mq[q]);
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float l = 0.f;
+#pragma unroll
+    for (int q = 0; q < NPG; ++q) {
+      const float f = (mq[q] == -INFINITY) ? 0.f : __expf(mq[q] - M);
+      acc.x += f * oq[q].x;
+      acc.y += f * oq[q].y;
+      acc.z += f * oq[q].z;
+      acc.w += f * oq[q].w;
+      l += f * lq4[q];
+    }
+    const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + g) * p.nsplit + split;
+    *reinterpret_cast<float4*>(p.part_o + (pidx * 16 + row) * DH + dd) = acc;
+    if (dd == 0) {
+      p.part_ml[pidx * 32 + 2 * row] = M;
+      p.part_ml[pidx * 32 + 2 * row + 1] = l;
     }
   }
 }
@@ -251,23 +418,55 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
   TT<T>::st(reinterpret_cast<T*>(p.out), (size_t)row * p.Hq * DH + hq * DH + d, v);
 }
 
+constexpr int ATTN_WAVES = 16;
+
+// Dynamic LDS of the attention kernel: the split's K and V pages plus the
+// query tile (fused variant) or the merge statistics.
 template <typename T, int DH>
-static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
-  const int blocks = p.nseq * p.Hkv * p.nsplit;
-  const size_t lds = 2 * 2 * (size_t)PAGE * DH * sizeof(T);   // two page buffers, K and V
-  if (lds > 160 * 1024) return hipErrorInvalidConfiguration;
-  static bool lds_set = false;   // allow more than the default dynamic LDS once per instantiation
+static size_t attn_lds(bool fused, int R) {
+  const size_t tile = fused ? (size_t)R * (DH + TT<T>::KL) * sizeof(T) : 0;
+  const size_t ml = (size_t)ATTN_WAVES * 16 * 2 * sizeof(float);
+  return 2 * (size_t)SplitKeys<T>::value * DH * sizeof(T) + (tile > ml ? tile : ml);
+}
+static constexpr size_t ATTN_LDS_MAX = 159 * 1024;
+
+template <typename T, int DH>
+static bool fuses_dh(int Bq, int G) {
+  return Bq <= 4 * ATTN_WAVES && attn_lds<T, DH>(true, Bq * G) <= ATTN_LDS_MAX;
+}
+
+template <typename T, int DH, bool FUSED>
+static hipError_t launch_k(const AttnParams& p, hipStream_t st) {
+  constexpr int NW = ATTN_WAVES;
+  const size_t lds = attn_lds<T, DH>(FUSED, p.Bq * (p.Hq / p.Hkv));
+  if (lds > ATTN_LDS_MAX) return hipErrorInvalidConfiguration;
+  static bool lds_set = false;   // allow the largest dynamic LDS once per instantiation
   if (!lds_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATTN_LDS_MAX);
     if (e != hipSuccess) return e;
     lds_set = true;
   }
-  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(blocks), dim3(256), lds, st, p);
+  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(p.nseq * p.Bq, p.Hq), dim3(DH), 0, st, p);
   return hipGetLastError();
+}
+
+template <typename T, int DH>
+static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
+  if (p.fused) {
+    if (!fuses_dh<T, DH>(p.Bq, p.Hq / p.Hkv)) return hipErrorInvalidConfiguration;
+    return launch_k<T, DH, true>(p, st);
+  }
+  return launch_k<T, DH, false>(p, st);
+}
+
+bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh) {
+  if (Dh == 128) return bf16 ? fuses_dh<dflow::bf16, 128>(Bq, G) : fuses_dh<float, 128>(Bq, G);
+  if (Dh == 64) return bf16 ? fuses_dh<dflow::bf16, 64>(Bq, G) : fuses_dh<float, 64>(Bq, G);
+  return false;
 }
 
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t st) {

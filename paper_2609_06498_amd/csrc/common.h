@@ -29,14 +29,15 @@ __device__ __host__ inline float bf2f(uint16_t u) {
   c.i = (uint32_t)u << 16;
   return c.f;
 }
-// round-to-nearest-even; values here are finite
-__device__ __host__ inline uint16_t f2bf(float f) {
-  union { uint32_t i; float f; } c;
-  c.f = f;
-  uint32_t u = c.i;
-  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// fp32 -> bf16 round-to-nearest-even with the gfx950 conversion instruction
+// (v_cvt_pk_bf16_f32; bit-identical to the integer RNE formula on every
+// finite input, and NaN stays NaN)
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_hw_t __attribute__((ext_vector_type(2)));
+__device__ inline uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// two values packed low | high << 16 in one instruction
+__device__ inline uint32_t f2bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_hw_t));
 }
 
 template <> struct SplitKeys<bf16> { static constexpr int value = 256; };
@@ -78,7 +79,7 @@ template <> struct Row16<bf16> {
     for (int h = 0; h < 2; ++h) {
       uint32_t w[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[8 * h + 2 * i]) | ((uint32_t)f2bf(v[8 * h + 2 * i + 1]) << 16);
+      for (int i = 0; i < 4; ++i) w[i] = f2bf2(v[8 * h + 2 * i], v[8 * h + 2 * i + 1]);
       q[h] = make_uint4(w[0], w[1], w[2], w[3]);
     }
   }

@@ -56,9 +56,16 @@ namespace dflow {
 //       with kt = key/16, q = (key%16)/4, dt = d/16, DT = Dh/16
 // (KL, KT: 8, 32 for bf16 and 4, 16 for fp32.)
 struct AttnParams {
-  const void* Q;             // [nseq*Bq, Hq*Dh] storage type, after QK-norm + RoPE
-  const void* kpool;
-  const void* vpool;
+  int fused;                 // 1: QK-norm + RoPE + the block's KV write done here from qkv
+  const void* q;             // fused = 0: [nseq*Bq, Hq*Dh] queries after QK-norm + RoPE
+  const void* qkv; int ld_qkv;   // fused = 1: raw projection rows [q heads | k heads | v heads] x Dh
+  const void* q_norm;        // [Dh] QK-norm gains
+  const void* k_norm;        // [Dh]
+  const float2* rope;        // [max_pages*64][Dh/2] (cos, sin)
+  float eps;
+  int* status;
+  void* kpool;               // this layer's pools (the block's own rows are written)
+  void* vpool;
   const int* page_table;     // [nseq][max_pages]
   int max_pages;
   const int* start_pos;      // [nseq] absolute position of block row 0
@@ -72,6 +79,8 @@ struct AttnParams {
   void* out;                 // [nseq*Bq, Hq*Dh] storage type
 };
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
+// Whether the fused variant fits (block rows per wave, LDS) for this shape.
+bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh);
 
 }  // namespace dflow
 
