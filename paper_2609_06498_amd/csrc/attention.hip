@@ -116,19 +116,34 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   const T* qkv = reinterpret_cast<const T*>(p.qkv);
   if constexpr (FUSED) {
     const T* gq = reinterpret_cast<const T*>(p.q_norm);
-    for (int rr = w; rr < R; rr += NW) {       // uniform per wave
-      const int j = rr / G, g = rr - j * G;
-      const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH;
-      float x1 = 0.f, x2 = 0.f;
-      if (lane < HALF) { x1 = TT<T>::ld(src, lane); x2 = TT<T>::ld(src, lane + HALF); }
-      const float r = rsqrtf(wave_sum(x1 * x1 + x2 * x2) / (float)DH + p.eps);
-      if (lane < HALF) {
-        const int pos = min(t0 + j, cap - 1);   // past capacity: status set above
-        const float2 c = p.rope[(size_t)pos * HALF + lane];
-        const float y1 = x1 * r * TT<T>::ld(gq, lane);
-        const float y2 = x2 * r * TT<T>::ld(gq, lane + HALF);
-        TT<T>::st(lq, (size_t)rr * QLD + lane, y1 * c.x - y2 * c.y);
-        TT<T>::st(lq, (size_t)rr * QLD + lane + HALF, y2 * c.x + y1 * c.y);
+    const float g1 = lane < HALF ? TT<T>::ld(gq, lane) : 0.f;
+    const float g2 = lane < HALF ? TT<T>::ld(gq, lane + HALF) : 0.f;
+    constexpr int QB = 4;                      // rows per wave per batch: all their loads in flight together
+    for (int rr0 = w; rr0 < R; rr0 += QB * NW) {   // uniform per wave
+      float x1[QB], x2[QB];
+      float2 c[QB];
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+        const int rr = min(rr0 + b * NW, R - 1);   // clamped rows are computed and not stored
+        const int j = rr / G, g = rr - j * G;
+        const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH;
+        const int pos = min(t0 + j, cap - 1);     // past capacity: status set above
+        const int l = lane < HALF ? lane : 0;
+        x1[b] = TT<T>::ld(src, l);
+        x2[b] = TT<T>::ld(src, l + HALF);
+        c[b] = p.rope[(size_t)pos * HALF + l];
+      }
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+        const int rr = rr0 + b * NW;
+        const float v1 = lane < HALF ? x1[b] : 0.f, v2 = lane < HALF ? x2[b] : 0.f;
+        const float r = rsqrtf(wave_sum(v1 * v1 + v2 * v2) / (float)DH + p.eps);
+        if (rr < R && lane < HALF) {
+          const float y1 = v1 * r * g1;
+          const float y2 = v2 * r * g2;
+          TT<T>::st(lq, (size_t)rr * QLD + lane, y1 * c[b].x - y2 * c[b].y);
+          TT<T>::st(lq, (size_t)rr * QLD + lane + HALF, y2 * c[b].x + y1 * c[b].y);
+        }
       }
     }
   }
