@@ -101,12 +101,11 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 
   // ---- 1. stage all pages (absent pages read page 0 of the pool; never used) ...
   constexpr int V16 = PG * (int)sizeof(T) / 16;   // 16-byte vectors per page block
-  constexpr int PER = NPG * V16 / NT;             // per thread, K and V each
-  static_assert((NPG * V16) % NT == 0, "page staging assumes whole vectors per thread");
+  constexpr int PER = (NPG * V16 + NT - 1) / NT;  // per thread, K and V each (the last one partial)
   u32x4_t kr[PER], vr[PER];
 #pragma unroll
   for (int it = 0; it < PER; ++it) {
-    const int idx = threadIdx.x + it * NT;
+    const int idx = min(threadIdx.x + it * NT, NPG * V16 - 1);   // a clamped duplicate is never stored
     const int pi = idx / V16, vi = idx - pi * V16;
     const size_t off = ((size_t)max(s_page[pi], 0) * p.Hkv + kvh) * PG;
     kr[it] = ((const gu4*)(reinterpret_cast<const T*>(p.kpool) + off))[vi];
@@ -177,8 +176,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 #pragma unroll
   for (int it = 0; it < PER; ++it) {
     const int idx = threadIdx.x + it * NT;
-    reinterpret_cast<u32x4_t*>(lk)[idx] = kr[it];
-    reinterpret_cast<u32x4_t*>(lv)[idx] = vr[it];
+    if ((NPG * V16) % NT == 0 || idx < NPG * V16) {
+      reinterpret_cast<u32x4_t*>(lk)[idx] = kr[it];
+      reinterpret_cast<u32x4_t*>(lv)[idx] = vr[it];
+    }
   }
   __syncthreads();
 
@@ -220,8 +221,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   __syncthreads();
 
   // ---- 3. row groups x page subsets
-  int wpr = 1;
-  while (wpr * 2 <= NPG && wpr * 2 * nrg <= NW) wpr *= 2;
+  // merge area (units x 16 x DH fp32) must fit in the K/V tiles it reuses
+  constexpr int MAXU = (2 * NPG * PG * (int)sizeof(T)) / (16 * DH * 4) < NW ? (2 * NPG * PG * (int)sizeof(T)) / (16 * DH * 4) : NW;
+  int wpr = MAXU / nrg < NPG ? MAXU / nrg : NPG;
+  if (wpr < 1) wpr = 1;
   const int units = nrg * wpr;                 // waves with work in a pass (merge) or row groups (wpr = 1)
   auto run_unit = [&](int rg, int part, u32x4_t (&qf)[KS], float& mrow, float& lrow, f32x4_t (&o)[DT]) {
     {
