@@ -130,8 +130,6 @@ typedef struct dflow_layer {
   const void* wo;         /* packed [d, n_heads*head_dim] */
   const void* wgu;        /* packed (gate_up=1) [2*ffn, d], col_gain = FFN-norm gain */
   const void* wdown;      /* packed [d, ffn] */
-  const void* wkv_ctx;    /* drafter layers only: packed [Wk; Wv] [2*n_kv_heads*head_dim, d]
-                             without gain, projecting the context features F (Sec. 4.1) */
 } dflow_layer;
 
 typedef struct dflow_weights {
@@ -140,6 +138,9 @@ typedef struct dflow_weights {
   const dflow_layer* layers;    /* HOST array [n_layers] */
   const dflow_layer* draft_layers; /* HOST array [n_draft_layers] */
   const void* draft_lm_head;    /* the shared LM head packed with col_gain = drafter final-norm gain */
+  const void* draft_wkv_ctx;    /* packed [n_draft_layers*2*n_kv_heads*head_dim, d], no gain: for each drafter
+                                   layer l its [Wk; Wv] (rows from l*2*n_kv_heads*head_dim), projecting the
+                                   context features F into that layer's K/V (Sec. 3, eq. dflash_context) */
   const void* e_mask;           /* [d] mask embedding E_mask */
   const void* w_c;              /* packed [d, n_capture*d] feature projection W_c */
   const void* g_c;              /* [d] RMSNorm gain after W_c */

@@ -64,6 +64,8 @@ struct dflow_ctx {
   float* ssq;   // [mmax][SSQ_LD] sums of squares of x per 16-column strip (RMSNorm row scales)
   uint64_t* amax_part;   // [ARGMAX_SPLITS][mmax]
   unsigned* counters;    // arrival counters of last-workgroup reductions; every launch leaves them at 0
+  void* ctxkv;           // [mmax][n_draft_layers * 2 * kv_dim] drafter-context K/V projections
+  const void** dknorm;   // device [n_draft_layers] K-norm gain pointers of the drafter layers
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -175,6 +177,8 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)mmax * SSQ_LD * 4);                      // 20 ssq: per-strip sums of squares of the residual rows
   add((size_t)ARGMAX_SPLITS * mmax * 8);               // 21 amax_part: [split][row] partial argmax keys
   add(256);                                            // 22 counters (zero between launches)
+  add((size_t)mmax * d->n_draft_layers * 2 * kvd * elt);   // 23 ctxkv: drafter-context K/V rows of all drafter layers
+  add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 24 drafter K-norm gain pointers
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -194,20 +198,19 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   int rc = validate(dims);
   if (rc) return rc;
   if (!w || !cache || !out) return fail(DFLOW_EINVAL, "create: null argument");
-  const void* req[] = {w->embed, w->lm_head, w->layers, w->draft_layers, w->draft_lm_head,
+  const void* req[] = {w->embed, w->lm_head, w->layers, w->draft_layers, w->draft_lm_head, w->draft_wkv_ctx,
                        w->e_mask, w->w_c, w->g_c, w->relay_w1, w->relay_c1, w->relay_w2, w->relay_c2,
                        w->relay_ln_g, w->relay_ln_b, cache->k_pool, cache->v_pool, cache->ck_pool, cache->cv_pool,
                        cache->page_table};
   for (size_t i = 0; i < sizeof(req) / sizeof(req[0]); ++i)
     if (!req[i]) return fail(DFLOW_EINVAL, "create: required pointer #%zu is null", i);
-  auto chk_layer = [](const dflow_layer& L, bool draft) {
-    return L.wqkv && L.q_norm && L.k_norm && L.wo && L.wgu && L.wdown && (!draft || L.wkv_ctx);
+  auto chk_layer = [](const dflow_layer& L) {
+    return L.wqkv && L.q_norm && L.k_norm && L.wo && L.wgu && L.wdown;
   };
   for (int l = 0; l < dims->n_layers; ++l)
-    if (!chk_layer(w->layers[l], false)) return fail(DFLOW_EINVAL, "create: null pointer in target layer %d", l);
+    if (!chk_layer(w->layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in target layer %d", l);
   for (int l = 0; l < dims->n_draft_layers; ++l)
-    if (!chk_layer(w->draft_layers[l], true))
-      return fail(DFLOW_EINVAL, "create: null pointer in drafter layer %d", l);
+    if (!chk_layer(w->draft_layers[l])) return fail(DFLOW_EINVAL, "create: null pointer in drafter layer %d", l);
 
   dflow_ctx* c = new dflow_ctx();
   c->dm = *dims;
@@ -259,6 +262,8 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->ssq = (float*)(b + L.off[20]);
   c->amax_part = (uint64_t*)(b + L.off[21]);
   c->counters = (unsigned*)(b + L.off[22]);
+  c->ctxkv = b + L.off[23];
+  c->dknorm = (const void**)(b + L.off[24]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -275,6 +280,11 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   }
   e = hipMemset(c->ws, 0, c->ws_bytes);
   if (e == hipSuccess) e = hipMemcpy(c->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+  if (e == hipSuccess && dims->n_draft_layers > 0) {
+    std::vector<const void*> kn(dims->n_draft_layers);
+    for (int l = 0; l < dims->n_draft_layers; ++l) kn[l] = c->dlayers[l].k_norm;
+    e = hipMemcpy(c->dknorm, kn.data(), kn.size() * sizeof(void*), hipMemcpyHostToDevice);
+  }
   if (e != hipSuccess) {
     (void)hipFree(c->ws);
     delete c;
@@ -420,6 +430,7 @@ hipError_t qk_rope(dflow_ctx* c, hipStream_t st, const dflow_layer& L, const voi
   r.num_pages = c->dm.num_pages;
   r.status = c->status;
   r.eps = c->dm.rms_eps;
+  r.nlayers = 1;
   return launch_qk_rope_write(c->bf, r, st);
 }
 
@@ -493,19 +504,39 @@ hipError_t project(dflow_ctx* c, hipStream_t st, int M, void* fout) {
 }
 
 // Drafter context K/V of feature rows (nseq x Bq) at start_pos + j for rows j <= row_limit[s].
+// All drafter layers at once: one GEMM over the stacked [Wk; Wv] of every
+// layer, then K-norm + RoPE + paged write for every layer in one launch.
 hipError_t ctx_append(dflow_ctx* c, hipStream_t st, const void* feat, int nseq, int Bq, const int* start_pos,
                       const int* row_limit, const int* page_table) {
   const dflow_dims& d = c->dm;
+  if (d.n_draft_layers < 1) return hipSuccess;
   const int M = nseq * Bq;
+  const int ncols = d.n_draft_layers * 2 * c->kv_dim;
   hipError_t e;
-  for (int l = 0; l < d.n_draft_layers; ++l) {
-    const dflow_layer& L = c->dlayers[l];
-    if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, L.wkv_ctx, M, 2 * c->kv_dim, d.d, c->qkv, 2 * c->kv_dim))) return e;
-    if ((e = qk_rope(c, st, L, c->qkv, 2 * c->kv_dim, nseq, Bq, 0, start_pos, row_limit, page_table,
-                     pool_layer(c, c->c.ck_pool, l), pool_layer(c, c->c.cv_pool, l))))
-      return e;
-  }
-  return hipSuccess;
+  if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, c->w.draft_wkv_ctx, M, ncols, d.d, c->ctxkv, ncols))) return e;
+  RopeParams r{};
+  r.qkv = c->ctxkv;
+  r.ld = ncols;
+  r.M = M;
+  r.Bq = Bq;
+  r.nq = 0;
+  r.Hkv = d.n_kv_heads;
+  r.Dh = d.head_dim;
+  r.rope = c->rope;
+  r.start_pos = start_pos;
+  r.row_limit = row_limit;
+  r.kpool = c->c.ck_pool;
+  r.vpool = c->c.cv_pool;
+  r.page_table = page_table;
+  r.max_pages = d.max_pages;
+  r.num_pages = d.num_pages;
+  r.status = c->status;
+  r.eps = d.rms_eps;
+  r.nlayers = d.n_draft_layers;
+  r.layer_cols = 2 * c->kv_dim;
+  r.pool_stride = c->pool_layer_elems;
+  r.k_norms = c->dknorm;
+  return launch_qk_rope_write(c->bf, r, st);
 }
 
 int check_nseq(dflow_ctx* c, int nseq) {

@@ -133,7 +133,8 @@ __global__ void qk_rope_kernel(RopeParams p) {
   if (p.row_limit && j > p.row_limit[s]) return;
   const int Dh = p.Dh, half = Dh / 2;
   const int pos = p.start_pos[s] + j;
-  const T* src = reinterpret_cast<const T*>(p.qkv) + (size_t)row * p.ld + (size_t)h * Dh;
+  const int layer = blockIdx.z;
+  const T* src = reinterpret_cast<const T*>(p.qkv) + (size_t)row * p.ld + (size_t)layer * p.layer_cols + (size_t)h * Dh;
   const bool is_q = h < p.nq;
   const bool is_k = !is_q && h < p.nq + p.Hkv;
   const int kvh = is_q ? 0 : (is_k ? h - p.nq : h - p.nq - p.Hkv);
@@ -157,7 +158,7 @@ __global__ void qk_rope_kernel(RopeParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
   const int KS = Dh / KT, DT = Dh / 16;
   if (!is_q && !is_k) {        // value head, fragment order (see kernels.h)
-    T* vp = reinterpret_cast<T*>(p.vpool) + page_base;
+    T* vp = reinterpret_cast<T*>(p.vpool) + (size_t)layer * p.pool_stride + page_base;
     const int kt = slot / 16, q = (slot % 16) / 4, r = slot % 4;
     for (int e = i; e < Dh; e += blockDim.x)
       vp[((size_t)(kt * DT + e / 16) * 64 + q * 16 + e % 16) * 4 + r] = src[e];
@@ -167,7 +168,7 @@ __global__ void qk_rope_kernel(RopeParams p) {
   auto koff = [&](int d) -> size_t {
     return ((size_t)((slot / 16) * KS + d / KT) * 64 + ((d % KT) / KL) * 16 + slot % 16) * KL + d % KL;
   };
-  const T* gain = reinterpret_cast<const T*>(is_q ? p.q_norm : p.k_norm);
+  const T* gain = reinterpret_cast<const T*>(is_q ? p.q_norm : (p.k_norms ? p.k_norms[layer] : p.k_norm));
   float x1 = 0.f, x2 = 0.f;
   if (i < half) { x1 = TT<T>::ld(src, i); x2 = TT<T>::ld(src, i + half); }
   const float ss = wave_sum(x1 * x1 + x2 * x2);
@@ -183,7 +184,7 @@ __global__ void qk_rope_kernel(RopeParams p) {
       TT<T>::st(q, i, o1);
       TT<T>::st(q, i + half, o2);
     } else {
-      T* kp = reinterpret_cast<T*>(p.kpool) + page_base;
+      T* kp = reinterpret_cast<T*>(p.kpool) + (size_t)layer * p.pool_stride + page_base;
       TT<T>::st(kp, koff(i), o1);
       TT<T>::st(kp, koff(i + half), o2);
     }
@@ -193,7 +194,8 @@ __global__ void qk_rope_kernel(RopeParams p) {
 hipError_t launch_qk_rope_write(bool isbf, const RopeParams& p, hipStream_t s) {
   if (p.M <= 0) return hipSuccess;
   if (p.Dh > 128 || (p.Dh & 1)) return hipErrorInvalidValue;
-  dim3 grid(p.M, p.nq + 2 * p.Hkv);
+  if (p.nlayers < 1 || (p.nlayers > 1 && p.nq != 0)) return hipErrorInvalidValue;
+  dim3 grid(p.M, p.nq + 2 * p.Hkv, p.nlayers);
   if (isbf) hipLaunchKernelGGL(qk_rope_kernel<bf16>, grid, dim3(64), 0, s, p);
   else hipLaunchKernelGGL(qk_rope_kernel<float>, grid, dim3(64), 0, s, p);
   return hipGetLastError();

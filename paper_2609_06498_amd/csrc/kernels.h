@@ -100,6 +100,9 @@ struct RopeParams {
   const int* page_table; int max_pages; int num_pages;
   int* status;
   float eps;
+  // several layers in one launch (grid z): layer l reads columns from l * layer_cols,
+  // writes the pools at l * pool_stride elements and takes its K-norm gain from k_norms[l]
+  int nlayers; int layer_cols; size_t pool_stride; const void* const* k_norms;
 };
 
 hipError_t launch_embed(bool bf16, const int* tok, int M, const void* E, int V, int d, void* out, int* status,

@@ -40,13 +40,14 @@ class Dims(ctypes.Structure):
 
 class Layer(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
-                ("wqkv", "q_norm", "k_norm", "wo", "wgu", "wdown", "wkv_ctx")]
+                ("wqkv", "q_norm", "k_norm", "wo", "wgu", "wdown")]
 
 
 class Weights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("lm_head", ctypes.c_void_p),
                 ("layers", ctypes.POINTER(Layer)), ("draft_layers", ctypes.POINTER(Layer)),
-                ("draft_lm_head", ctypes.c_void_p), ("e_mask", ctypes.c_void_p), ("w_c", ctypes.c_void_p),
+                ("draft_lm_head", ctypes.c_void_p), ("draft_wkv_ctx", ctypes.c_void_p),
+                ("e_mask", ctypes.c_void_p), ("w_c", ctypes.c_void_p),
                 ("g_c", ctypes.c_void_p), ("relay_w1", ctypes.c_void_p), ("relay_c1", ctypes.c_void_p),
                 ("relay_w2", ctypes.c_void_p), ("relay_c2", ctypes.c_void_p), ("relay_ln_g", ctypes.c_void_p),
                 ("relay_ln_b", ctypes.c_void_p)]
@@ -161,10 +162,14 @@ class Runtime:
         W.lm_head = self._packed(weights["lm_head"], gain=weights["final_norm"])
         self.layers = (Layer * dims.n_layers)(*[self._layer(weights, f"layers.{l}") for l in range(dims.n_layers)])
         self.dlayers = (Layer * dims.n_draft_layers)(
-            *[self._layer(weights, f"draft.layers.{l}", draft=True) for l in range(dims.n_draft_layers)])
+            *[self._layer(weights, f"draft.layers.{l}") for l in range(dims.n_draft_layers)])
         W.layers = self.layers
         W.draft_layers = self.dlayers
         W.draft_lm_head = self._packed(weights["lm_head"], gain=weights["draft.final_norm"])
+        # the context features enter each drafter layer's K/V without its attention norm
+        W.draft_wkv_ctx = self._packed(np.concatenate(
+            [np.concatenate([weights[f"draft.layers.{l}.wk"], weights[f"draft.layers.{l}.wv"]])
+             for l in range(dims.n_draft_layers)]))
         W.e_mask = up(weights["draft.e_mask"])
         W.w_c = self._packed(weights["draft.w_c"])
         W.g_c = up(weights["draft.g_c"])
@@ -218,7 +223,7 @@ class Runtime:
         self._keep.append(out)
         return out.data_ptr()
 
-    def _layer(self, w, p, draft: bool = False) -> Layer:
+    def _layer(self, w, p) -> Layer:
         L = Layer()
         L.wqkv = self._packed(np.concatenate([w[f"{p}.wq"], w[f"{p}.wk"], w[f"{p}.wv"]]),
                               gain=w[f"{p}.attn_norm"])
@@ -228,8 +233,6 @@ class Runtime:
         L.wgu = self._packed(np.concatenate([w[f"{p}.w_gate"], w[f"{p}.w_up"]]), gate_up=1,
                              gain=w[f"{p}.ffn_norm"])
         L.wdown = self._packed(w[f"{p}.w_down"])
-        if draft:   # the context features F enter K/V without the layer's attention norm
-            L.wkv_ctx = self._packed(np.concatenate([w[f"{p}.wk"], w[f"{p}.wv"]]))
         return L
 
     # ------------------------------------------------------------ calls
