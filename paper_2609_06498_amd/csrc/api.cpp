@@ -60,7 +60,7 @@ struct dflow_ctx {
   float *fproj, *bg, *part_o, *part_ml;
   float2* rope;
   uint64_t* amax;
-  int *row_argmax, *carry_rec, *status, *tmp_pos, *tmp_argmax;
+  int *carry_rec, *status, *tmp_pos, *tmp_argmax;
   float* ssq;   // [mmax][SSQ_LD] sums of squares of x per 16-column strip (RMSNorm row scales)
   uint64_t* amax_part;   // [ARGMAX_SPLITS][mmax]
   unsigned* counters;    // arrival counters of last-workgroup reductions; every launch leaves them at 0
@@ -169,16 +169,15 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)items * d->n_kv_heads * nsplit * 32 * 4);               // 12 part_ml
   add((size_t)d->max_pages * PAGE * (d->head_dim / 2) * sizeof(float2));  // 13 rope
   add((size_t)lm_groups * mmax * 8);                   // 14 amax: [lm_groups][rows] argmax keys
-  add((size_t)mmax * 4);                               // 15 row_argmax
-  add((size_t)d->max_batch * CARRY_REC * 4);           // 16 carry_rec
-  add(4);                                              // 17 status
-  add((size_t)(d->max_batch + 1) * 4);                 // 18 tmp_pos
-  add((size_t)mmax * 4);                               // 19 tmp_argmax
-  add((size_t)mmax * SSQ_LD * 4);                      // 20 ssq: per-strip sums of squares of the residual rows
-  add((size_t)ARGMAX_SPLITS * mmax * 8);               // 21 amax_part: [split][row] partial argmax keys
-  add(256);                                            // 22 counters (zero between launches)
-  add((size_t)mmax * d->n_draft_layers * 2 * kvd * elt);   // 23 ctxkv: drafter-context K/V rows of all drafter layers
-  add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 24 drafter K-norm gain pointers
+  add((size_t)d->max_batch * CARRY_REC * 4);           // 15 carry_rec
+  add(4);                                              // 16 status
+  add((size_t)(d->max_batch + 1) * 4);                 // 17 tmp_pos
+  add((size_t)mmax * 4);                               // 18 tmp_argmax
+  add((size_t)mmax * SSQ_LD * 4);                      // 19 ssq: per-strip sums of squares of the residual rows
+  add((size_t)ARGMAX_SPLITS * mmax * 8);               // 20 amax_part: [split][row] partial argmax keys
+  add(256);                                            // 21 counters (zero between launches)
+  add((size_t)mmax * d->n_draft_layers * 2 * kvd * elt);   // 22 ctxkv: drafter-context K/V rows of all drafter layers
+  add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -254,16 +253,15 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->part_ml = (float*)(b + L.off[12]);
   c->rope = (float2*)(b + L.off[13]);
   c->amax = (uint64_t*)(b + L.off[14]);
-  c->row_argmax = (int*)(b + L.off[15]);
-  c->carry_rec = (int*)(b + L.off[16]);
-  c->status = (int*)(b + L.off[17]);
-  c->tmp_pos = (int*)(b + L.off[18]);
-  c->tmp_argmax = (int*)(b + L.off[19]);
-  c->ssq = (float*)(b + L.off[20]);
-  c->amax_part = (uint64_t*)(b + L.off[21]);
-  c->counters = (unsigned*)(b + L.off[22]);
-  c->ctxkv = b + L.off[23];
-  c->dknorm = (const void**)(b + L.off[24]);
+  c->carry_rec = (int*)(b + L.off[15]);
+  c->status = (int*)(b + L.off[16]);
+  c->tmp_pos = (int*)(b + L.off[17]);
+  c->tmp_argmax = (int*)(b + L.off[18]);
+  c->ssq = (float*)(b + L.off[19]);
+  c->amax_part = (uint64_t*)(b + L.off[20]);
+  c->counters = (unsigned*)(b + L.off[21]);
+  c->ctxkv = b + L.off[22];
+  c->dknorm = (const void**)(b + L.off[23]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -491,7 +489,7 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
   if ((e = gemm(c, st, EPI_ARGMAX, (char*)c->x + off, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr,
                 0, nullptr, 0, nullptr, logits, d.vocab, fin)))
     return e;
-  return launch_argmax_reduce(c->amax, c->lm_groups, lm_rows, c->amax_part, c->counters, argmax_out, st);
+  return launch_argmax_reduce(c->amax, c->lm_groups, lm_rows, c->amax_part, c->counters, argmax_out, nullptr, st);
 }
 
 // F = RMSNorm(W_c [captured states]) for M rows -> fout (storage type)
@@ -597,8 +595,8 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   fin.ssq = c->ssq;
   HIPCHK(gemm(c, st, EPI_ARGMAX, c->x, d.d, c->w.draft_lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
               nullptr, draft_logits, d.vocab, fin));
-  HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, M, c->amax_part, c->counters, c->row_argmax, st));
-  HIPCHK(launch_draft_assemble(c->row_argmax, anchor_tok, nseq, B, draft_tok, block_out, st));
+  const DraftOut dr{anchor_tok, B, draft_tok, block_out};
+  HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, M, c->amax_part, c->counters, nullptr, &dr, st));
   return DFLOW_OK;
 }
 

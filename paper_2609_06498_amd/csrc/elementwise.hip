@@ -210,7 +210,7 @@ hipError_t launch_qk_rope_write(bool isbf, const RopeParams& p, hipStream_t s) {
 // writes the indices.  Max is order-independent, so the result does not
 // depend on arrival order.
 __global__ void __launch_bounds__(256) argmax_reduce_kernel(const uint64_t* amax, int groups, int M, uint64_t* part,
-                                                            unsigned* counter, int* out) {
+                                                            unsigned* counter, int* out, DraftOut dr) {
   __shared__ uint64_t sh[16][17];
   __shared__ bool s_last;
   const int r16 = threadIdx.x & 15, slice = threadIdx.x >> 4;
@@ -256,7 +256,13 @@ __global__ void __launch_bounds__(256) argmax_reduce_kernel(const uint64_t* amax
     if (threadIdx.x < 16 && m < M) {
       uint64_t b = sh[0][r16];
       for (int i = 1; i < 16; ++i) b = sh[i][r16] > b ? sh[i][r16] : b;
-      out[m] = argmax_key_index(b);
+      const int v = argmax_key_index(b);
+      if (out) out[m] = v;
+      if (dr.B > 0) {
+        const int sq = m / dr.B, j = m - sq * dr.B;
+        if (dr.block_out) dr.block_out[m] = j == 0 ? dr.anchor[sq] : v;
+        if (dr.draft_tok && j > 0) dr.draft_tok[(size_t)sq * (dr.B - 1) + j - 1] = v;
+      }
     }
     __syncthreads();
   }
@@ -264,32 +270,15 @@ __global__ void __launch_bounds__(256) argmax_reduce_kernel(const uint64_t* amax
 }
 
 hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_t* part, unsigned* counter, int* out,
-                                hipStream_t s) {
+                                const DraftOut* draft, hipStream_t s) {
   if (M <= 0 || groups <= 0) return hipSuccess;
-  const int nb = groups < ARGMAX_SPLITS ? groups : ARGMAX_SPLITS;
-  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(nb), dim3(256), 0, s, amax, groups, M, part, counter, out);
-  return hipGetLastError();
-}
-
-// draft_tok[s][j-1] = argmax of block row j (j = 1..B-1); block_out = [anchor, drafts]
-__global__ void draft_assemble_kernel(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
-                                      int* block_out) {
-  const int s = blockIdx.x;
-  for (int j = threadIdx.x; j < B; j += blockDim.x) {
-    if (j == 0) {
-      if (block_out) block_out[(size_t)s * B] = anchor[s];
-    } else {
-      const int t = row_argmax[(size_t)s * B + j];
-      if (draft_tok) draft_tok[(size_t)s * (B - 1) + j - 1] = t;
-      if (block_out) block_out[(size_t)s * B + j] = t;
-    }
+  DraftOut dr{nullptr, 0, nullptr, nullptr};
+  if (draft) {
+    if (draft->B < 1 || M % draft->B || !draft->anchor) return hipErrorInvalidValue;
+    dr = *draft;
   }
-}
-
-hipError_t launch_draft_assemble(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
-                                 int* block_out, hipStream_t s) {
-  hipLaunchKernelGGL(draft_assemble_kernel, dim3(nseq), dim3(64), 0, s, row_argmax, anchor, nseq, B, draft_tok,
-                     block_out);
+  const int nb = groups < ARGMAX_SPLITS ? groups : ARGMAX_SPLITS;
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(nb), dim3(256), 0, s, amax, groups, M, part, counter, out, dr);
   return hipGetLastError();
 }
 

@@ -111,10 +111,11 @@ hipError_t launch_rmsnorm(bool bf16, bool in_f32, const void* x, int ldx, int M,
                           void* out, int ldo, hipStream_t s);
 hipError_t launch_qk_rope_write(bool bf16, const RopeParams& p, hipStream_t s);
 constexpr int ARGMAX_SPLITS = 32;   // workgroups of the argmax reduction
+// Optional drafter layout of the row argmaxes (rows s*B + j): block_out[s][j] =
+// anchor[s] for j = 0 else the argmax; draft_tok[s][j-1] = the argmax of rows j >= 1.
+struct DraftOut { const int* anchor; int B; int* draft_tok; int* block_out; };
 hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_t* part, unsigned* counter, int* out,
-                                hipStream_t s);
-hipError_t launch_draft_assemble(const int* row_argmax, const int* anchor, int nseq, int B, int* draft_tok,
-                                 int* block_out, hipStream_t s);
+                                const DraftOut* draft, hipStream_t s);
 hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
                          int* bonus, int* committed, int* n_carry, int* carry_rec, hipStream_t s);
 hipError_t launch_relay_gather(bool bf16, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
