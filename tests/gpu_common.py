@@ -29,3 +29,19 @@ def bf16_bits(t):
 
 def dev_values(t, dtype):
     return bf16_bits(t) if dtype == "bf16" else t.cpu().numpy()
+
+
+def check_argmax(gpu_idx, ref_logits, tol, err_abs=None):
+    """Rows whose argmax must agree: margin above tol (and above 4x observed error)."""
+    mr = margin_rel(ref_logits)
+    ok = gpu_idx == np.argmax(ref_logits, axis=-1)
+    need = mr > tol
+    bad = need & ~ok
+    assert not bad.any(), f"argmax mismatch at rows {np.where(bad)[0]} margins {mr[bad]}"
+    if err_abs is not None:
+        l = np.asarray(ref_logits, np.float64)
+        part = np.partition(l, -2, axis=-1)
+        gap = part[..., -1] - part[..., -2]
+        strong = gap > 4 * err_abs
+        assert not (strong & ~ok).any(), "argmax mismatch on a row with a clear margin"
+    return int((~need).sum())

@@ -12,7 +12,7 @@ exceeds four times the observed logit error of the row.
 import numpy as np
 import pytest
 
-from tests.gpu_common import TOL, dev_values, margin_rel, rel_rows
+from tests.gpu_common import TOL, check_argmax as _check_argmax, dev_values, margin_rel, rel_rows
 from workload import get_config
 from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
 
@@ -44,22 +44,6 @@ def _setup(name):
     max_ctx = max(need) + wl.block
     rt = Runtime(dm, wl.block, wl.batch, max_ctx, w, wl.carry_window)
     return wl, w, o, prompts, sched, need, rt
-
-
-def _check_argmax(gpu_idx, ref_logits, tol, err_abs=None):
-    """Rows whose argmax must agree: margin above tol (and above 4x observed error)."""
-    mr = margin_rel(ref_logits)
-    ok = gpu_idx == np.argmax(ref_logits, axis=-1)
-    need = mr > tol
-    bad = need & ~ok
-    assert not bad.any(), f"argmax mismatch at rows {np.where(bad)[0]} margins {mr[bad]}"
-    if err_abs is not None:
-        l = np.asarray(ref_logits, np.float64)
-        part = np.partition(l, -2, axis=-1)
-        gap = part[..., -1] - part[..., -2]
-        strong = gap > 4 * err_abs
-        assert not (strong & ~ok).any(), "argmax mismatch on a row with a clear margin"
-    return int((~need).sum())
 
 
 @pytest.mark.parametrize("carry_on", [True, False])
