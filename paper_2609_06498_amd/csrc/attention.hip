@@ -84,7 +84,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   const int G = p.Hq / p.Hkv;
   const int R = p.Bq * G;
   const int nrg = (R + 15) / 16;
-  const float scale = rsqrtf((float)DH);
+  const float sl2 = rsqrtf((float)DH) * 1.4426950408889634f;   // softmax scale x log2(e)
   const int key0 = split * SK;
   const int t0 = p.start_pos[s];
   const int kv_len = t0 + p.Bq;
@@ -247,6 +247,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     const int ar = rg * 16 + (lane & 15);
     const bool row_ok = ar < R;
     const int pos_row = t0 + (row_ok ? ar / G : 0);
+    bool first = true;                        // uniform: the unit's first present page
     for (int pi = part; pi < NPG; pi += wpr) {
       if (s_page[pi] < 0) continue;          // uniform
       const int kp0 = key0 + pi * PAGE;
@@ -254,6 +255,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
       // every key of the page precedes the block and every row is valid: no mask
       const bool full = kp0 + PAGE <= t0 && rg * 16 + 16 <= R;   // uniform
+      // scores in log2 units (scale folded with log2 e), so the softmax uses exp2
       float sc[4][4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
@@ -261,7 +263,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 #pragma unroll
         for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[k], acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sc[kt][r] = acc[r] * scale;
+        for (int r = 0; r < 4; ++r) sc[kt][r] = acc[r] * sl2;
       }
       if (!full) {
 #pragma unroll
@@ -282,15 +284,14 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       // rows with nothing visible so far keep m = -inf, l = 0 and a zero output;
       // control flow stays uniform (the matrix-core ops and shuffles need all lanes)
-      const float mnew = fmaxf(mrow, mx);
-      const float alpha = (mrow == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : __expf(mrow - mnew);
+      const float mnew = first ? mx : fmaxf(mrow, mx);
       float ls = 0.f;
       if (full) {                              // mnew is finite and no score is masked
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            sc[kt][r] = __expf(sc[kt][r] - mnew);
+            sc[kt][r] = exp2f(sc[kt][r] - mnew);
             ls += sc[kt][r];
           }
       } else {
@@ -298,26 +299,49 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float e = (sc[kt][r] == -INFINITY) ? 0.f : __expf(sc[kt][r] - mnew);
+            const float e = (sc[kt][r] == -INFINITY) ? 0.f : exp2f(sc[kt][r] - mnew);
             sc[kt][r] = e;
             ls += e;
           }
       }
       ls += __shfl_xor(ls, 16, 64);
       ls += __shfl_xor(ls, 32, 64);
-      lrow = lrow * alpha + ls;
+      if (first) {                             // the output is still zero: nothing to rescale
+        lrow = ls;
+      } else {
+        const float alpha = (mrow == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : exp2f(mrow - mnew);
+        lrow = lrow * alpha + ls;
+        float al[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o[dt][r] *= al[r];
+      }
       mrow = mnew;
-      float al[4];
+      first = false;
+      if constexpr (KL == 8) {
+        // P V with 32 keys per matrix-core op: lane group g supplies keys
+        // 4g..4g+3 of key tiles 2c and 2c+1, and the same keys of V
 #pragma unroll
-      for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
+        for (int c = 0; c < 2; ++c) {
+          const u32x4_t pa = {f2bf2(sc[2 * c][0], sc[2 * c][1]), f2bf2(sc[2 * c][2], sc[2 * c][3]),
+                              f2bf2(sc[2 * c + 1][0], sc[2 * c + 1][1]), f2bf2(sc[2 * c + 1][2], sc[2 * c + 1][3])};
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+          for (int dt = 0; dt < DT; ++dt) {
+            const uint2 v0 = reinterpret_cast<const uint2*>(vb)[((2 * c) * DT + dt) * 64 + lane];
+            const uint2 v1 = reinterpret_cast<const uint2*>(vb)[((2 * c + 1) * DT + dt) * 64 + lane];
+            const u32x4_t vv = {v0.x, v0.y, v1.x, v1.y};
+            o[dt] = mma_frag(T(), pa, vv, o[dt]);
+          }
+        }
+      } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) o[dt][r] *= al[r];
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
+          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
+      }
     }
   };
   auto write_partial = [&](int rg, float mrow, float lrow, const f32x4_t (&o)[DT]) {
@@ -387,7 +411,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     float l = 0.f;
 #pragma unroll
     for (int q = 0; q < NPG; ++q) {
-      const float f = (mq[q] == -INFINITY) ? 0.f : __expf(mq[q] - M);
+      const float f = (mq[q] == -INFINITY) ? 0.f : exp2f(mq[q] - M);
       acc.x += f * oq[q].x;
       acc.y += f * oq[q].y;
       acc.z += f * oq[q].z;
@@ -403,7 +427,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   }
 }
 
-// out[row, head, :] = sum_split e^(m_s - M) O_s / sum_split e^(m_s - M) l_s
+// out[row, head, :] = sum_split 2^(m_s - M) O_s / sum_split 2^(m_s - M) l_s (m in log2 units)
 // (split order fixed; the split loads are independent and unrolled)
 template <typename T, int DH>
 __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
@@ -428,7 +452,7 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
 #pragma unroll 8
   for (int sp = 0; sp < ns; ++sp) {
     const float m = ml[(size_t)sp * 32];
-    const float f = (m == -INFINITY) ? 0.f : __expf(m - M);
+    const float f = (m == -INFINITY) ? 0.f : exp2f(m - M);   // partial maxima are in log2 units
     acc += f * po[(size_t)sp * 16 * DH];
     lsum += f * ml[(size_t)sp * 32 + 1];
   }
