@@ -45,3 +45,36 @@ def check_argmax(gpu_idx, ref_logits, tol, err_abs=None):
         strong = gap > 4 * err_abs
         assert not (strong & ~ok).any(), "argmax mismatch on a row with a clear margin"
     return int((~need).sum())
+
+
+def gpu_trajectory(rt, sess, prompts, need):
+    """The target's greedy continuation of every prompt, produced on the GPU by
+    junk-draft rounds through the round kernels (each commits at least the
+    bonus token); returns int32 [b, max(need)] with the prompts in front."""
+    import torch
+    b, B = len(prompts), rt.block
+    sess.prefill(prompts)
+    P = [len(p) for p in prompts]
+    L = max(need)
+    traj = torch.zeros(b, L, dtype=torch.int32, device="cuda")
+    zmode = torch.zeros(b, B, dtype=torch.int8, device="cuda")
+    ztok = torch.zeros(b, B, dtype=torch.int32, device="cuda")
+    first = sess.anchor.cpu().numpy().copy()
+    hist = []
+    while int((sess.seq_len.cpu().numpy() - np.array(P)).min()) < max(n - p for n, p in zip(need, P)):
+        pos = sess.seq_len.cpu().numpy().copy()
+        rt.force_drafts(b, traj, 1, zmode, ztok, sess.anchor, sess.seq_len, sess.block)
+        rt.verify_block(b, sess.block, sess.seq_len, sess.tgt)
+        rt.accept_and_carry(b, sess.block, sess.tgt, sess.accept, sess.anchor, sess.committed, sess.n_carry)
+        rt.kv_commit(b, sess.accept, sess.seq_len)
+        hist.append((pos, sess.accept.cpu().numpy().copy(), sess.committed.cpu().numpy().copy()))
+    out = np.zeros((b, L), np.int32)
+    for s in range(b):
+        out[s, :P[s]] = prompts[s]
+        out[s, P[s]] = first[s]
+    for pos, acc, com in hist:
+        for s in range(b):
+            for j in range(acc[s] + 1):
+                if pos[s] + 1 + j < L:
+                    out[s, pos[s] + 1 + j] = com[s, j]
+    return out

@@ -1,21 +1,30 @@
-"""GPU parity at the Qwen3-8B shape (36 + 5 layers, d 4096, 32/8 heads,
-FFN 12288, vocab 151936, bf16) in the launch configuration bench.py times
-(b = 1, B = 16): the same GEMM, attention and reduction instantiations and
-launch shapes as the benchmark, on the benchmark's seeded weights.
+"""GPU parity at full model widths in the launch configuration bench.py
+times (b = 1, B = 16, bf16), on the benchmark's seeded weights:
 
-The oracle cannot prefill 4096 tokens in a test, so the context is the first
-48 prompt tokens (one attention split; the multi-split path and ragged
-batches are covered by the small workloads).  Drafts are seeded random
-tokens, so nearly every round rejects at the first draft and relays K - 1
-verifier states: round 0 has no carry yet, rounds 1 and 2 exercise the relay.
+* qwen3-8b  -- the benchmarked shape (36 + 5 layers, d 4096, 32/8 heads,
+  FFN 12288, vocab 151936);
+* qwen3-1.7b -- 28 + 5 layers, d 2048, 16/8 heads, FFN 6144;
+* qwen3-32b-d5 -- the Qwen3-32B widths (d 5120, 64/8 heads: GQA group 8,
+  which takes the attention path without the fused QK-norm/RoPE, FFN 25600)
+  at 5 target layers, since the oracle cannot hold the 64-layer model; the
+  full-depth 32B shape is covered by the batch-invariance test.
 
-Bar.  At this depth the bf16 storage noise of the random-init model is larger
-than 2e-2: the oracle's own bf16 mode differs from its fp32 mode by about 5 %
-in logits.  So the device is compared with the fp32 oracle, and each
-quantity must be within max(2e-2, 1.5 x the bf16 oracle's distance to the
-fp32 oracle) per row; decisions (acceptance, bonus, argmax) must match the
-fp32 oracle wherever its top-1 margin exceeds that bound (near ties follow
-the device's decision in both oracles, and are counted)."""
+The oracle cannot prefill thousands of tokens in a test, so the context is the
+first 48 prompt tokens (one attention split; the multi-split path and ragged
+batches are covered by the small workloads and the invariance tests).  Drafts
+are seeded random tokens, so nearly every round rejects at the first draft
+and relays K - 1 verifier states: round 0 has no carry yet, rounds 1 and 2
+exercise the relay.
+
+Bar.  At these depths the bf16 storage noise of the random-init models is
+larger than 2e-2 (the oracle's own bf16 mode differs from its fp32 mode by
+about 5 % in the 8B logits).  So the device is compared with the fp32 oracle,
+and each quantity must be within max(2e-2, 1.5 x the bf16 oracle's distance
+to the fp32 oracle, capped at 0.15) per row -- the cap matters for the 1.7B
+model, whose bf16 oracle drifts from its fp32 mode by more than 100 % while
+the device stays within 3 %; decisions (acceptance, bonus, argmax) must match
+the fp32 oracle wherever its top-1 margin exceeds that bound (near ties
+follow the device's decision in both oracles, and are counted)."""
 import numpy as np
 import pytest
 
@@ -29,15 +38,27 @@ pytestmark = pytest.mark.gpu
 CTX = 48
 ROUNDS = 3
 NOISE_FACTOR = 1.5
+NOISE_CAP = 0.15     # a chaotic bf16 oracle (1.7B: >100 %) must not make the bound vacuous
 
 
-def test_round_parity_qwen3_8b_shape():
+def _workload(name):
+    from dataclasses import replace
+    from workload.configs import evenly_spaced_layers
+    if name == "qwen3-32b-d5":
+        wl = get_config("qwen3-32b")
+        dm = replace(wl.dims, n_layers=5, capture_layers=evenly_spaced_layers(5, 5))
+        return wl.with_(name=name, dims=dm, batch=1)
+    return get_config(name)
+
+
+@pytest.mark.parametrize("name", ["qwen3-8b", "qwen3-1.7b", "qwen3-32b-d5"])
+def test_round_parity_full_width(name):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from oracle import Mode, OracleDFlow, OracleModel
     from paper_2609_06498_amd import Runtime
     from paper_2609_06498_amd.session import Session
-    wl = get_config("qwen3-8b")
+    wl = _workload(name)
     dm, B, K, V = wl.dims, wl.block, wl.K, wl.dims.vocab
     prompt = make_prompts(wl)[0][:CTX]
     print(f"[fullsize] {wl.name} ctx {CTX} rounds {ROUNDS}", flush=True)
@@ -87,7 +108,7 @@ def test_round_parity_qwen3_8b_shape():
         bound = {}
         for name, (dev, ref, ref16) in g.items():
             noise = rel_rows(ref16, ref).max()
-            bound[name] = max(TOL[dm.dtype], NOISE_FACTOR * noise)
+            bound[name] = min(NOISE_CAP, max(TOL[dm.dtype], NOISE_FACTOR * noise))
             e = rel_rows(dev, ref).max()
             print(f"[fullsize] r{r} {name}: device vs fp32 oracle {e:.3e}, bf16 oracle vs fp32 oracle {noise:.3e}",
                   flush=True)
