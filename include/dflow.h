@@ -234,6 +234,15 @@ int dflow_accept_and_carry(dflow_ctx* ctx, hipStream_t stream, int nseq, const i
  * seq_len..seq_len+accept_len (the name follows the paper's round contract). */
 int kv_commit(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* accept_len, int32_t* seq_len);
 
+/* Serving support (continuous batching keeps the active sequences in slots
+ * 0..nseq-1): moves the per-sequence state the library keeps between rounds
+ * -- the carry record and the projected feature rows of the last verify, which
+ * the next dflow_draft_block relays (Sec. 4.2) -- from slot `from` to slot `to`
+ * (overwriting it).  The caller moves its own per-slot state: the page-table
+ * row (the KV and drafter-context pages follow it), sequence length and anchor.
+ * Slots must be in 0..max_batch-1; asynchronous on `stream`. */
+int dflow_move_slot(dflow_ctx* ctx, hipStream_t stream, int from, int to);
+
 /* Measurement construct (not part of the method): builds the verified block
  * [anchor, forced drafts] from a target trajectory traj [b, traj_stride]
  * (absolute positions, traj_len valid entries) and this round's plan

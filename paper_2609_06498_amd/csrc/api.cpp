@@ -639,6 +639,19 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
   return DFLOW_OK;
 }
 
+extern "C" int dflow_move_slot(dflow_ctx* c, hipStream_t st, int from, int to) {
+  if (!c) return fail(DFLOW_EINVAL, "move_slot: null context");
+  if (from < 0 || from >= c->dm.max_batch || to < 0 || to >= c->dm.max_batch)
+    return fail(DFLOW_EINVAL, "move_slot: slots %d -> %d outside 0..%d", from, to, c->dm.max_batch - 1);
+  if (from == to) return DFLOW_OK;
+  const size_t frow = (size_t)c->dm.block * c->dm.d * c->elt;
+  HIPCHK(hipMemcpyAsync(c->carry_rec + (size_t)to * CARRY_REC, c->carry_rec + (size_t)from * CARRY_REC,
+                        CARRY_REC * sizeof(int), hipMemcpyDeviceToDevice, st));
+  HIPCHK(hipMemcpyAsync((char*)c->f + (size_t)to * frow, (const char*)c->f + (size_t)from * frow, frow,
+                        hipMemcpyDeviceToDevice, st));
+  return DFLOW_OK;
+}
+
 extern "C" int dflow_bench_force_drafts(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* traj,
                                         int traj_stride, int traj_len, const int8_t* mode, const int32_t* tok,
                                         const int32_t* anchor, const int32_t* start_pos, int32_t* block_tok) {

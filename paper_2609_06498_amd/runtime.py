@@ -78,6 +78,7 @@ EXPORTS = {
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p]),
     "kv_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_move_slot": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]),
     "dflow_bench_force_drafts": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                 ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
@@ -261,6 +262,9 @@ class Runtime:
 
     def kv_commit(self, nseq, accept_len, seq_len):
         self._check(self.lib.kv_commit(self.ctx, _stream(), nseq, _ptr(accept_len), _ptr(seq_len)), "kv_commit")
+
+    def move_slot(self, src: int, dst: int):
+        self._check(self.lib.dflow_move_slot(self.ctx, _stream(), int(src), int(dst)), "dflow_move_slot")
 
     def force_drafts(self, nseq, traj, traj_len, mode, tok, anchor, start_pos, block_tok):
         self._check(self.lib.dflow_bench_force_drafts(self.ctx, _stream(), nseq, _ptr(traj), int(traj.shape[1]),
