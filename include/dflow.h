@@ -60,8 +60,8 @@
  *    bf16; 4, 16 for f32):
  *      K (slot, e): ((slot/16 * head_dim/KT + e/KT) * 64 + (e%KT)/KL * 16
  *                    + slot%16) * KL + e%KL
- *      V (slot, e): ((slot/16 * head_dim/16 + e/16) * 64 + (slot%16)/4 * 16
- *                    + e%16) * 4 + slot%4
+ *      V (slot, e): ((slot/(4 KL) * head_dim/16 + e/16) * 64 + (slot%16)/4 * 16
+ *                    + e%16) * KL + (slot%(4 KL))/16 * 4 + slot%4
  *    The drafter's context cache has the same layout with n_draft_layers
  *    layers and shares the page table.
  */

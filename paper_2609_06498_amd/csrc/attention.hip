@@ -37,23 +37,69 @@ __device__ inline f32x4_t mma_pv_frag<float>(const float p[4], const float4& vb,
   return acc;
 }
 
+// 16 bytes of storage-type values <-> fp32
+template <typename T> struct Chunk;
+template <> struct Chunk<bf16> {
+  __device__ static inline void unpack(const u32x4_t& u, float* x) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = bf2f(u[i] & 0xFFFFu);
+      x[2 * i + 1] = bf2f(u[i] >> 16);
+    }
+  }
+  __device__ static inline u32x4_t pack(const float* x) {
+    return u32x4_t{f2bf2(x[0], x[1]), f2bf2(x[2], x[3]), f2bf2(x[4], x[5]), f2bf2(x[6], x[7])};
+  }
+  __device__ static inline bf16 elem(const u32x4_t& u, int i) {
+    return bf16{(uint16_t)((i & 1) ? (u[i >> 1] >> 16) : (u[i >> 1] & 0xFFFFu))};
+  }
+};
+template <> struct Chunk<float> {
+  __device__ static inline void unpack(const u32x4_t& u, float* x) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = __uint_as_float(u[i]);
+  }
+  __device__ static inline u32x4_t pack(const float* x) {
+    return u32x4_t{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3])};
+  }
+  __device__ static inline float elem(const u32x4_t& u, int i) { return __uint_as_float(u[i]); }
+};
+
+// Offsets of element (slot, e) of a page block in matrix-core fragment order.
+template <typename T, int DH>
+__device__ inline int kfrag_off(int slot, int e) {
+  constexpr int KL = TT<T>::KL, KT = TT<T>::KT, KS = DH / KT;
+  return (((slot / 16) * KS + e / KT) * 64 + ((e % KT) / KL) * 16 + slot % 16) * KL + e % KL;
+}
+// V: a lane fragment holds KL keys of one channel: keys 4g..4g+3 of the
+// KL/4 consecutive 16-key tiles of a 4*KL-key group, g = lane/16.
+template <typename T, int DH>
+__device__ inline int vfrag_off(int slot, int e) {
+  constexpr int KL = TT<T>::KL, DT = DH / 16, VG = 4 * KL;
+  return (((slot / VG) * DT + e / 16) * 64 + ((slot % 16) / 4) * 16 + e % 16) * KL + ((slot % VG) / 16) * 4 + slot % 4;
+}
+
 // One workgroup of NW waves per (sequence, kv head, split of SplitKeys keys at
-// fixed absolute positions).
-//  1. The split's K/V pages are staged into LDS, all loads in flight at once.
-//     Meanwhile the waves apply QK-norm + RoPE to the group's R = Bq * G query
-//     rows (one row per wave and pass, one rotate-half pair per lane) into an
-//     LDS query tile, and to the block's own key rows that fall into this
-//     split (V copied).
-//  2. The block rows' keys and values are written into the staged tiles and
-//     into the paged cache.
-//  3. Work units are (16-row group, page subset): with nrg row groups, WPR =
-//     min(pages, NW / nrg) waves share a row group and take pages part,
-//     part + WPR, ... with an online softmax (S^T = K Q^T on the matrix cores,
-//     mask, running max/sum, P V).  Their partials are merged through LDS in
-//     part order and written as this split's partial (m, l, O); with WPR = 1
-//     each wave owns whole row groups and writes directly.
-// WPR depends only on (Bq, G), so a row's arithmetic does not depend on the
-// batch it is part of.
+// fixed absolute positions); wave w owns the 16-row groups w, w + NW, ...
+// Attention rows of a group are (block row j, query head g) pairs, R = Bq * G.
+//  1. Loads are issued in the order their consumers need them and all stay in
+//     flight together: the query rows and the block's own key/value rows of
+//     this split (fused variant) first, then the split's K/V pages, page by
+//     page, into registers.  Vector loads complete in issue order, so the
+//     query math below waits only for the query loads.
+//  2. Fused variant: QK-norm + RoPE of the R query rows into an LDS query
+//     tile; QK-norm + RoPE of the block rows' keys, written to the paged
+//     cache and to an LDS row tile together with their values.
+//  3. Page by page in key order: the staged page goes to LDS, the block rows
+//     replace their (stale) slots, and every wave computes the masked scores
+//     of its first row group against the page (S^T = K Q^T on the matrix
+//     cores), so early pages are consumed while later ones still arrive.
+//  4. One softmax over the split's scores (row maximum, exp2, sum), P V on
+//     the matrix cores, and the split partial (m, l, O) of the row group.  A
+//     wave's further row groups then run over the resident pages.  The
+//     combine kernel merges the splits in split order.
+// A row's arithmetic depends only on its own visible keys and the fixed split
+// boundaries, never on the batch it is part of.
 template <typename T, int DH, int NW, bool FUSED>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
@@ -64,16 +110,20 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int PG = PAGE * DH;               // elements of one K (or V) page block
   constexpr int NT = NW * 64;
   constexpr int HALF = DH / 2;
+  constexpr int V16 = PG * (int)sizeof(T) / 16;   // 16-byte vectors per page block
+  constexpr int PER = V16 / NT;                   // per thread, page and K or V
+  static_assert(V16 % NT == 0, "page blocks split evenly over the workgroup");
   typedef typename VFrag<T>::type vfrag_t;
   constexpr int QLD = DH + KL;                // padded row of the query tile
-  constexpr int MAXB = 4;                     // block rows per wave held in registers (Bq <= 64)
+  constexpr int CE = 16 / (int)sizeof(T);     // channels per 16-byte chunk
+  constexpr int LPR = DH / CE;                // lanes per head row
+  constexpr int RPI = 64 / LPR;               // head rows per wave and pass
+  constexpr int QI = FUSED ? (64 + NW * RPI - 1) / (NW * RPI) : 1;   // query passes per wave (R <= 64)
+  constexpr int RC = CE * 8 / 16;             // 16-byte chunks of the lane's CE (cos, sin) pairs
+  static_assert(CE == KL, "a key chunk is one fragment run of the paged layout");
   extern __shared__ __align__(16) unsigned char smem[];
   T* lk = reinterpret_cast<T*>(smem);         // [NPG][PG] keys, fragment order
   T* lv = lk + (size_t)NPG * PG;              // [NPG][PG] values, fragment order
-  T* lq = lv + (size_t)NPG * PG;              // [R][QLD] queries after QK-norm + RoPE
-  float* mo = reinterpret_cast<float*>(smem); // merge area [NW][16][DH], reuses the K/V tiles after use
-  float* s_ml = reinterpret_cast<float*>(lq); // merge (m, l) [NW][16][2], reuses the query tile after use
-  __shared__ int s_page[NPG];
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -91,260 +141,230 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   const int cap = p.max_pages * PAGE;
   if (threadIdx.x == 0 && split == 0 && kv_len > cap) set_status(p.status, ST_CAPACITY);
   if (key0 >= kv_len) return;                 // uniform over the workgroup
+  T* lq = lv + (size_t)NPG * PG;              // [R][QLD] queries after QK-norm + RoPE (fused)
+  T* ln = lq + (size_t)(FUSED ? R : 0) * QLD; // [rows][2][DH] block rows' keys and values (fused)
 
-  if (threadIdx.x < NPG) {
-    const int pidx = min(key0 / PAGE + (int)threadIdx.x, p.max_pages - 1);
-    const int pg = p.page_table[(size_t)s * p.max_pages + pidx];
-    s_page[threadIdx.x] = (key0 + (int)threadIdx.x * PAGE < kv_len && pg >= 0 && pg < p.num_pages) ? pg : -1;
-  }
-  __syncthreads();
-
-  // ---- 1. stage all pages (absent pages read page 0 of the pool; never used) ...
-  constexpr int V16 = PG * (int)sizeof(T) / 16;   // 16-byte vectors per page block
-  constexpr int PER = (NPG * V16 + NT - 1) / NT;  // per thread, K and V each (the last one partial)
-  u32x4_t kr[PER], vr[PER];
-#pragma unroll
-  for (int it = 0; it < PER; ++it) {
-    const int idx = min(threadIdx.x + it * NT, NPG * V16 - 1);   // a clamped duplicate is never stored
-    const int pi = idx / V16, vi = idx - pi * V16;
-    const size_t off = ((size_t)max(s_page[pi], 0) * p.Hkv + kvh) * PG;
-    kr[it] = ((const gu4*)(reinterpret_cast<const T*>(p.kpool) + off))[vi];
-    vr[it] = ((const gu4*)(reinterpret_cast<const T*>(p.vpool) + off))[vi];
-  }
-  // ... while the query rows get QK-norm + RoPE (lane i < DH/2 owns channels i, i + DH/2)
+  // ---- 1. loads, in this order: page ids; query rows and the block rows of
+  // the split as raw storage values (clamped rows are loaded and never
+  // stored); then, once the page ids are in, the K/V pages.  Nothing between
+  // the first load and the last K/V load waits on memory.
+  // (one vector load: lane i < NPG reads page i; broadcast once it is needed)
+  const int pvl = p.page_table[(size_t)s * p.max_pages + min(key0 / PAGE + (lane < NPG ? lane : 0), p.max_pages - 1)];
+  // Head rows (queries, block keys/values) are handled as 16-byte chunks: LPR
+  // lanes per row, lane chunk cl holds channels [cl*CE, cl*CE + CE); its
+  // rotate-half partner chunk sits LPR/2 lanes away and shares its RoPE angles.
   const T* qkv = reinterpret_cast<const T*>(p.qkv);
+  const int cl = lane % LPR, rl = lane / LPR;
+  const int rc0 = (cl % (LPR / 2)) * CE;      // RoPE angle index of the chunk's first channel
+  u32x4_t qraw[QI], qrope[QI][RC];
   if constexpr (FUSED) {
-    const T* gq = reinterpret_cast<const T*>(p.q_norm);
-    const float g1 = lane < HALF ? TT<T>::ld(gq, lane) : 0.f;
-    const float g2 = lane < HALF ? TT<T>::ld(gq, lane + HALF) : 0.f;
-    constexpr int QB = 4;                      // rows per wave per batch: all their loads in flight together
-    for (int rr0 = w; rr0 < R; rr0 += QB * NW) {   // uniform per wave
-      float x1[QB], x2[QB];
-      float2 c[QB];
 #pragma unroll
-      for (int b = 0; b < QB; ++b) {
-        const int rr = min(rr0 + b * NW, R - 1);   // clamped rows are computed and not stored
-        const int j = rr / G, g = rr - j * G;
-        const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH;
-        const int pos = min(t0 + j, cap - 1);     // past capacity: status set above
-        const int l = lane < HALF ? lane : 0;
-        x1[b] = TT<T>::ld(src, l);
-        x2[b] = TT<T>::ld(src, l + HALF);
-        c[b] = p.rope[(size_t)pos * HALF + l];
-      }
+    for (int it = 0; it < QI; ++it) {
+      const int rr = min((w + NW * it) * RPI + rl, R - 1);   // clamped rows are computed and not stored
+      const int j = rr / G, g = rr - j * G;
+      qraw[it] = *(const gu4*)(qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH + cl * CE);
+      const gu4* rp = (const gu4*)(p.rope + (size_t)min(t0 + j, cap - 1) * HALF + rc0);   // past capacity: status set above
 #pragma unroll
-      for (int b = 0; b < QB; ++b) {
-        const int rr = rr0 + b * NW;
-        const float v1 = lane < HALF ? x1[b] : 0.f, v2 = lane < HALF ? x2[b] : 0.f;
-        const float r = rsqrtf(wave_sum(v1 * v1 + v2 * v2) / (float)DH + p.eps);
-        if (rr < R && lane < HALF) {
-          const float y1 = v1 * r * g1;
-          const float y2 = v2 * r * g2;
-          TT<T>::st(lq, (size_t)rr * QLD + lane, y1 * c[b].x - y2 * c[b].y);
-          TT<T>::st(lq, (size_t)rr * QLD + lane + HALF, y2 * c[b].x + y1 * c[b].y);
-        }
-      }
+      for (int c = 0; c < RC; ++c) qrope[it][c] = rp[c];
     }
   }
-  // ... and the block's own key rows in this split (wave w: rows jlo + w + NW * b)
-  const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SK - t0);
-  float nk1[MAXB], nk2[MAXB], nv1[MAXB], nv2[MAXB];
+  const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SK - t0);   // block rows in this split
+  u32x4_t kraw, vraw, krope[RC];
+  auto load_rows = [&](int it) {
+    const int j = max(0, min(jlo + (w + NW * it) * RPI + rl, jhi - 1));   // clamped rows are not stored
+    const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)p.Hq * DH + (size_t)kvh * DH + cl * CE;
+    kraw = *(const gu4*)src;
+    vraw = *(const gu4*)(src + (size_t)p.Hkv * DH);
+    const gu4* rp = (const gu4*)(p.rope + (size_t)min(t0 + j, cap - 1) * HALF + rc0);
+#pragma unroll
+    for (int c = 0; c < RC; ++c) krope[c] = rp[c];
+  };
+  u32x4_t gq, gk;                             // QK-norm gains of the lane's chunk
   if constexpr (FUSED) {
-    const T* gk = reinterpret_cast<const T*>(p.k_norm);
-#pragma unroll
-    for (int b = 0; b < MAXB; ++b) {
-      const int j = jlo + w + NW * b;
-      if (j >= jhi) break;                     // uniform per wave
-      const int pos = min(t0 + j, cap - 1);
-      const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)p.Hq * DH + (size_t)kvh * DH;
-      const T* vsrc = src + (size_t)p.Hkv * DH;
-      float x1 = 0.f, x2 = 0.f;
-      if (lane < HALF) { x1 = TT<T>::ld(src, lane); x2 = TT<T>::ld(src, lane + HALF); }
-      const float r = rsqrtf(wave_sum(x1 * x1 + x2 * x2) / (float)DH + p.eps);
-      nk1[b] = nk2[b] = 0.f;
-      if (lane < HALF) {
-        const float2 c = p.rope[(size_t)pos * HALF + lane];
-        const float y1 = x1 * r * TT<T>::ld(gk, lane);
-        const float y2 = x2 * r * TT<T>::ld(gk, lane + HALF);
-        nk1[b] = y1 * c.x - y2 * c.y;
-        nk2[b] = y2 * c.x + y1 * c.y;
-      }
-      nv1[b] = TT<T>::ld(vsrc, lane);
-      nv2[b] = lane + 64 < DH ? TT<T>::ld(vsrc, lane + 64) : 0.f;
-    }
+    load_rows(0);
+    gq = *(const gu4*)(reinterpret_cast<const T*>(p.q_norm) + cl * CE);
+    gk = *(const gu4*)(reinterpret_cast<const T*>(p.k_norm) + cl * CE);
   }
+  __builtin_amdgcn_sched_barrier(0);
+  int pgid[NPG];
+  unsigned present = 0;                       // pages holding keys of the sequence, with valid ids
 #pragma unroll
-  for (int it = 0; it < PER; ++it) {
-    const int idx = threadIdx.x + it * NT;
-    if ((NPG * V16) % NT == 0 || idx < NPG * V16) {
-      reinterpret_cast<u32x4_t*>(lk)[idx] = kr[it];
-      reinterpret_cast<u32x4_t*>(lv)[idx] = vr[it];
-    }
+  for (int i = 0; i < NPG; ++i) {
+    const int pv = __builtin_amdgcn_readlane(pvl, i);
+    const bool ok = key0 + i * PAGE < kv_len && pv >= 0 && pv < p.num_pages;
+    pgid[i] = ok ? pv : 0;                    // absent pages read page 0 of the pool, never used
+    present |= ok ? (1u << i) : 0u;
   }
-  __syncthreads();
+  u32x4_t kr[NPG][PER], vr[NPG][PER];
+#pragma unroll
+  for (int i = 0; i < NPG; ++i) {
+    const size_t off = ((size_t)pgid[i] * p.Hkv + kvh) * PG;
+    const gu4* kg = (const gu4*)(reinterpret_cast<const T*>(p.kpool) + off);
+    const gu4* vg = (const gu4*)(reinterpret_cast<const T*>(p.vpool) + off);
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      kr[i][it] = kg[threadIdx.x + it * NT];
+      vr[i][it] = vg[threadIdx.x + it * NT];
+    }
+    __builtin_amdgcn_sched_barrier(0);        // issue order = page order = consumption order
+  }
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int i = 0; i < NPG; ++i)
+      if (key0 + i * PAGE < kv_len && !((present >> i) & 1u)) set_status(p.status, ST_BAD_PAGE);
+  }
 
-  // ---- 2. the block rows' keys and values into the staged tiles and the cache
+  // ---- 2. query tile; block rows to the cache and the row tile
+  // RMSNorm over the row's LPR lanes, gain, then RoPE against the partner chunk
+  auto norm_rope = [&](const u32x4_t& raw, const u32x4_t& gain, const u32x4_t (&rope)[RC], u32x4_t& out) {
+    float x[CE], g[CE], y[CE], cs[2 * CE];
+    Chunk<T>::unpack(raw, x);
+    Chunk<T>::unpack(gain, g);
 #pragma unroll
-  for (int b = 0; b < (FUSED ? MAXB : 0); ++b) {
-    const int j = jlo + w + NW * b;
-    if (j >= jhi) break;                       // uniform per wave
-    const int pos = t0 + j;
-    if (pos >= cap) continue;                  // status set above
-    const int pi = (pos - key0) / PAGE, slot = pos % PAGE;
-    const int gpage = s_page[pi];
-    if (lane == 0 && gpage < 0) set_status(p.status, ST_BAD_PAGE);
-    T* kt_l = lk + (size_t)pi * PG;
-    T* vt_l = lv + (size_t)pi * PG;
-    T* kt_g = gpage >= 0 ? reinterpret_cast<T*>(p.kpool) + ((size_t)gpage * p.Hkv + kvh) * PG : nullptr;
-    T* vt_g = gpage >= 0 ? reinterpret_cast<T*>(p.vpool) + ((size_t)gpage * p.Hkv + kvh) * PG : nullptr;
-    auto koff = [&](int d) -> int {
-      return (((slot / 16) * KS + d / KT) * 64 + ((d % KT) / KL) * 16 + slot % 16) * KL + d % KL;
-    };
-    auto voff = [&](int e) -> int {
-      return (((slot / 16) * DT + e / 16) * 64 + ((slot % 16) / 4) * 16 + e % 16) * 4 + slot % 4;
-    };
-    if (lane < HALF) {
-      TT<T>::st(kt_l, koff(lane), nk1[b]);
-      TT<T>::st(kt_l, koff(lane + HALF), nk2[b]);
-      if (kt_g) {
-        TT<T>::st(kt_g, koff(lane), nk1[b]);
-        TT<T>::st(kt_g, koff(lane + HALF), nk2[b]);
-      }
+    for (int c = 0; c < RC; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cs[4 * c + e] = __uint_as_float(rope[c][e]);
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < CE; ++i) ss += x[i] * x[i];
+#pragma unroll
+    for (int o = LPR / 2; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    const float r = rsqrtf(ss / (float)DH + p.eps);
+#pragma unroll
+    for (int i = 0; i < CE; ++i) y[i] = x[i] * r * g[i];
+    const bool lo = cl < LPR / 2;
+#pragma unroll
+    for (int i = 0; i < CE; ++i) {
+      const float q = __shfl_xor(y[i], LPR / 2, 64);
+      x[i] = lo ? y[i] * cs[2 * i] - q * cs[2 * i + 1] : y[i] * cs[2 * i] + q * cs[2 * i + 1];
     }
-    TT<T>::st(vt_l, voff(lane), nv1[b]);
-    if (vt_g) TT<T>::st(vt_g, voff(lane), nv1[b]);
-    if (lane + 64 < DH) {
-      TT<T>::st(vt_l, voff(lane + 64), nv2[b]);
-      if (vt_g) TT<T>::st(vt_g, voff(lane + 64), nv2[b]);
+    out = Chunk<T>::pack(x);
+  };
+  if constexpr (FUSED) {
+#pragma unroll
+    for (int it = 0; it < QI; ++it) {
+      const int rr = (w + NW * it) * RPI + rl;
+      u32x4_t y;
+      norm_rope(qraw[it], gq, qrope[it], y);
+      if (rr < R) *reinterpret_cast<u32x4_t*>(lq + (size_t)rr * QLD + cl * CE) = y;
+    }
+    for (int it = 0; jlo + (w + NW * it) * RPI < jhi; ++it) {   // uniform per wave
+      if (it > 0) load_rows(it);
+      u32x4_t y;
+      norm_rope(kraw, gk, krope, y);
+      const int j = jlo + (w + NW * it) * RPI + rl;
+      const int pos = t0 + j;
+      if (j >= jhi) continue;
+      T* row = ln + (size_t)(j - jlo) * 2 * DH;
+      *reinterpret_cast<u32x4_t*>(row + cl * CE) = y;
+      *reinterpret_cast<u32x4_t*>(row + DH + cl * CE) = vraw;
+      if (pos >= cap) continue;                // status set above
+      const int pi = (pos - key0) / PAGE, slot = pos % PAGE;
+      if (!((present >> pi) & 1u)) continue;   // status set above
+      int gp = 0;
+#pragma unroll
+      for (int i = 0; i < NPG; ++i) gp = i == pi ? pgid[i] : gp;
+      T* kt_g = reinterpret_cast<T*>(p.kpool) + ((size_t)gp * p.Hkv + kvh) * PG;
+      T* vt_g = reinterpret_cast<T*>(p.vpool) + ((size_t)gp * p.Hkv + kvh) * PG;
+      *reinterpret_cast<u32x4_t*>(kt_g + kfrag_off<T, DH>(slot, cl * CE)) = y;   // CE = KL consecutive channels
+#pragma unroll
+      for (int i = 0; i < CE; ++i) vt_g[vfrag_off<T, DH>(slot, cl * CE + i)] = Chunk<T>::elem(vraw, i);
     }
   }
-  __syncthreads();
 
-  // ---- 3. row groups x page subsets
-  // merge area (units x 16 x DH fp32) must fit in the K/V tiles it reuses
-  constexpr int MAXU = (2 * NPG * PG * (int)sizeof(T)) / (16 * DH * 4) < NW ? (2 * NPG * PG * (int)sizeof(T)) / (16 * DH * 4) : NW;
-  int wpr = MAXU / nrg < NPG ? MAXU / nrg : NPG;
-  if (wpr < 1) wpr = 1;
-  const int units = nrg * wpr;                 // waves with work in a pass (merge) or row groups (wpr = 1)
-  auto run_unit = [&](int rg, int part, u32x4_t (&qf)[KS], float& mrow, float& lrow, f32x4_t (&o)[DT]) {
-    {
-      const int qr = min(rg * 16 + (lane & 15), R - 1);
-      if constexpr (FUSED) {
-#pragma unroll
-        for (int k = 0; k < KS; ++k)
-          qf[k] = *reinterpret_cast<const u32x4_t*>(lq + (size_t)qr * QLD + k * KT + (lane >> 4) * KL);
-      } else {
-        const int j = qr / G, g = qr - j * G;
-        const T* qrow = reinterpret_cast<const T*>(p.q) + ((size_t)(s * p.Bq + j) * p.Hq + kvh * G + g) * DH;
-#pragma unroll
-        for (int k = 0; k < KS; ++k) qf[k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
-      }
-    }
-    mrow = -INFINITY;
-    lrow = 0.f;
-#pragma unroll
-    for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // ---- 3. page by page: scores as pages land, then one softmax over the split
+  // The softmax runs in log2 units (scale folded with log2 e) with exp2; the
+  // split partial is (M, sum 2^(s - M), sum 2^(s - M) v) with
+  // M the row's maximum over the split's visible keys, so no running rescale.
+  typedef float score_t[4][4];               // [key tile][key within the lane's group of 4]
+  auto scores = [&](int rg, int pi, const u32x4_t (&qf)[KS], score_t& sc) {
     const int ar = rg * 16 + (lane & 15);
     const bool row_ok = ar < R;
     const int pos_row = t0 + (row_ok ? ar / G : 0);
-    bool first = true;                        // uniform: the unit's first present page
-    for (int pi = part; pi < NPG; pi += wpr) {
-      if (s_page[pi] < 0) continue;          // uniform
-      const int kp0 = key0 + pi * PAGE;
-      const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)pi * PG);
-      const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
-      // every key of the page precedes the block and every row is valid: no mask
-      const bool full = kp0 + PAGE <= t0 && rg * 16 + 16 <= R;   // uniform
-      // scores in log2 units (scale folded with log2 e), so the softmax uses exp2
-      float sc[4][4];
+    const int kp0 = key0 + pi * PAGE;
+    const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)pi * PG);
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kt = 0; kt < 4; ++kt) {
+      f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[k], acc);
+      for (int k = 0; k < KS; ++k) acc = mma_frag(T(), kb[(kt * KS + k) * 64 + lane], qf[k], acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) sc[kt][r] = acc[r] * sl2;
-      }
-      if (!full) {
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
-            const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
-            if (!vis) sc[kt][r] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
+      for (int r = 0; r < 4; ++r) sc[kt][r] = acc[r];
+    }
+    // every key of the page precedes the block and every row is valid: no mask
+    const bool full = kp0 + PAGE <= t0 && rg * 16 + 16 <= R;   // uniform
+    if (!full) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // rows with nothing visible so far keep m = -inf, l = 0 and a zero output;
-      // control flow stays uniform (the matrix-core ops and shuffles need all lanes)
-      const float mnew = first ? mx : fmaxf(mrow, mx);
-      float ls = 0.f;
-      if (full) {                              // mnew is finite and no score is masked
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            sc[kt][r] = exp2f(sc[kt][r] - mnew);
-            ls += sc[kt][r];
-          }
-      } else {
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float e = (sc[kt][r] == -INFINITY) ? 0.f : exp2f(sc[kt][r] - mnew);
-            sc[kt][r] = e;
-            ls += e;
-          }
-      }
-      ls += __shfl_xor(ls, 16, 64);
-      ls += __shfl_xor(ls, 32, 64);
-      if (first) {                             // the output is still zero: nothing to rescale
-        lrow = ls;
-      } else {
-        const float alpha = (mrow == -INFINITY) ? (mnew == -INFINITY ? 1.f : 0.f) : exp2f(mrow - mnew);
-        lrow = lrow * alpha + ls;
-        float al[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * (lane >> 4) + r, 64);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) o[dt][r] *= al[r];
-      }
-      mrow = mnew;
-      first = false;
-      if constexpr (KL == 8) {
-        // P V with 32 keys per matrix-core op: lane group g supplies keys
-        // 4g..4g+3 of key tiles 2c and 2c+1, and the same keys of V
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const u32x4_t pa = {f2bf2(sc[2 * c][0], sc[2 * c][1]), f2bf2(sc[2 * c][2], sc[2 * c][3]),
-                              f2bf2(sc[2 * c + 1][0], sc[2 * c + 1][1]), f2bf2(sc[2 * c + 1][2], sc[2 * c + 1][3])};
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const uint2 v0 = reinterpret_cast<const uint2*>(vb)[((2 * c) * DT + dt) * 64 + lane];
-            const uint2 v1 = reinterpret_cast<const uint2*>(vb)[((2 * c + 1) * DT + dt) * 64 + lane];
-            const u32x4_t vv = {v0.x, v0.y, v1.x, v1.y};
-            o[dt] = mma_frag(T(), pa, vv, o[dt]);
-          }
+        for (int r = 0; r < 4; ++r) {
+          const int key = kp0 + kt * 16 + 4 * (lane >> 4) + r;
+          const bool vis = row_ok && key < kv_len && (!p.causal || key <= pos_row);
+          if (!vis) sc[kt][r] = -INFINITY;
         }
-      } else {
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
-      }
     }
   };
-  auto write_partial = [&](int rg, float mrow, float lrow, const f32x4_t (&o)[DT]) {
+  // softmax over the present pages, P V, and the split partial of row group rg
+  auto finish = [&](int rg, score_t (&sc)[NPG]) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int pi = 0; pi < NPG; ++pi)
+      if ((present >> pi) & 1u)                // uniform
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[pi][kt][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    // scores are raw dot products; in log2 units a score is s * sl2 and the
+    // row maximum m = mx * sl2 (sl2 > 0).  A row with no visible key keeps
+    // m = -inf, l = 0 and a zero output: its scores are all -inf and
+    // exponentiate to 0 against a finite reference.
+    mx *= sl2;
+    const float mref = mx == -INFINITY ? 0.f : mx;
+    float ls = 0.f;
+#pragma unroll
+    for (int pi = 0; pi < NPG; ++pi) {
+      if (!((present >> pi) & 1u)) continue;   // uniform
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          // hardware 2^x: arguments are <= 0; results below 2^-126 flush to 0
+          const float e = __builtin_amdgcn_exp2f(fmaf(sc[pi][kt][r], sl2, -mref));
+          sc[pi][kt][r] = e;
+          ls += e;
+        }
+    }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    f32x4_t o[DT];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int pi = 0; pi < NPG; ++pi) {
+      if (!((present >> pi) & 1u)) continue;   // uniform
+      if constexpr (KL == 8) {
+        // P V with 32 keys per matrix-core op: lane group g supplies keys
+        // 4g..4g+3 of key tiles 2c and 2c+1, and V holds the same keys in
+        // one 16-byte fragment
+        const u32x4_t* vb = reinterpret_cast<const u32x4_t*>(lv + (size_t)pi * PG);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const float (&a)[4] = sc[pi][2 * c];
+          const float (&b)[4] = sc[pi][2 * c + 1];
+          const u32x4_t pa = {f2bf2(a[0], a[1]), f2bf2(a[2], a[3]), f2bf2(b[0], b[1]), f2bf2(b[2], b[3])};
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_frag(T(), pa, vb[(c * DT + dt) * 64 + lane], o[dt]);
+        }
+      } else {
+        const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[pi][kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
+      }
+    }
     const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + rg) * p.nsplit + split;
     float* po = p.part_o + pidx * 16 * DH;
 #pragma unroll
@@ -352,78 +372,61 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) po[(4 * (lane >> 4) + r) * DH + dt * 16 + (lane & 15)] = o[dt][r];
     if (lane < 16) {
-      p.part_ml[pidx * 32 + 2 * lane] = mrow;
-      p.part_ml[pidx * 32 + 2 * lane + 1] = lrow;
+      p.part_ml[pidx * 32 + 2 * lane] = mx;
+      p.part_ml[pidx * 32 + 2 * lane + 1] = ls;
+    }
+  };
+  auto load_q = [&](int rg, u32x4_t (&qf)[KS]) {
+    const int qr = min(rg * 16 + (lane & 15), R - 1);
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int k = 0; k < KS; ++k)
+        qf[k] = *reinterpret_cast<const u32x4_t*>(lq + (size_t)qr * QLD + k * KT + (lane >> 4) * KL);
+    } else {
+      const int j = qr / G, g = qr - j * G;
+      const T* qrow = reinterpret_cast<const T*>(p.q) + ((size_t)(s * p.Bq + j) * p.Hq + kvh * G + g) * DH;
+#pragma unroll
+      for (int k = 0; k < KS; ++k) qf[k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
     }
   };
 
   u32x4_t qf[KS];
-  float mrow, lrow;
-  f32x4_t o[DT];
-  if (wpr == 1) {
-    for (int rg = w; rg < nrg; rg += NW) {     // uniform per wave; no barrier inside
-      run_unit(rg, 0, qf, mrow, lrow, o);
-      write_partial(rg, mrow, lrow, o);
+  score_t sc[NPG];
+  const bool own = w < nrg;                    // uniform: the wave has a row group
+#pragma unroll
+  for (int pi = 0; pi < NPG; ++pi) {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      reinterpret_cast<u32x4_t*>(lk + (size_t)pi * PG)[threadIdx.x + it * NT] = kr[pi][it];
+      reinterpret_cast<u32x4_t*>(lv + (size_t)pi * PG)[threadIdx.x + it * NT] = vr[pi][it];
     }
-    return;
-  }
-  const bool active = w < units;
-  const int rg = w % nrg, part = w / nrg;
-  if (active) run_unit(rg, part, qf, mrow, lrow, o);
-  __syncthreads();                             // every wave is done with the K/V tiles
-  if (active) {
-    float* mw = mo + (size_t)w * 16 * DH;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)   // 16-column blocks XOR-swizzled by row/4: conflict-free stores
-        mw[(4 * (lane >> 4) + r) * DH + ((dt * 16 + (lane & 15)) ^ ((lane >> 4) << 4))] = o[dt][r];
-    if (lane < 16) {
-      s_ml[(w * 16 + lane) * 2] = mrow;
-      s_ml[(w * 16 + lane) * 2 + 1] = lrow;
-    }
-  }
-  __syncthreads();
-  // merge the wpr partials of each row group in part order; lane handles 4
-  // consecutive channels, all partial loads in flight together
-  for (int e4 = threadIdx.x; e4 < nrg * 4 * DH; e4 += NT) {
-    const int e = e4 * 4;
-    const int g = e / (16 * DH), rem = e - g * 16 * DH, row = rem / DH, dd = rem - row * DH;
-    float mq[NPG], lq4[NPG];
-    float4 oq[NPG];
-#pragma unroll
-    for (int q = 0; q < NPG; ++q) {
-      if (q < wpr) {                               // uniform
-        const int u = q * nrg + g;
-        mq[q] = s_ml[(u * 16 + row) * 2];
-        lq4[q] = s_ml[(u * 16 + row) * 2 + 1];
-        oq[q] = *reinterpret_cast<const float4*>(mo + ((size_t)u * 16 + row) * DH + (dd ^ (((row >> 2) & 3) << 4)));
-      } else {
-        mq[q] = -INFINITY;
-        lq4[q] = 0.f;
-        oq[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+    if constexpr (FUSED) {
+      // block rows of this page replace the slots staged from the cache
+      const int jp0 = max(jlo, key0 + pi * PAGE - t0), jp1 = min(jhi, key0 + (pi + 1) * PAGE - t0);
+      if (jp0 < jp1) {                         // uniform
+        T* kt_l = lk + (size_t)pi * PG;
+        T* vt_l = lv + (size_t)pi * PG;
+        for (int e = threadIdx.x; e < (jp1 - jp0) * DH; e += NT) {
+          const int j = jp0 + e / DH, d = e % DH;
+          const int slot = (t0 + j) % PAGE;
+          const T* row = ln + (size_t)(j - jlo) * 2 * DH;
+          kt_l[kfrag_off<T, DH>(slot, d)] = row[d];
+          vt_l[vfrag_off<T, DH>(slot, d)] = row[DH + d];
+        }
+        __syncthreads();
       }
     }
-    float M = -INFINITY;
+    if (pi == 0 && own) load_q(w, qf);
+    if (own && ((present >> pi) & 1u)) scores(w, pi, qf, sc[pi]);
+  }
+  if (own) finish(w, sc);
+  for (int rg = w + NW; rg < nrg; rg += NW) {  // uniform per wave; pages resident, no barrier
+    load_q(rg, qf);
 #pragma unroll
-    for (int q = 0; q < NPG; ++q) M = fmaxf(M, mq[q]);
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    float l = 0.f;
-#pragma unroll
-    for (int q = 0; q < NPG; ++q) {
-      const float f = (mq[q] == -INFINITY) ? 0.f : exp2f(mq[q] - M);
-      acc.x += f * oq[q].x;
-      acc.y += f * oq[q].y;
-      acc.z += f * oq[q].z;
-      acc.w += f * oq[q].w;
-      l += f * lq4[q];
-    }
-    const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + g) * p.nsplit + split;
-    *reinterpret_cast<float4*>(p.part_o + (pidx * 16 + row) * DH + dd) = acc;
-    if (dd == 0) {
-      p.part_ml[pidx * 32 + 2 * row] = M;
-      p.part_ml[pidx * 32 + 2 * row + 1] = l;
-    }
+    for (int pi = 0; pi < NPG; ++pi)
+      if ((present >> pi) & 1u) scores(rg, pi, qf, sc[pi]);
+    finish(rg, sc);
   }
 }
 
@@ -460,27 +463,26 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
   TT<T>::st(reinterpret_cast<T*>(p.out), (size_t)row * p.Hq * DH + hq * DH + d, v);
 }
 
-constexpr int ATTN_WAVES = 16;
-
-// Dynamic LDS of the attention kernel: the split's K and V pages plus the
-// query tile (fused variant) or the merge statistics.
+// Dynamic LDS of the attention kernel: the split's K and V pages, plus the
+// query tile and the block rows' key/value tile in the fused variant.
 template <typename T, int DH>
-static size_t attn_lds(bool fused, int R) {
-  const size_t tile = fused ? (size_t)R * (DH + TT<T>::KL) * sizeof(T) : 0;
-  const size_t ml = (size_t)ATTN_WAVES * 16 * 2 * sizeof(float);
-  return 2 * (size_t)SplitKeys<T>::value * DH * sizeof(T) + (tile > ml ? tile : ml);
+static size_t attn_lds(bool fused, int Bq, int G) {
+  const size_t pages = 2 * (size_t)SplitKeys<T>::value * DH * sizeof(T);
+  if (!fused) return pages;
+  const int rows = Bq < SplitKeys<T>::value ? Bq : SplitKeys<T>::value;
+  return pages + ((size_t)Bq * G * (DH + TT<T>::KL) + (size_t)rows * 2 * DH) * sizeof(T);
 }
 static constexpr size_t ATTN_LDS_MAX = 159 * 1024;
 
+// Fused: four waves, one 16-row group each (R = Bq * G <= 64).
 template <typename T, int DH>
 static bool fuses_dh(int Bq, int G) {
-  return Bq <= 4 * ATTN_WAVES && attn_lds<T, DH>(true, Bq * G) <= ATTN_LDS_MAX;
+  return Bq * G <= 64 && attn_lds<T, DH>(true, Bq, G) <= ATTN_LDS_MAX;
 }
 
-template <typename T, int DH, bool FUSED>
+template <typename T, int DH, int NW, bool FUSED>
 static hipError_t launch_k(const AttnParams& p, hipStream_t st) {
-  constexpr int NW = ATTN_WAVES;
-  const size_t lds = attn_lds<T, DH>(FUSED, p.Bq * (p.Hq / p.Hkv));
+  const size_t lds = attn_lds<T, DH>(FUSED, p.Bq, p.Hq / p.Hkv);
   if (lds > ATTN_LDS_MAX) return hipErrorInvalidConfiguration;
   static bool lds_set = false;   // allow the largest dynamic LDS once per instantiation
   if (!lds_set) {
@@ -500,9 +502,11 @@ template <typename T, int DH>
 static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
   if (p.fused) {
     if (!fuses_dh<T, DH>(p.Bq, p.Hq / p.Hkv)) return hipErrorInvalidConfiguration;
-    return launch_k<T, DH, true>(p, st);
+    return launch_k<T, DH, 4, true>(p, st);
   }
-  return launch_k<T, DH, false>(p, st);
+  // one wave per 16-row group up to eight; beyond, waves take several groups
+  if (p.Bq * (p.Hq / p.Hkv) <= 64) return launch_k<T, DH, 4, false>(p, st);
+  return launch_k<T, DH, 8, false>(p, st);
 }
 
 bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh) {

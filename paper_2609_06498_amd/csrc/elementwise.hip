@@ -159,9 +159,9 @@ __global__ void qk_rope_kernel(RopeParams p) {
   const int KS = Dh / KT, DT = Dh / 16;
   if (!is_q && !is_k) {        // value head, fragment order (see kernels.h)
     T* vp = reinterpret_cast<T*>(p.vpool) + (size_t)layer * p.pool_stride + page_base;
-    const int kt = slot / 16, q = (slot % 16) / 4, r = slot % 4;
+    const int vg = slot / (4 * KL), q = (slot % 16) / 4, r = ((slot % (4 * KL)) / 16) * 4 + slot % 4;
     for (int e = i; e < Dh; e += blockDim.x)
-      vp[((size_t)(kt * DT + e / 16) * 64 + q * 16 + e % 16) * 4 + r] = src[e];
+      vp[((size_t)(vg * DT + e / 16) * 64 + q * 16 + e % 16) * KL + r] = src[e];
     return;
   }
   // key element d of this slot, fragment order (see kernels.h)

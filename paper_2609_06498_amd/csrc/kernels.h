@@ -52,8 +52,9 @@ namespace dflow {
 // 64 x Dh block of a page is stored in matrix-core fragment order:
 //   K element (key, d): ((kt*KS + ks)*64 + q*16 + key%16)*KL + d%KL
 //       with kt = key/16, ks = d/KT, q = (d%KT)/KL, KS = Dh/KT
-//   V element (key, d): ((kt*DT + dt)*64 + q*16 + d%16)*4 + key%4
-//       with kt = key/16, q = (key%16)/4, dt = d/16, DT = Dh/16
+//   V element (key, d): ((vg*DT + dt)*64 + q*16 + d%16)*KL + (key%(4 KL))/16*4 + key%4
+//       with vg = key/(4 KL), q = (key%16)/4, dt = d/16, DT = Dh/16
+//       (a lane fragment holds KL keys of one channel)
 // (KL, KT: 8, 32 for bf16 and 4, 16 for fp32.)
 struct AttnParams {
   int fused;                 // 1: QK-norm + RoPE + the block's KV write done here from qkv
