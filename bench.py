@@ -88,7 +88,8 @@ def gemm_bytes(rt, nseq):
     def g(N, K, out_elt=elt, n_out=None):
         return N * K * elt + M * K * elt + M * (N if n_out is None else n_out) * out_elt
 
-    layer = g(qkv, d) + g(d, qd) + g(2 * F, d, n_out=F) + g(d, F)
+    # the QKV projection writes its fp32 partial sums, one per K part
+    layer = g(qkv, d, 4 * rt.qkv_parts) + g(d, qd) + g(2 * F, d, n_out=F) + g(d, F)
     verify = dm.n_layers * layer + g(V, d, 0)
     draft = dm.n_draft_layers * layer + g(V, d, 0) + g(dm.d_h, 3 * d) + g(2 * d, dm.d_h, 4)
     accept = g(d, dm.m * d, 4)

@@ -186,6 +186,13 @@ size_t dflow_workspace_bytes(const dflow_dims* dims);
 int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache, dflow_ctx** out);
 int dflow_destroy(dflow_ctx* ctx);
 
+/* Number of K parts the context streams each QKV projection in (1 or 2):
+ * with two, the projection writes two fp32 partial sums that the attention
+ * (or QK-norm/RoPE) kernel adds.  Fixed at create from (d, q/kv widths) and
+ * the device's compute-unit count; for byte accounting.  Returns -1 on a
+ * null context. */
+int dflow_qkv_parts(const dflow_ctx* ctx);
+
 /* Prompt processing for sequence slot `seq` (set-up, not part of the round):
  * target KV for positions 0..len-1, fused features and drafter context K/V
  * for the same positions, and first_anchor[0] = the target's greedy token

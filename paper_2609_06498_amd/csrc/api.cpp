@@ -47,6 +47,7 @@ struct dflow_ctx {
   int mmax, rows_round;
   int G, nsplit, part_items;
   int lm_groups;
+  int qkv_ks;                // K parts of the QKV projection (fp32 partial sums, added by the consumers)
 
   dflow_weights w;
   std::vector<dflow_layer> layers, dlayers;
@@ -156,7 +157,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   auto add = [&](size_t bytes) { L.off[i++] = o; o += align256(bytes); };
   add((size_t)mmax * d->d * elt);                      // 0 x
   add((size_t)mmax * 3 * d->d * elt);                  // 1 xn (also relay u rows)
-  add((size_t)mmax * qkvn * elt);                      // 2 qkv
+  add((size_t)2 * mmax * qkvn * 4);                    // 2 qkv: up to two fp32 K parts
   add((size_t)mmax * qd * elt);                        // 3 q
   add((size_t)mmax * qd * elt);                        // 4 attn
   add((size_t)mmax * (d->ffn > d->relay_hidden ? d->ffn : d->relay_hidden) * elt);  // 5 act / relay hidden
@@ -222,6 +223,15 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->rows_round = dims->max_batch * dims->block;
   c->mmax = c->rows_round > dims->max_rows ? c->rows_round : dims->max_rows;
   c->G = dims->n_heads / dims->n_kv_heads;
+  {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                                hipSuccess) {
+      delete c;
+      return fail(DFLOW_EHIP, "create: no device attributes");
+    }
+    c->qkv_ks = gemm_ksplit(c->qkv_n / 16, dims->d / c->KT, cus);
+  }
   c->w = *w;
   c->layers.assign(w->layers, w->layers + dims->n_layers);
   c->dlayers.assign(w->draft_layers, w->draft_layers + dims->n_draft_layers);
@@ -312,8 +322,10 @@ struct NormIn {            // RMSNorm of the A rows: per-strip sums of squares; 
 hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, const void* W, int M, int N, int K,
                 void* Y, int ldy, const void* R = nullptr, int ldr = 0, void* Y2 = nullptr, int ldy2 = 0,
                 const void* bias = nullptr, float* logits = nullptr, int ldl = 0, NormIn nin = NormIn(),
-                float* ssq_out = nullptr) {
+                float* ssq_out = nullptr, int ksplit = 1) {
   GemmParams p{};
+  p.ksplit = ksplit;
+  p.y_part = (size_t)M * ldy;
   if (nin.ssq) {
     p.norm = 1;
     p.ssq = nin.ssq;
@@ -352,7 +364,8 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
     if ((e = hipEventRecord(c->ev1[c->n_ev], st)) != hipSuccess) return e;
     const double out_elt = (epi == EPI_ARGMAX) ? 0.0 : ((epi == EPI_STORE_F32 || epi == EPI_BIAS_F32) ? 4.0 : c->elt);
     const double n_out = (epi == EPI_SWIGLU) ? N / 2.0 : N;
-    c->ev_rec[c->n_ev] = {epi, N, K, M, (double)N * K * c->elt + (double)M * K * c->elt + (double)M * n_out * out_elt};
+    c->ev_rec[c->n_ev] = {epi, N, K, M,
+                          (double)N * K * c->elt + (double)M * K * c->elt + (double)M * n_out * out_elt * ksplit};
     ++c->n_ev;
   }
   return hipSuccess;
@@ -368,8 +381,10 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
   AttnParams a{};
   a.fused = fused ? 1 : 0;
   a.q = c->q;
-  a.qkv = c->qkv;
+  a.qkv = reinterpret_cast<const float*>(c->qkv);
   a.ld_qkv = c->qkv_n;
+  a.qkv_ks = c->qkv_ks;
+  a.qkv_part = (size_t)nseq * Bq * c->qkv_n;
   a.q_norm = L.q_norm;
   a.k_norm = L.k_norm;
   a.rope = c->rope;
@@ -404,12 +419,9 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
 }
 
 // QK-norm + RoPE + KV write for rows of `nseq` x Bq.
-hipError_t qk_rope(dflow_ctx* c, hipStream_t st, const dflow_layer& L, const void* qkv, int ld, int nseq, int Bq,
-                   int nq, const int* start_pos, const int* row_limit, const int* page_table, void* kpool,
-                   void* vpool) {
+RopeParams rope_params(dflow_ctx* c, const dflow_layer& L, int nseq, int Bq, int nq, const int* start_pos,
+                       const int* row_limit, const int* page_table, void* kpool, void* vpool) {
   RopeParams r{};
-  r.qkv = qkv;
-  r.ld = ld;
   r.M = nseq * Bq;
   r.Bq = Bq;
   r.nq = nq;
@@ -429,7 +441,7 @@ hipError_t qk_rope(dflow_ctx* c, hipStream_t st, const dflow_layer& L, const voi
   r.status = c->status;
   r.eps = c->dm.rms_eps;
   r.nlayers = 1;
-  return launch_qk_rope_write(c->bf, r, st);
+  return r;
 }
 
 // One Qwen3-style decoder layer over x (M = nseq*Bq rows) in place.
@@ -445,13 +457,19 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   NormIn attn_n, ffn_n;
   attn_n.ssq = c->ssq;
   ffn_n.ssq = c->ssq;
-  if ((e = gemm(c, st, EPI_STORE_T, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
-                nullptr, nullptr, 0, attn_n)))
+  // QKV projection as fp32 partial sums over qkv_ks K parts (spreads the
+  // weight stream evenly over the compute units); its consumers add them
+  if ((e = gemm(c, st, EPI_STORE_F32, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
+                nullptr, nullptr, 0, attn_n, nullptr, c->qkv_ks)))
     return e;
   const bool fused = attention_fuses_rope(c->bf, Bq, c->G, d.head_dim);
-  if (!fused &&
-      (e = qk_rope(c, st, L, c->qkv, c->qkv_n, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool)))
-    return e;
+  if (!fused) {
+    RopeParams r = rope_params(c, L, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool);
+    r.qkv32 = reinterpret_cast<const float*>(c->qkv);
+    r.ld = c->qkv_n;
+    r.part = c->qkv_ks == 2 ? (size_t)M * c->qkv_n : 0;
+    if ((e = launch_qk_rope_write(c->bf, r, st))) return e;
+  }
   if ((e = attention(c, st, L, nseq, Bq, start_pos, page_table, kpool, vpool, causal, fused))) return e;
   if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d, nullptr, 0,
                 nullptr, nullptr, 0, NormIn(), c->ssq)))
@@ -638,6 +656,8 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
   HIPCHK(launch_commit(accept_len, nseq, seq_len, st));
   return DFLOW_OK;
 }
+
+extern "C" int dflow_qkv_parts(const dflow_ctx* c) { return c ? c->qkv_ks : fail(DFLOW_EINVAL, "qkv_parts: null context"); }
 
 extern "C" int dflow_move_slot(dflow_ctx* c, hipStream_t st, int from, int to) {
   if (!c) return fail(DFLOW_EINVAL, "move_slot: null context");

@@ -100,7 +100,7 @@ __device__ inline int vfrag_off(int slot, int e) {
 //     combine kernel merges the splits in split order.
 // A row's arithmetic depends only on its own visible keys and the fixed split
 // boundaries, never on the batch it is part of.
-template <typename T, int DH, int NW, bool FUSED>
+template <typename T, int DH, int NW, bool FUSED, int NPART>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
   constexpr int KS = DH / KT;                 // k steps of S^T
@@ -121,6 +121,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int QI = FUSED ? (64 + NW * RPI - 1) / (NW * RPI) : 1;   // query passes per wave (R <= 64)
   constexpr int RC = CE * 8 / 16;             // 16-byte chunks of the lane's CE (cos, sin) pairs
   static_assert(CE == KL, "a key chunk is one fragment run of the paged layout");
+  constexpr int NQ = CE / 4;                  // 16-byte fp32 loads per chunk and projection part
   extern __shared__ __align__(16) unsigned char smem[];
   T* lk = reinterpret_cast<T*>(smem);         // [NPG][PG] keys, fragment order
   T* lv = lk + (size_t)NPG * PG;              // [NPG][PG] values, fragment order
@@ -153,31 +154,54 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   // Head rows (queries, block keys/values) are handled as 16-byte chunks: LPR
   // lanes per row, lane chunk cl holds channels [cl*CE, cl*CE + CE); its
   // rotate-half partner chunk sits LPR/2 lanes away and shares its RoPE angles.
-  const T* qkv = reinterpret_cast<const T*>(p.qkv);
+  // The projection rows arrive as NPART fp32 partial sums (K parts of the QKV
+  // projection) that are added here and rounded to the storage type.
+  const float* qkv = p.qkv;
   const int cl = lane % LPR, rl = lane / LPR;
   const int rc0 = (cl % (LPR / 2)) * CE;      // RoPE angle index of the chunk's first channel
-  u32x4_t qraw[QI], qrope[QI][RC];
+  u32x4_t qraw[QI][NPART][NQ], qrope[QI][RC];
   if constexpr (FUSED) {
 #pragma unroll
     for (int it = 0; it < QI; ++it) {
       const int rr = min((w + NW * it) * RPI + rl, R - 1);   // clamped rows are computed and not stored
       const int j = rr / G, g = rr - j * G;
-      qraw[it] = *(const gu4*)(qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH + cl * CE);
+      const float* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)(kvh * G + g) * DH + cl * CE;
+#pragma unroll
+      for (int k = 0; k < NPART; ++k)
+#pragma unroll
+        for (int c = 0; c < NQ; ++c) qraw[it][k][c] = *(const gu4*)(src + k * p.qkv_part + 4 * c);
       const gu4* rp = (const gu4*)(p.rope + (size_t)min(t0 + j, cap - 1) * HALF + rc0);   // past capacity: status set above
 #pragma unroll
       for (int c = 0; c < RC; ++c) qrope[it][c] = rp[c];
     }
   }
   const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SK - t0);   // block rows in this split
-  u32x4_t kraw, vraw, krope[RC];
+  u32x4_t kraw[NPART][NQ], vraw[NPART][NQ], krope[RC];
   auto load_rows = [&](int it) {
     const int j = max(0, min(jlo + (w + NW * it) * RPI + rl, jhi - 1));   // clamped rows are not stored
-    const T* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)p.Hq * DH + (size_t)kvh * DH + cl * CE;
-    kraw = *(const gu4*)src;
-    vraw = *(const gu4*)(src + (size_t)p.Hkv * DH);
+    const float* src = qkv + (size_t)(s * p.Bq + j) * p.ld_qkv + (size_t)p.Hq * DH + (size_t)kvh * DH + cl * CE;
+#pragma unroll
+    for (int k = 0; k < NPART; ++k)
+#pragma unroll
+      for (int c = 0; c < NQ; ++c) {
+        kraw[k][c] = *(const gu4*)(src + k * p.qkv_part + 4 * c);
+        vraw[k][c] = *(const gu4*)(src + (size_t)p.Hkv * DH + k * p.qkv_part + 4 * c);
+      }
     const gu4* rp = (const gu4*)(p.rope + (size_t)min(t0 + j, cap - 1) * HALF + rc0);
 #pragma unroll
     for (int c = 0; c < RC; ++c) krope[c] = rp[c];
+  };
+  // the lane's CE channels: sum of the parts, rounded to the storage type
+  auto combine = [&](const u32x4_t (&raw)[NPART][NQ], float (&x)[CE]) {
+#pragma unroll
+    for (int c = 0; c < NQ; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float v = __uint_as_float(raw[0][c][e]);
+#pragma unroll
+        for (int k = 1; k < NPART; ++k) v += __uint_as_float(raw[k][c][e]);
+        x[4 * c + e] = TT<T>::rnd(v);
+      }
   };
   u32x4_t gq, gk;                             // QK-norm gains of the lane's chunk
   if constexpr (FUSED) {
@@ -216,9 +240,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 
   // ---- 2. query tile; block rows to the cache and the row tile
   // RMSNorm over the row's LPR lanes, gain, then RoPE against the partner chunk
-  auto norm_rope = [&](const u32x4_t& raw, const u32x4_t& gain, const u32x4_t (&rope)[RC], u32x4_t& out) {
-    float x[CE], g[CE], y[CE], cs[2 * CE];
-    Chunk<T>::unpack(raw, x);
+  auto norm_rope = [&](float (&x)[CE], const u32x4_t& gain, const u32x4_t (&rope)[RC], u32x4_t& out) {
+    float g[CE], y[CE], cs[2 * CE];
     Chunk<T>::unpack(gain, g);
 #pragma unroll
     for (int c = 0; c < RC; ++c)
@@ -245,19 +268,25 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     for (int it = 0; it < QI; ++it) {
       const int rr = (w + NW * it) * RPI + rl;
       u32x4_t y;
-      norm_rope(qraw[it], gq, qrope[it], y);
+      float x[CE];
+      combine(qraw[it], x);
+      norm_rope(x, gq, qrope[it], y);
       if (rr < R) *reinterpret_cast<u32x4_t*>(lq + (size_t)rr * QLD + cl * CE) = y;
     }
     for (int it = 0; jlo + (w + NW * it) * RPI < jhi; ++it) {   // uniform per wave
       if (it > 0) load_rows(it);
-      u32x4_t y;
-      norm_rope(kraw, gk, krope, y);
+      u32x4_t y, vchunk;
+      float x[CE];
+      combine(kraw, x);
+      norm_rope(x, gk, krope, y);
+      combine(vraw, x);
+      vchunk = Chunk<T>::pack(x);
       const int j = jlo + (w + NW * it) * RPI + rl;
       const int pos = t0 + j;
       if (j >= jhi) continue;
       T* row = ln + (size_t)(j - jlo) * 2 * DH;
       *reinterpret_cast<u32x4_t*>(row + cl * CE) = y;
-      *reinterpret_cast<u32x4_t*>(row + DH + cl * CE) = vraw;
+      *reinterpret_cast<u32x4_t*>(row + DH + cl * CE) = vchunk;
       if (pos >= cap) continue;                // status set above
       const int pi = (pos - key0) / PAGE, slot = pos % PAGE;
       if (!((present >> pi) & 1u)) continue;   // status set above
@@ -268,7 +297,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       T* vt_g = reinterpret_cast<T*>(p.vpool) + ((size_t)gp * p.Hkv + kvh) * PG;
       *reinterpret_cast<u32x4_t*>(kt_g + kfrag_off<T, DH>(slot, cl * CE)) = y;   // CE = KL consecutive channels
 #pragma unroll
-      for (int i = 0; i < CE; ++i) vt_g[vfrag_off<T, DH>(slot, cl * CE + i)] = Chunk<T>::elem(vraw, i);
+      for (int i = 0; i < CE; ++i) vt_g[vfrag_off<T, DH>(slot, cl * CE + i)] = Chunk<T>::elem(vchunk, i);
     }
   }
 
@@ -480,18 +509,18 @@ static bool fuses_dh(int Bq, int G) {
   return Bq * G <= 64 && attn_lds<T, DH>(true, Bq, G) <= ATTN_LDS_MAX;
 }
 
-template <typename T, int DH, int NW, bool FUSED>
+template <typename T, int DH, int NW, bool FUSED, int NPART>
 static hipError_t launch_k(const AttnParams& p, hipStream_t st) {
   const size_t lds = attn_lds<T, DH>(FUSED, p.Bq, p.Hq / p.Hkv);
   if (lds > ATTN_LDS_MAX) return hipErrorInvalidConfiguration;
   static bool lds_set = false;   // allow the largest dynamic LDS once per instantiation
   if (!lds_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATTN_LDS_MAX);
     if (e != hipSuccess) return e;
     lds_set = true;
   }
-  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64), lds, st, p);
+  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((attn_combine_kernel<T, DH>), dim3(p.nseq * p.Bq, p.Hq), dim3(DH), 0, st, p);
@@ -502,11 +531,13 @@ template <typename T, int DH>
 static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
   if (p.fused) {
     if (!fuses_dh<T, DH>(p.Bq, p.Hq / p.Hkv)) return hipErrorInvalidConfiguration;
-    return launch_k<T, DH, 4, true>(p, st);
+    if (p.qkv_ks == 2) return launch_k<T, DH, 4, true, 2>(p, st);
+    if (p.qkv_ks == 1) return launch_k<T, DH, 4, true, 1>(p, st);
+    return hipErrorInvalidValue;
   }
   // one wave per 16-row group up to eight; beyond, waves take several groups
-  if (p.Bq * (p.Hq / p.Hkv) <= 64) return launch_k<T, DH, 4, false>(p, st);
-  return launch_k<T, DH, 8, false>(p, st);
+  if (p.Bq * (p.Hq / p.Hkv) <= 64) return launch_k<T, DH, 4, false, 1>(p, st);
+  return launch_k<T, DH, 8, false, 1>(p, st);
 }
 
 bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh) {

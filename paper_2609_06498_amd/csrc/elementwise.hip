@@ -134,7 +134,14 @@ __global__ void qk_rope_kernel(RopeParams p) {
   const int Dh = p.Dh, half = Dh / 2;
   const int pos = p.start_pos[s] + j;
   const int layer = blockIdx.z;
-  const T* src = reinterpret_cast<const T*>(p.qkv) + (size_t)row * p.ld + (size_t)layer * p.layer_cols + (size_t)h * Dh;
+  const size_t off = (size_t)row * p.ld + (size_t)layer * p.layer_cols + (size_t)h * Dh;
+  const T* src = reinterpret_cast<const T*>(p.qkv) + off;
+  const float* src32 = p.qkv32 ? p.qkv32 + off : nullptr;
+  // element e of the head row as a storage-type value (fp32 parts: sum, rounded)
+  auto val = [&](int e) -> float {
+    if (!src32) return TT<T>::ld(src, e);
+    return TT<T>::rnd(p.part ? src32[e] + src32[p.part + e] : src32[e]);
+  };
   const bool is_q = h < p.nq;
   const bool is_k = !is_q && h < p.nq + p.Hkv;
   const int kvh = is_q ? 0 : (is_k ? h - p.nq : h - p.nq - p.Hkv);
@@ -161,7 +168,7 @@ __global__ void qk_rope_kernel(RopeParams p) {
     T* vp = reinterpret_cast<T*>(p.vpool) + (size_t)layer * p.pool_stride + page_base;
     const int vg = slot / (4 * KL), q = (slot % 16) / 4, r = ((slot % (4 * KL)) / 16) * 4 + slot % 4;
     for (int e = i; e < Dh; e += blockDim.x)
-      vp[((size_t)(vg * DT + e / 16) * 64 + q * 16 + e % 16) * KL + r] = src[e];
+      TT<T>::st(vp, ((size_t)(vg * DT + e / 16) * 64 + q * 16 + e % 16) * KL + r, val(e));
     return;
   }
   // key element d of this slot, fragment order (see kernels.h)
@@ -170,7 +177,7 @@ __global__ void qk_rope_kernel(RopeParams p) {
   };
   const T* gain = reinterpret_cast<const T*>(is_q ? p.q_norm : (p.k_norms ? p.k_norms[layer] : p.k_norm));
   float x1 = 0.f, x2 = 0.f;
-  if (i < half) { x1 = TT<T>::ld(src, i); x2 = TT<T>::ld(src, i + half); }
+  if (i < half) { x1 = val(i); x2 = val(i + half); }
   const float ss = wave_sum(x1 * x1 + x2 * x2);
   const float r = rsqrtf(ss / (float)Dh + p.eps);
   if (i < half) {

@@ -8,6 +8,8 @@
 // ranges that depend only on (N, K), and the wave partials are summed in LDS
 // in wave order.  Every output element therefore sees the same reduction
 // order whatever M is, which keeps results batch- and position-invariant.
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -24,12 +26,16 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   // wave index as a scalar: keeps the k-range bounds and the pipeline control uniform
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nw = blockDim.x >> 6;
-  const int g = blockIdx.x;
+  // workgroup (strip group g, K part h): the K parts of a group sit on adjacent workgroups
+  const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  const int g = blockIdx.x / ks, h = blockIdx.x - g * ks;
   const int nt0 = g * NG;
   const int nvalid = min(NG, p.ntiles - nt0);
-  const int kper = (p.ktiles + nw - 1) / nw;
-  const int kb = min(p.ktiles, w * kper);
-  const int ke = min(p.ktiles, kb + kper);
+  const int kpart = (p.ktiles + ks - 1) / ks;
+  const int k0 = min(p.ktiles, h * kpart), k1 = min(p.ktiles, k0 + kpart);
+  const int kper = (k1 - k0 + nw - 1) / nw;
+  const int kb = min(k1, k0 + w * kper);
+  const int ke = min(k1, kb + kper);
   const int M = p.M;
   const int mtiles = (M + 15) >> 4;
 
@@ -247,7 +253,7 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
       if constexpr (EPI == EPI_STORE_T) {
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
       } else if constexpr (EPI == EPI_STORE_F32) {
-        reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
+        reinterpret_cast<float*>(p.Y)[(size_t)h * p.y_part + (size_t)m * p.ldy + col] = v;
       } else if constexpr (EPI == EPI_RESID) {
         v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col));
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
@@ -279,21 +285,36 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   }
 }
 
-// Launch shape from (N, K) only, never from M.  Wide weights (>= 1024
+// Launch shape from (N, K) (and the K parts) only, never from M.  Wide weights (>= 1024
 // strips) and the LM head take two 16-column strips per workgroup (the A
 // fragments are reused across both); narrower ones take one so that enough
 // workgroups exist.  The wave count (the K split) is the smallest power of
 // two in 2..8 that puts at least 1024 waves in flight while leaving each wave
 // at least 8 k tiles.  Chosen from a sweep over the 8B-shape projections at
 // M = 16 with weights streamed from HBM.
-GemmShape gemm_shape(int ntiles, int ktiles, int epi) {
+GemmShape gemm_shape(int ntiles, int ktiles, int epi, int ksplit) {
   GemmShape s;
   s.ng = (epi == EPI_ARGMAX || ntiles >= 1024) ? 2 : 1;
-  s.groups = (ntiles + s.ng - 1) / s.ng;
+  s.groups = (ntiles + s.ng - 1) / s.ng * ksplit;   // workgroups: strip groups x K parts
+  const int kpart = (ktiles + ksplit - 1) / ksplit;
   int waves = 2;
-  while (waves < 8 && (long long)s.groups * waves < 1024 && ktiles / (2 * waves) >= 8) waves *= 2;
+  while (waves < 8 && (long long)s.groups * waves < 1024 && kpart / (2 * waves) >= 8) waves *= 2;
   s.waves = waves;
   return s;
+}
+
+// K parts for a projection whose consumer adds fp32 partial outputs: two when
+// that spreads the strip groups more evenly over the compute units (every
+// unit streams weights at about the same rate, so the slowest unit sets the
+// time), one otherwise.  Depends only on (N, K) and the device.
+int gemm_ksplit(int ntiles, int ktiles, int cus) {
+  const GemmShape s = gemm_shape(ntiles, ktiles, EPI_STORE_F32, 1);
+  if (cus < 1 || ktiles < 8) return 1;
+  auto imbalance = [&](int ks) {
+    const double per = (double)s.groups * ks / cus;
+    return std::ceil(per) / per;
+  };
+  return imbalance(2) < imbalance(1) - 1e-9 ? 2 : 1;
 }
 
 template <typename T, int NG, int EPI, bool NORM>
@@ -314,7 +335,9 @@ static hipError_t launch_mtn(const GemmParams& p, const GemmShape& sh, hipStream
 }
 
 // The RMSNorm row scale is instantiated only for the projections that follow a norm.
-template <int EPI> struct HasNorm { static constexpr bool value = EPI == EPI_STORE_T || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX; };
+template <int EPI> struct HasNorm {
+  static constexpr bool value = EPI == EPI_STORE_T || EPI == EPI_STORE_F32 || EPI == EPI_SWIGLU || EPI == EPI_ARGMAX;
+};
 
 template <typename T, int NG, int EPI>
 static hipError_t launch_mt(const GemmParams& p, const GemmShape& sh, hipStream_t st) {
@@ -333,7 +356,9 @@ static hipError_t launch_ng(const GemmParams& p, const GemmShape& sh, hipStream_
 
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
-  const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi);
+  const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  if (ks > 1 && epi != EPI_STORE_F32) return hipErrorInvalidValue;   // only partial fp32 outputs are split
+  const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi, ks);
   switch (epi) {
     case EPI_STORE_T: return launch_ng<T, EPI_STORE_T>(p, sh, st);
     case EPI_STORE_F32: return launch_ng<T, EPI_STORE_F32>(p, sh, st);

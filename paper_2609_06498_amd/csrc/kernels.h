@@ -36,10 +36,14 @@ struct GemmParams {
   float eps;
   // EPI_RESID: per-16-column-strip sums of squares of the stored rows, [m * ssq_out_ld + strip]
   float* ssq_out; int ssq_out_ld;
+  // EPI_STORE_F32 only: K split into ksplit parts; part h writes its partial
+  // sums at Y + h * y_part (floats), and the consumer adds the parts
+  int ksplit; size_t y_part;
 };
 
 struct GemmShape { int ng; int waves; int groups; };
-GemmShape gemm_shape(int ntiles, int ktiles, int epi);
+GemmShape gemm_shape(int ntiles, int ktiles, int epi, int ksplit = 1);
+int gemm_ksplit(int ntiles, int ktiles, int cus);
 hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
 hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
                        hipStream_t s);
@@ -59,7 +63,9 @@ namespace dflow {
 struct AttnParams {
   int fused;                 // 1: QK-norm + RoPE + the block's KV write done here from qkv
   const void* q;             // fused = 0: [nseq*Bq, Hq*Dh] queries after QK-norm + RoPE
-  const void* qkv; int ld_qkv;   // fused = 1: raw projection rows [q heads | k heads | v heads] x Dh
+  // fused = 1: raw projection rows [q heads | k heads | v heads] x Dh as qkv_ks
+  // fp32 partial sums (K parts) qkv_part floats apart, added by the kernel
+  const float* qkv; int ld_qkv; int qkv_ks; size_t qkv_part;
   const void* q_norm;        // [Dh] QK-norm gains
   const void* k_norm;        // [Dh]
   const float2* rope;        // [max_pages*64][Dh/2] (cos, sin)
@@ -89,6 +95,9 @@ namespace dflow {
 
 struct RopeParams {
   const void* qkv; int ld;        // rows: [q heads (nq)][k heads][v heads] x Dh, storage type
+  // or, when qkv32 is set, the same rows as fp32 partial sums: part k at
+  // qkv32 + k * part (parts = 2 when part > 0), added and rounded here
+  const float* qkv32; size_t part;
   int M, Bq;                      // rows, rows per sequence
   int nq, Hkv, Dh;                // nq = query heads present (0 for context rows)
   const void* q_norm;             // [Dh]

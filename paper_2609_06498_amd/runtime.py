@@ -78,6 +78,7 @@ EXPORTS = {
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p]),
     "kv_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_qkv_parts": (ctypes.c_int, [ctypes.c_void_p]),
     "dflow_move_slot": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]),
     "dflow_bench_force_drafts": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                 ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -262,6 +263,11 @@ class Runtime:
 
     def kv_commit(self, nseq, accept_len, seq_len):
         self._check(self.lib.kv_commit(self.ctx, _stream(), nseq, _ptr(accept_len), _ptr(seq_len)), "kv_commit")
+
+    @property
+    def qkv_parts(self) -> int:
+        """K parts of the QKV projection (fp32 partial sums added by its consumers)."""
+        return int(self.lib.dflow_qkv_parts(self.ctx))
 
     def move_slot(self, src: int, dst: int):
         self._check(self.lib.dflow_move_slot(self.ctx, _stream(), int(src), int(dst)), "dflow_move_slot")

@@ -54,6 +54,7 @@ def test_validation_errors_without_device(lib):
     assert lib.dflow_pack_linear(None, 1, ctypes.c_void_p(16), 16, 48, 0, None, ctypes.c_void_p(16)) == -2
     assert lib.dflow_create(None, None, None, None) == -1
     assert lib.dflow_move_slot(None, None, 0, 1) == -1
+    assert lib.dflow_qkv_parts(None) == -1
     assert lib.dflow_packed_bytes(1, 32, 64) == 32 * 64 * 2
     assert lib.dflow_packed_bytes(0, 32, 64) == 32 * 64 * 4
 
