@@ -113,8 +113,8 @@ typedef struct dflow_dims {
   int capture_layers[16]; /* 0-based target layer indices, increasing */
   int relay_hidden;       /* MLP_phi hidden width */
   int block;              /* B = anchor + K drafted tokens */
-  int max_batch;          /* sequences per call */
-  int max_rows;           /* rows per prefill chunk (>= block) */
+  int max_batch;          /* sequences per call; max_batch * block <= 1024 */
+  int max_rows;           /* rows per prefill chunk (block..1024) */
   int max_pages;          /* page-table row length per sequence */
   int num_pages;          /* pages in each layer pool */
   int carry_window;       /* DFLOW_CARRY_* */

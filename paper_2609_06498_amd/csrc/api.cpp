@@ -79,6 +79,8 @@ struct dflow_ctx {
 static const char* kClassName[] = {"gemm.store", "gemm.store_f32", "gemm.resid", "gemm.swiglu",
                                    "gemm.bias_silu", "gemm.bias_f32", "gemm.argmax", "attention"};
 static constexpr int CLS_ATTN = 7;
+// rows of one call (b x B per round, a prefill chunk); up to 128 the weight-streaming GEMM, beyond the tiled one
+static constexpr int MAX_ROWS = 1024;
 
 static constexpr int PROF_MAX = 16384;
 
@@ -123,9 +125,10 @@ int validate(const dflow_dims* d) {
       return fail(DFLOW_ESHAPE, "capture_layers must be increasing layer indices");
   }
   if (d->block < 2 || d->block > 64) return fail(DFLOW_ESHAPE, "block %d (2..64)", d->block);
-  if (d->max_batch < 1 || d->max_batch * d->block > 128)
-    return fail(DFLOW_ECAPACITY, "max_batch*block = %d exceeds 128 rows", d->max_batch * d->block);
-  if (d->max_rows < d->block || d->max_rows > 128) return fail(DFLOW_ECAPACITY, "max_rows %d (block..128)", d->max_rows);
+  if (d->max_batch < 1 || d->max_batch * d->block > MAX_ROWS)
+    return fail(DFLOW_ECAPACITY, "max_batch*block = %d exceeds %d rows", d->max_batch * d->block, MAX_ROWS);
+  if (d->max_rows < d->block || d->max_rows > MAX_ROWS)
+    return fail(DFLOW_ECAPACITY, "max_rows %d (block..%d)", d->max_rows, MAX_ROWS);
   if (d->max_pages < 1 || d->num_pages < 1) return fail(DFLOW_ECAPACITY, "page counts");
   if (d->carry_window != DFLOW_CARRY_SUFFIX && d->carry_window != DFLOW_CARRY_SUFFIX_TAIL)
     return fail(DFLOW_EINVAL, "carry_window %d", d->carry_window);

@@ -285,6 +285,249 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   }
 }
 
+// ------------------------------------------------------------------ large M
+// Tiled GEMM for M > 128 rows (serving batches, prefill chunks): workgroup
+// tile of 128 rows x 8 strips (128 columns), four waves of 64 rows x 4
+// strips, A and W staged through LDS in MFMA fragment order, double
+// buffered.  The K loop runs the same contiguous ranges as the weight-
+// streaming kernel's waves (gemm_shape's wave count for this N, K) and folds
+// each range's MFMA chain into the running sum in range order, starting from
+// zero, so every output element is bit-identical to what the weight-streaming
+// kernel computes for it at any M: the result of a row never depends on the
+// batch it is part of.  The M tiles of one strip tile are dispatched to the
+// same XCD (round-robin placement, id mod 8), so its weights are fetched from
+// HBM once and shared through that XCD's L2.
+// Same row scale as the weight-streaming kernel: lane q of a 16-lane group
+// sums strips c = q (mod 16) in increasing c, then the fixed butterfly.
+__device__ inline float norm_row_scale(const GemmParams& p, int m, int q16) {
+  constexpr int EL = 16;
+  const int np = p.ssq_parts;
+  gf32* r = (gf32*)(p.ssq) + (size_t)m * p.ssq_ld + q16;
+  float v[EL];
+#pragma unroll
+  for (int it = 0; it < EL; ++it) v[it] = r[16 * it];   // padded rows: ssq_ld >= 256 entries
+  float sa = 0.f;
+#pragma unroll
+  for (int it = 0; it < EL; ++it) sa += (q16 + 16 * it < np) ? v[it] : 0.f;
+  for (int c = q16 + 16 * EL; c < np; c += 16) sa += p.ssq[(size_t)m * p.ssq_ld + c];
+#pragma unroll
+  for (int x = 8; x >= 1; x >>= 1) sa += __shfl_xor(sa, x, 16);
+  return rsqrtf(sa / (float)(np * 16) + p.eps);
+}
+
+constexpr int TILE_BM = 128, TILE_BS = 8, TILE_CW = TILE_BS * 16 + 4;
+constexpr size_t TILE_LDS = (size_t)TILE_BM * TILE_CW * sizeof(float);   // >= 2 stages x 16 KB
+
+template <typename T, int EPI, bool NORM>
+__global__ void __launch_bounds__(256) gemm_tile_kernel(GemmParams p, int nw, int mt, int units) {
+  constexpr int KL = TT<T>::KL;
+  constexpr int KT = TT<T>::KT;
+  extern __shared__ float lds[];
+  __shared__ float s_rs[NORM ? TILE_BM : 1];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  // block -> (m tile, unit = strip tile x K part); the m tiles of a unit share an XCD
+  const int x8 = blockIdx.x & 7, y = blockIdx.x >> 3;
+  const int mtile = y % mt, unit = (y / mt) * 8 + x8;
+  if (unit >= units) return;                                  // padding of the dispatch grid
+  const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  const int stile = unit / ks, h = unit - stile * ks;
+  const int nt0 = stile * TILE_BS;
+  const int nvalid = min(TILE_BS, p.ntiles - nt0);
+  const int m0 = mtile * TILE_BM;
+  const int rows = min(TILE_BM, p.M - m0);
+  const int kpart = (p.ktiles + ks - 1) / ks;
+  const int k0 = min(p.ktiles, h * kpart), k1 = min(p.ktiles, k0 + kpart);
+  const int kper = (k1 - k0 + nw - 1) / nw;                  // the weight-streaming kernel's wave ranges
+  const T* Ap = reinterpret_cast<const T*>(p.A);
+  const gu4* Wp = (const gu4*)(p.W);
+
+  if constexpr (NORM) {
+    const int q16 = threadIdx.x & 15, grp = threadIdx.x >> 4;   // 16 groups of 16 lanes
+    for (int r = grp; r < TILE_BM; r += 16) {
+      const float rs = norm_row_scale(p, m0 + min(r, rows - 1), q16);
+      if (q16 == 0) s_rs[r] = rs;
+    }
+  }
+
+  // staging: 512 16-byte A chunks (row r, quarter q of its KT values) and 512
+  // W chunks (strip s, lane l) per k tile, two of each per thread
+  u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [stage][8 m tiles][64]
+  u32x4_t* sw = sa + 2 * 512;                                 // [stage][8 strips][64]
+  const gu4* asrc[2];
+  int adst[2], wst[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    const int r = c >> 2, q = c & 3;
+    asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
+    adst[i] = (r >> 4) * 64 + q * 16 + (r & 15);
+    wst[i] = min(nt0 + (c >> 6), p.ntiles - 1) * p.ktiles;   // clamped strips are not stored
+  }
+  constexpr int AST = KT * (int)sizeof(T) / 16;              // 16-byte chunks per k tile along an A row
+  u32x4_t ra[2], rw[2];
+  auto load = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      ra[i] = asrc[i][(size_t)kt * AST];
+      rw[i] = Wp[((size_t)wst[i] + kt) * 64 + ((threadIdx.x + 256 * i) & 63)];
+    }
+  };
+  auto store = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      sa[st * 512 + adst[i]] = ra[i];
+      sw[st * 512 + threadIdx.x + 256 * i] = rw[i];
+    }
+  };
+
+  f32x4_t acc[4][4], tot[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  int folds = 0;
+  auto fold = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) tot[i][j][r] += acc[i][j][r];
+        acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+    ++folds;
+  };
+
+  if (k0 < k1) {
+    load(k0);
+    store(0);
+  }
+  __syncthreads();
+  for (int kt = k0; kt < k1; ++kt) {                          // uniform
+    const int cur = (kt - k0) & 1;
+    if (kt + 1 < k1) load(kt + 1);
+    u32x4_t a[4], b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) a[i] = sa[cur * 512 + (wm * 4 + i) * 64 + lane];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) b[j] = sw[cur * 512 + (wn * 4 + j) * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = mma_frag(T(), a[i], b[j], acc[i][j]);
+    if ((kt - k0 + 1) % kper == 0 || kt + 1 == k1) fold();   // end of a range
+    if (kt + 1 < k1) store(cur ^ 1);
+    __syncthreads();
+  }
+  while (folds < nw) fold();                                  // empty ranges add +0, as their waves do
+
+  // C tile to LDS (the staging buffers are free), then the epilogue
+  float* ct = lds;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        ct[(wm * 64 + i * 16 + 4 * (lane >> 4) + r) * TILE_CW + (wn * 4 + j) * 16 + (lane & 15)] = tot[i][j][r];
+  __syncthreads();
+  const int ncols = nvalid * 16;
+  const int colbase = p.col0 + nt0 * 16;
+  if constexpr (EPI == EPI_ARGMAX) {
+    for (int e = threadIdx.x; e < rows * ncols; e += blockDim.x) {
+      const int m = e / ncols, n = e - m * ncols;
+      float v = ct[m * TILE_CW + n];
+      if constexpr (NORM) ct[m * TILE_CW + n] = v = v * s_rs[m];
+      if (p.logits) p.logits[(size_t)(m0 + m) * p.ldl + colbase + n] = v;
+    }
+    __syncthreads();
+    // one key per row and group of two strips, as the weight-streaming kernel's workgroups
+    const int ngrp = (nvalid + 1) / 2;
+    for (int e = threadIdx.x; e < rows * ngrp; e += blockDim.x) {
+      const int m = e / ngrp, gi = e - m * ngrp;
+      const int c0 = gi * 32, c1 = min(ncols, c0 + 32);
+      float best = ct[m * TILE_CW + c0];
+      int bi = c0;
+      for (int n = c0 + 1; n < c1; ++n) {
+        const float v = ct[m * TILE_CW + n];
+        if (v > best) { best = v; bi = n; }
+      }
+      p.amax[(size_t)(nt0 / 2 + gi) * p.amax_ld + m0 + m] = argmax_key(best, colbase + bi);
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    const int half = ncols / 2;
+    const int obase = (p.col0 + nt0 * 16) / 2;
+    for (int e = threadIdx.x; e < rows * half; e += blockDim.x) {
+      const int m = e / half, c = e - m * half;
+      const int strip = c >> 3, cc = c & 7;
+      float gt = ct[m * TILE_CW + strip * 16 + cc];
+      float up = ct[m * TILE_CW + strip * 16 + 8 + cc];
+      if constexpr (NORM) {
+        gt *= s_rs[m];
+        up *= s_rs[m];
+      }
+      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)(m0 + m) * p.ldy + obase + c, silu(gt) * up);
+    }
+  } else {
+    for (int e = threadIdx.x; e < rows * ncols; e += blockDim.x) {
+      const int m = e / ncols, n = e - m * ncols;
+      const int col = colbase + n;
+      const size_t gm = (size_t)(m0 + m);
+      float v = ct[m * TILE_CW + n];
+      if constexpr (NORM) v *= s_rs[m];
+      if constexpr (EPI == EPI_STORE_T) {
+        TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, v);
+      } else if constexpr (EPI == EPI_STORE_F32) {
+        reinterpret_cast<float*>(p.Y)[(size_t)h * p.y_part + gm * p.ldy + col] = v;
+      } else if constexpr (EPI == EPI_RESID) {
+        v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), gm * p.ldr + col));
+        TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, v);
+        if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), gm * p.ldy2 + col, v);
+        ct[m * TILE_CW + n] = v;
+      } else if constexpr (EPI == EPI_BIAS_SILU) {
+        v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+        TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, silu(v));
+      } else if constexpr (EPI == EPI_BIAS_F32) {
+        v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+        reinterpret_cast<float*>(p.Y)[gm * p.ldy + col] = v;
+      }
+    }
+    if constexpr (EPI == EPI_RESID) {
+      if (p.ssq_out) {
+        __syncthreads();
+        for (int e = threadIdx.x; e < rows * nvalid; e += blockDim.x) {
+          const int m = e / nvalid, j = e - m * nvalid;
+          float sq = 0.f;
+#pragma unroll
+          for (int c = 0; c < 16; ++c) {
+            const float v = ct[m * TILE_CW + j * 16 + c];
+            sq += v * v;
+          }
+          p.ssq_out[(size_t)(m0 + m) * p.ssq_out_ld + nt0 + j] = sq;
+        }
+      }
+    }
+  }
+}
+
+template <typename T, int EPI, bool NORM>
+static hipError_t launch_tile(const GemmParams& p, const GemmShape& sh, int ks, hipStream_t st) {
+  const int mt = (p.M + TILE_BM - 1) / TILE_BM;
+  const int units = (p.ntiles + TILE_BS - 1) / TILE_BS * ks;
+  const int blocks = (units + 7) / 8 * 8 * mt;
+  static bool lds_set = false;   // the C tile needs more than the default dynamic LDS
+  if (!lds_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_tile_kernel<T, EPI, NORM>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)TILE_LDS);
+    if (e != hipSuccess) return e;
+    lds_set = true;
+  }
+  hipLaunchKernelGGL((gemm_tile_kernel<T, EPI, NORM>), dim3(blocks), dim3(256), TILE_LDS, st, p, sh.waves, mt, units);
+  return hipGetLastError();
+}
+
 // Launch shape from (N, K) (and the K parts) only, never from M.  Wide weights (>= 1024
 // strips) and the LM head take two 16-column strips per workgroup (the A
 // fragments are reused across both); narrower ones take one so that enough
@@ -331,7 +574,7 @@ static hipError_t launch_mtn(const GemmParams& p, const GemmShape& sh, hipStream
   if (mt <= 2) return go(gemm_kernel<T, NG, 2, EPI, NORM>, 2);
   if (mt <= 4) return go(gemm_kernel<T, NG, 4, EPI, NORM>, 4);
   if (mt <= 8) return go(gemm_kernel<T, NG, 8, EPI, NORM>, 8);
-  return hipErrorInvalidValue;
+  return launch_tile<T, EPI, NORM>(p, sh, p.ksplit > 1 ? p.ksplit : 1, st);
 }
 
 // The RMSNorm row scale is instantiated only for the projections that follow a norm.

@@ -3,7 +3,9 @@
 * qwen3-8b-b8: the Qwen3-8B shape with 8 sequences of ragged contexts
   (2048..8192 positions), M = 128 verify rows;
 * qwen3-32b: the Qwen3-32B shape (64 + 5 layers, d 5120, GQA group 8),
-  4 sequences of 16384 positions.
+  4 sequences of 16384 positions;
+* small-bf16-b24: 24 sequences, M = 384 rows, so the batched run takes the
+  tiled GEMM and each sequence alone the weight-streaming one.
 
 Batch invariance: every kernel's arithmetic for a row depends only on that
 row's own data (K reductions split by (N, K) only, attention splits at fixed
@@ -27,7 +29,8 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name, rounds, alone", [("qwen3-8b-b8", 3, "extremes"), ("qwen3-32b", 2, "extremes")])
+@pytest.mark.parametrize("name, rounds, alone", [("qwen3-8b-b8", 3, "extremes"), ("qwen3-32b", 2, "extremes"),
+                                                 ("small-bf16-b24", 3, "all")])
 def test_batch_invariance(name, rounds, alone):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")

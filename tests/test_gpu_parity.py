@@ -19,7 +19,7 @@ from workload.synth import make_prompts, make_schedule, make_weights, trajectory
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-CASES = ["tiny-f32", "small-f32", "small-bf16"]
+CASES = ["tiny-f32", "small-f32", "small-bf16", "tiny-f32-b20"]
 
 
 @pytest.fixture(scope="module")

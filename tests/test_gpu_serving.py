@@ -112,3 +112,29 @@ def test_serving_concurrency_invariant(lib, force):
     assert stats["max_active"] == SLOTS
     for i, (a, b) in enumerate(zip(one, many)):
         assert a == b, f"request {i}: outputs differ at concurrency 1 and {SLOTS}"
+
+
+def test_serving_many_slots_invariant(lib):
+    """30 requests through 24 slots (up to 384 rows per round, the tiled
+    GEMM) give the same tokens as through one slot (16 rows)."""
+    from paper_2609_06498_amd import Runtime
+    from paper_2609_06498_amd.engine import Engine
+    wl = get_config("small-bf16")
+    w = make_weights(wl.dims, wl.seed_w)
+    r = np.random.default_rng([wl.seed_prompt, 91])
+    prompts = [r.integers(0, wl.dims.vocab, size=int(r.integers(20, 200))).astype(np.int32) for _ in range(30)]
+    budgets = [int(x) for x in r.integers(1, 24, size=30)]
+    print(f"[serving] small-bf16 30 requests, 24 slots vs 1", flush=True)
+    rt = Runtime(wl.dims, wl.block, 24, 200 + 24 + 2 * wl.block, w, wl.carry_window)
+    outs = {}
+    for slots in (24, 1):
+        eng = Engine(rt, max_active=slots)
+        rids = [eng.submit(p, n) for p, n in zip(prompts, budgets)]
+        res = eng.run()
+        torch.cuda.synchronize()
+        assert rt.status() == 0
+        assert max(eng.active_hist) == slots
+        outs[slots] = [res[i] for i in rids]
+    rt.close()
+    for i, (a, b) in enumerate(zip(outs[1], outs[24])):
+        assert a == b, f"request {i}: outputs differ with 1 and 24 slots"

@@ -96,6 +96,9 @@ CONFIGS = {
     "qwen3-8b-b8": Workload("qwen3-8b-b8", _QWEN3_8B, block=16, batch=8, ctx=(2048, 8192), rounds=128,
                             schedule="geometric", sched_param=6.0,
                             description="Qwen3-8B shape bf16, b=8 ragged ctx in [2048, 8192], B=16"),
+    "qwen3-8b-b32": Workload("qwen3-8b-b32", _QWEN3_8B, block=16, batch=32, ctx=(1024, 2048), rounds=64,
+                             schedule="geometric", sched_param=6.0,
+                             description="Qwen3-8B shape bf16, b=32 ragged ctx in [1024, 2048], B=16: 512 rows per round"),
     "qwen3-32b": Workload("qwen3-32b", _QWEN3_32B, block=16, batch=4, ctx=(16384, 16384), rounds=64,
                           schedule="geometric", sched_param=6.0,
                           description="Qwen3-32B shape bf16, b=4, ctx 16384, B=16"),
@@ -107,6 +110,17 @@ CONFIGS = {
                            block=16, batch=3, ctx=(40, 520), rounds=6,
                            schedule="geometric", sched_param=4.0,
                            description="3-layer d=512 bf16, V=5008, b=3 ragged ctx, B=16"),
+    # more rows than the weight-streaming GEMM takes (M = b * B > 128): the
+    # tiled GEMM path, checked against the oracle (fp32) and by batch
+    # invariance against the same sequences run alone (bf16)
+    "tiny-f32-b20": Workload("tiny-f32-b20", _TINY_F32, block=8, batch=20, ctx=(30, 200), rounds=4,
+                             schedule="bernoulli", sched_param=0.7,
+                             description="tiny fp32 model, b=20 ragged ctx, B=8: 160 rows per round"),
+    "small-bf16-b24": Workload("small-bf16-b24",
+                               ModelDims("bf16", 512, 3, 8, 2, 128, 1376, 5008, 2, (0, 1, 2)),
+                               block=16, batch=24, ctx=(40, 520), rounds=4,
+                               schedule="geometric", sched_param=4.0,
+                               description="small bf16 model, b=24 ragged ctx, B=16: 384 rows per round"),
     "small-f32": Workload("small-f32",
                           ModelDims("f32", 512, 3, 8, 2, 128, 1376, 5008, 2, (0, 1, 2)),
                           block=16, batch=3, ctx=(40, 520), rounds=6,
