@@ -120,7 +120,10 @@ def main():
     prompts = make_prompts(wl)
     sched = make_schedule(wl, max(K, args.warmup))
     need = trajectory_length_needed(wl, sched)
-    max_ctx = max(need) + B
+    # the junk-draft trajectory rounds advance every sequence together until the
+    # longest continuation is done (checked every 8 rounds, <= B tokens each)
+    P0 = [len(p) for p in prompts]
+    max_ctx = max(P0) + max(n - p for n, p in zip(need, P0)) + 9 * B
     t = time.time()
     rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
     torch.cuda.synchronize()
@@ -160,7 +163,7 @@ def main():
         hist_com.append(sess.committed.clone())
         hist_acc.append(sess.accept.clone())
         hist_pos.append(pos)
-        if len(hist_com) % 64 == 0:
+        if len(hist_com) % 8 == 0:
             done = int((sess.seq_len.cpu().numpy() - np.array(P)).min())
     torch.cuda.synchronize()
     traj_h = np.zeros((b, L), np.int32)

@@ -286,10 +286,8 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
 }
 
 // ------------------------------------------------------------------ large M
-// Tiled GEMM for M > 128 rows (serving batches, prefill chunks): workgroup
-// tile of 128 rows x 8 strips (128 columns), four waves of 64 rows x 4
-// strips, A and W staged through LDS in MFMA fragment order, double
-// buffered.  The K loop runs the same contiguous ranges as the weight-
+// Tiled GEMM for M > 128 rows (serving batches, prefill chunks): A and W
+// staged through LDS in MFMA fragment order.  The K loop runs the same contiguous ranges as the weight-
 // streaming kernel's waves (gemm_shape's wave count for this N, K) and folds
 // each range's MFMA chain into the running sum in range order, starting from
 // zero, so every output element is bit-identical to what the weight-streaming
@@ -316,12 +314,19 @@ __device__ inline float norm_row_scale(const GemmParams& p, int m, int q16) {
 }
 
 constexpr int TILE_BM = 128, TILE_BS = 8, TILE_CW = TILE_BS * 16 + 4;
-constexpr size_t TILE_LDS = (size_t)TILE_BM * TILE_CW * sizeof(float);   // >= 2 stages x 16 KB
+constexpr size_t TILE_LDS = (size_t)TILE_BM * TILE_CW * sizeof(float);   // C tile; >= 2 staging buffers
 
+// Workgroup tile 128 rows x 8 strips (128 columns), four waves of 64 x 64.
+// Per k tile the workgroup stages 8 KB of A and 8 KB of W (four 16-byte
+// loads per thread); loads run TILE_D - 1 k tiles ahead in registers and the
+// LDS is double buffered.  About 250 registers per lane and 68 KB of LDS, so
+// two workgroups share a compute unit.
+constexpr int TILE_D = 4;
 template <typename T, int EPI, bool NORM>
-__global__ void __launch_bounds__(256) gemm_tile_kernel(GemmParams p, int nw, int mt, int units) {
+__global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw, int mt, int units) {
   constexpr int KL = TT<T>::KL;
   constexpr int KT = TT<T>::KT;
+  constexpr int D = TILE_D;
   extern __shared__ float lds[];
   __shared__ float s_rs[NORM ? TILE_BM : 1];
   const int lane = threadIdx.x & 63;
@@ -351,34 +356,36 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmParams p, int nw, in
     }
   }
 
-  // staging: 512 16-byte A chunks (row r, quarter q of its KT values) and 512
-  // W chunks (strip s, lane l) per k tile, two of each per thread
-  u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [stage][8 m tiles][64]
-  u32x4_t* sw = sa + 2 * 512;                                 // [stage][8 strips][64]
+  // staging: A chunk c (row c/4, quarter c%4 of its KT values) goes to the
+  // fragment slot of its m tile; W chunk c is lane c%64 of strip c/64
+  u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [buffer][8 m tiles][64]
+  u32x4_t* sw = sa + 2 * 512;                                 // [buffer][8 strips][64]
   const gu4* asrc[2];
-  int adst[2], wst[2];
+  const gu4* wsrc[2];
+  int adst[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = threadIdx.x + 256 * i;
     const int r = c >> 2, q = c & 3;
     asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
     adst[i] = (r >> 4) * 64 + q * 16 + (r & 15);
-    wst[i] = min(nt0 + (c >> 6), p.ntiles - 1) * p.ktiles;   // clamped strips are not stored
+    wsrc[i] = Wp + (size_t)min(nt0 + (c >> 6), p.ntiles - 1) * p.ktiles * 64 + (c & 63);   // clamped strips: not stored
   }
   constexpr int AST = KT * (int)sizeof(T) / 16;              // 16-byte chunks per k tile along an A row
-  u32x4_t ra[2], rw[2];
-  auto load = [&](int kt) {
+  u32x4_t ra[D][2], rw[D][2];                                 // register slots
+  auto load = [&](int slot, int kt) {                         // clamped: a load past the end is never used
+    kt = min(kt, k1 - 1);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      ra[i] = asrc[i][(size_t)kt * AST];
-      rw[i] = Wp[((size_t)wst[i] + kt) * 64 + ((threadIdx.x + 256 * i) & 63)];
+      ra[slot][i] = asrc[i][(size_t)kt * AST];
+      rw[slot][i] = wsrc[i][(size_t)kt * 64];
     }
   };
-  auto store = [&](int st) {
+  auto store = [&](int slot, int buf) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      sa[st * 512 + adst[i]] = ra[i];
-      sw[st * 512 + threadIdx.x + 256 * i] = rw[i];
+      sa[buf * 512 + adst[i]] = ra[slot][i];
+      sw[buf * 512 + threadIdx.x + 256 * i] = rw[slot][i];
     }
   };
 
@@ -399,29 +406,43 @@ __global__ void __launch_bounds__(256) gemm_tile_kernel(GemmParams p, int nw, in
       }
     ++folds;
   };
-
-  if (k0 < k1) {
-    load(k0);
-    store(0);
-  }
-  __syncthreads();
-  for (int kt = k0; kt < k1; ++kt) {                          // uniform
-    const int cur = (kt - k0) & 1;
-    if (kt + 1 < k1) load(kt + 1);
+  auto compute = [&](int buf) {
     u32x4_t a[4], b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = sa[cur * 512 + (wm * 4 + i) * 64 + lane];
+    for (int i = 0; i < 4; ++i) a[i] = sa[buf * 512 + (wm * 4 + i) * 64 + lane];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = sw[cur * 512 + (wn * 4 + j) * 64 + lane];
+    for (int j = 0; j < 4; ++j) b[j] = sw[buf * 512 + (wn * 4 + j) * 64 + lane];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = mma_frag(T(), a[i], b[j], acc[i][j]);
-    if ((kt - k0 + 1) % kper == 0 || kt + 1 == k1) fold();   // end of a range
-    if (kt + 1 < k1) store(cur ^ 1);
+  };
+  // k tile t sits in LDS buffer (t - k0) & 1 and, before that, in register
+  // slot (t - k0) % D; step t stores t + 1, loads t + D, multiplies t
+  auto step = [&](int t, int j) {
+    store((j + 1) % D, ((t - k0) & 1) ^ 1);
+    load(j, t + D);
+    compute((t - k0) & 1);
+    if ((t - k0 + 1) % kper == 0 || t + 1 == k1) fold();     // end of a range
     __syncthreads();
+  };
+
+  if (k0 < k1) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) load(j, k0 + j);
+    store(0, 0);
   }
+  __syncthreads();
+  int kt = k0;
+  for (; kt + D <= k1; kt += D) {                             // uniform
+#pragma unroll
+    for (int j = 0; j < D; ++j) step(kt + j, j);
+  }
+#pragma unroll
+  for (int j = 0; j < D; ++j)                                 // the last k1 - kt < D tiles
+    if (kt + j < k1) step(kt + j, j);
   while (folds < nw) fold();                                  // empty ranges add +0, as their waves do
+  __syncthreads();                                            // staging buffers free for the C tile
 
   // C tile to LDS (the staging buffers are free), then the epilogue
   float* ct = lds;

@@ -43,7 +43,8 @@ def test_batch_invariance(name, rounds, alone):
     need = trajectory_length_needed(wl, sched)
     print(f"[invariance] {name}: b={b} ctx={[len(p) for p in prompts]} rounds={rounds}", flush=True)
     w = make_weights(dm, wl.seed_w)
-    rt = Runtime(dm, B, b, max(need) + B, w, wl.carry_window)
+    P = [len(p) for p in prompts]   # trajectory rounds advance all sequences together
+    rt = Runtime(dm, B, b, max(P) + max(n - q for n, q in zip(need, P)) + 2 * B, w, wl.carry_window)
     del w
     sess = Session(rt, b)
     traj = gpu_trajectory(rt, sess, prompts, need)
