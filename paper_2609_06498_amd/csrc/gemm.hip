@@ -314,19 +314,23 @@ __device__ inline float norm_row_scale(const GemmParams& p, int m, int q16) {
 }
 
 constexpr int TILE_BM = 128, TILE_BS = 8, TILE_CW = TILE_BS * 16 + 4;
-constexpr size_t TILE_LDS = (size_t)TILE_BM * TILE_CW * sizeof(float);   // C tile; >= 2 staging buffers
+constexpr size_t TILE_LDS = (size_t)TILE_BM * TILE_CW * sizeof(float);   // C tile (widest); >= 2 staging buffers
 
-// Workgroup tile 128 rows x 8 strips (128 columns), four waves of 64 x 64.
-// Per k tile the workgroup stages 8 KB of A and 8 KB of W (four 16-byte
-// loads per thread); loads run TILE_D - 1 k tiles ahead in registers and the
-// LDS is double buffered.  About 250 registers per lane and 68 KB of LDS, so
-// two workgroups share a compute unit.
+// Workgroup tile 128 rows x BS strips (BS = 8: 128 columns; 4 for narrow
+// weights, so that enough workgroups exist), four waves of 64 rows x BS/2
+// strips.  Per k tile the workgroup stages 8 KB of A and BS KB of W; loads
+// run TILE_D - 1 k tiles ahead in registers and the LDS is double buffered.
+// About 250 registers per lane and at most 68 KB of LDS, so two workgroups
+// share a compute unit.
 constexpr int TILE_D = 4;
-template <typename T, int EPI, bool NORM>
+template <typename T, int EPI, bool NORM, int BS>
 __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw, int mt, int units) {
   constexpr int KL = TT<T>::KL;
   constexpr int KT = TT<T>::KT;
   constexpr int D = TILE_D;
+  constexpr int WS = BS / 2;                  // strips per wave
+  constexpr int NWC = BS / 4;                 // W chunks per thread and k tile
+  constexpr int CW = BS * 16 + 4;             // padded C-tile row
   extern __shared__ float lds[];
   __shared__ float s_rs[NORM ? TILE_BM : 1];
   const int lane = threadIdx.x & 63;
@@ -338,8 +342,8 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   if (unit >= units) return;                                  // padding of the dispatch grid
   const int ks = p.ksplit > 1 ? p.ksplit : 1;
   const int stile = unit / ks, h = unit - stile * ks;
-  const int nt0 = stile * TILE_BS;
-  const int nvalid = min(TILE_BS, p.ntiles - nt0);
+  const int nt0 = stile * BS;
+  const int nvalid = min(BS, p.ntiles - nt0);
   const int m0 = mtile * TILE_BM;
   const int rows = min(TILE_BM, p.M - m0);
   const int kpart = (p.ktiles + ks - 1) / ks;
@@ -359,9 +363,9 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   // staging: A chunk c (row c/4, quarter c%4 of its KT values) goes to the
   // fragment slot of its m tile; W chunk c is lane c%64 of strip c/64
   u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [buffer][8 m tiles][64]
-  u32x4_t* sw = sa + 2 * 512;                                 // [buffer][8 strips][64]
+  u32x4_t* sw = sa + 2 * 512;                                 // [buffer][BS strips][64]
   const gu4* asrc[2];
-  const gu4* wsrc[2];
+  const gu4* wsrc[NWC];
   int adst[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
@@ -369,37 +373,39 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     const int r = c >> 2, q = c & 3;
     asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
     adst[i] = (r >> 4) * 64 + q * 16 + (r & 15);
+  }
+#pragma unroll
+  for (int i = 0; i < NWC; ++i) {
+    const int c = threadIdx.x + 256 * i;
     wsrc[i] = Wp + (size_t)min(nt0 + (c >> 6), p.ntiles - 1) * p.ktiles * 64 + (c & 63);   // clamped strips: not stored
   }
   constexpr int AST = KT * (int)sizeof(T) / 16;              // 16-byte chunks per k tile along an A row
-  u32x4_t ra[D][2], rw[D][2];                                 // register slots
+  u32x4_t ra[D][2], rw[D][NWC];                               // register slots
   auto load = [&](int slot, int kt) {                         // clamped: a load past the end is never used
     kt = min(kt, k1 - 1);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      ra[slot][i] = asrc[i][(size_t)kt * AST];
-      rw[slot][i] = wsrc[i][(size_t)kt * 64];
-    }
+    for (int i = 0; i < 2; ++i) ra[slot][i] = asrc[i][(size_t)kt * AST];
+#pragma unroll
+    for (int i = 0; i < NWC; ++i) rw[slot][i] = wsrc[i][(size_t)kt * 64];
   };
   auto store = [&](int slot, int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      sa[buf * 512 + adst[i]] = ra[slot][i];
-      sw[buf * 512 + threadIdx.x + 256 * i] = rw[slot][i];
-    }
+    for (int i = 0; i < 2; ++i) sa[buf * 512 + adst[i]] = ra[slot][i];
+#pragma unroll
+    for (int i = 0; i < NWC; ++i) sw[buf * BS * 64 + threadIdx.x + 256 * i] = rw[slot][i];
   };
 
-  f32x4_t acc[4][4], tot[4][4];
+  f32x4_t acc[4][WS], tot[4][WS];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < WS; ++j) acc[i][j] = tot[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   int folds = 0;
   auto fold = [&]() {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < WS; ++j) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) tot[i][j][r] += acc[i][j][r];
         acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -407,15 +413,15 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     ++folds;
   };
   auto compute = [&](int buf) {
-    u32x4_t a[4], b[4];
+    u32x4_t a[4], b[WS];
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = sa[buf * 512 + (wm * 4 + i) * 64 + lane];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) b[j] = sw[buf * 512 + (wn * 4 + j) * 64 + lane];
+    for (int j = 0; j < WS; ++j) b[j] = sw[buf * BS * 64 + (wn * WS + j) * 64 + lane];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mma_frag(T(), a[i], b[j], acc[i][j]);
+      for (int j = 0; j < WS; ++j) acc[i][j] = mma_frag(T(), a[i], b[j], acc[i][j]);
   };
   // k tile t sits in LDS buffer (t - k0) & 1 and, before that, in register
   // slot (t - k0) % D; step t stores t + 1, loads t + D, multiplies t
@@ -449,18 +455,18 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < WS; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        ct[(wm * 64 + i * 16 + 4 * (lane >> 4) + r) * TILE_CW + (wn * 4 + j) * 16 + (lane & 15)] = tot[i][j][r];
+        ct[(wm * 64 + i * 16 + 4 * (lane >> 4) + r) * CW + (wn * WS + j) * 16 + (lane & 15)] = tot[i][j][r];
   __syncthreads();
   const int ncols = nvalid * 16;
   const int colbase = p.col0 + nt0 * 16;
   if constexpr (EPI == EPI_ARGMAX) {
     for (int e = threadIdx.x; e < rows * ncols; e += blockDim.x) {
       const int m = e / ncols, n = e - m * ncols;
-      float v = ct[m * TILE_CW + n];
-      if constexpr (NORM) ct[m * TILE_CW + n] = v = v * s_rs[m];
+      float v = ct[m * CW + n];
+      if constexpr (NORM) ct[m * CW + n] = v = v * s_rs[m];
       if (p.logits) p.logits[(size_t)(m0 + m) * p.ldl + colbase + n] = v;
     }
     __syncthreads();
@@ -469,10 +475,10 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     for (int e = threadIdx.x; e < rows * ngrp; e += blockDim.x) {
       const int m = e / ngrp, gi = e - m * ngrp;
       const int c0 = gi * 32, c1 = min(ncols, c0 + 32);
-      float best = ct[m * TILE_CW + c0];
+      float best = ct[m * CW + c0];
       int bi = c0;
       for (int n = c0 + 1; n < c1; ++n) {
-        const float v = ct[m * TILE_CW + n];
+        const float v = ct[m * CW + n];
         if (v > best) { best = v; bi = n; }
       }
       p.amax[(size_t)(nt0 / 2 + gi) * p.amax_ld + m0 + m] = argmax_key(best, colbase + bi);
@@ -483,8 +489,8 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     for (int e = threadIdx.x; e < rows * half; e += blockDim.x) {
       const int m = e / half, c = e - m * half;
       const int strip = c >> 3, cc = c & 7;
-      float gt = ct[m * TILE_CW + strip * 16 + cc];
-      float up = ct[m * TILE_CW + strip * 16 + 8 + cc];
+      float gt = ct[m * CW + strip * 16 + cc];
+      float up = ct[m * CW + strip * 16 + 8 + cc];
       if constexpr (NORM) {
         gt *= s_rs[m];
         up *= s_rs[m];
@@ -496,7 +502,7 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
       const int m = e / ncols, n = e - m * ncols;
       const int col = colbase + n;
       const size_t gm = (size_t)(m0 + m);
-      float v = ct[m * TILE_CW + n];
+      float v = ct[m * CW + n];
       if constexpr (NORM) v *= s_rs[m];
       if constexpr (EPI == EPI_STORE_T) {
         TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, v);
@@ -506,7 +512,7 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
         v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), gm * p.ldr + col));
         TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, v);
         if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), gm * p.ldy2 + col, v);
-        ct[m * TILE_CW + n] = v;
+        ct[m * CW + n] = v;
       } else if constexpr (EPI == EPI_BIAS_SILU) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, silu(v));
@@ -523,7 +529,7 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
           float sq = 0.f;
 #pragma unroll
           for (int c = 0; c < 16; ++c) {
-            const float v = ct[m * TILE_CW + j * 16 + c];
+            const float v = ct[m * CW + j * 16 + c];
             sq += v * v;
           }
           p.ssq_out[(size_t)(m0 + m) * p.ssq_out_ld + nt0 + j] = sq;
@@ -533,20 +539,30 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   }
 }
 
-template <typename T, int EPI, bool NORM>
-static hipError_t launch_tile(const GemmParams& p, const GemmShape& sh, int ks, hipStream_t st) {
-  const int mt = (p.M + TILE_BM - 1) / TILE_BM;
-  const int units = (p.ntiles + TILE_BS - 1) / TILE_BS * ks;
+template <typename T, int EPI, bool NORM, int BS>
+static hipError_t launch_tile_bs(const GemmParams& p, const GemmShape& sh, int ks, int mt, hipStream_t st) {
+  const int units = (p.ntiles + BS - 1) / BS * ks;
   const int blocks = (units + 7) / 8 * 8 * mt;
   static bool lds_set = false;   // the C tile needs more than the default dynamic LDS
   if (!lds_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_tile_kernel<T, EPI, NORM>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_tile_kernel<T, EPI, NORM, BS>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)TILE_LDS);
     if (e != hipSuccess) return e;
     lds_set = true;
   }
-  hipLaunchKernelGGL((gemm_tile_kernel<T, EPI, NORM>), dim3(blocks), dim3(256), TILE_LDS, st, p, sh.waves, mt, units);
+  const size_t lds = (size_t)TILE_BM * (BS * 16 + 4) * sizeof(float);
+  hipLaunchKernelGGL((gemm_tile_kernel<T, EPI, NORM, BS>), dim3(blocks), dim3(256), lds, st, p, sh.waves, mt, units);
   return hipGetLastError();
+}
+
+// Tile width from (N, M): 8 strips unless that leaves fewer workgroups than
+// compute units.  The arithmetic of an output element does not depend on it.
+template <typename T, int EPI, bool NORM>
+static hipError_t launch_tile(const GemmParams& p, const GemmShape& sh, int ks, hipStream_t st) {
+  const int mt = (p.M + TILE_BM - 1) / TILE_BM;
+  const int wide = (p.ntiles + TILE_BS - 1) / TILE_BS * ks * mt;
+  if (wide < 256) return launch_tile_bs<T, EPI, NORM, 4>(p, sh, ks, mt, st);
+  return launch_tile_bs<T, EPI, NORM, 8>(p, sh, ks, mt, st);
 }
 
 // Launch shape from (N, K) (and the K parts) only, never from M.  Wide weights (>= 1024
