@@ -38,6 +38,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--cpu-sample-ctx", type=int, default=48)
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's sequence count (batch sweeps)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (calibrates HBM counters)")
     return ap.parse_args()
@@ -111,6 +112,8 @@ def main():
     from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
 
     wl = get_config(args.workload)
+    if args.batch > 0:
+        wl = wl.with_(batch=args.batch)
     dm, B, b = wl.dims, wl.block, wl.batch
     K = args.steps
     log(f"workload {wl.name}: {wl.description}; steps {K} warmup {args.warmup}")

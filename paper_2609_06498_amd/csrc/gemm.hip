@@ -607,11 +607,16 @@ static hipError_t launch_mtn(const GemmParams& p, const GemmShape& sh, hipStream
     hipLaunchKernelGGL(kern, dim3(sh.groups), dim3(sh.waves * 64), lds, st, p);
     return hipGetLastError();
   };
+  // the tiled kernel for more than 128 rows, and from 64 rows for weights wide
+  // enough to give it a workgroup per compute unit or so (measured crossover:
+  // the weight-streaming kernel re-reads A from L2 once per strip group)
+  const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  const bool tile = mt > 8 || (mt >= 4 && (p.ntiles + TILE_BS - 1) / TILE_BS * ks >= 96);
+  if (tile) return launch_tile<T, EPI, NORM>(p, sh, ks, st);
   if (mt <= 1) return go(gemm_kernel<T, NG, 1, EPI, NORM>, 1);
   if (mt <= 2) return go(gemm_kernel<T, NG, 2, EPI, NORM>, 2);
   if (mt <= 4) return go(gemm_kernel<T, NG, 4, EPI, NORM>, 4);
-  if (mt <= 8) return go(gemm_kernel<T, NG, 8, EPI, NORM>, 8);
-  return launch_tile<T, EPI, NORM>(p, sh, p.ksplit > 1 ? p.ksplit : 1, st);
+  return go(gemm_kernel<T, NG, 8, EPI, NORM>, 8);
 }
 
 // The RMSNorm row scale is instantiated only for the projections that follow a norm.
