@@ -25,6 +25,10 @@ One round (Sec. 3 and Sec. 4.2):
                (Sec. 4.2, shift alignment); rows a+1..K-1 cover the rejected
                suffix positions t+a+2..t+K, so n_c = max(0, K-1-a).
 
+At temperature T > 0 (round_sampled) steps 1 and 3 draw the drafts from the
+drafter and accept them by speculative sampling (oracle.sampling); the other
+steps are unchanged, the corrected token taking the bonus' place.
+
 Pins: accept/commit/carry index maps are brute-forced and checked against
 position arithmetic; the whole loop is pinned by losslessness against plain
 greedy decoding and by KV/F equality with a fresh prefill
@@ -37,6 +41,7 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
+from . import sampling
 from .model import OracleModel
 
 CARRY_WINDOWS = ("suffix", "suffix+tail")
@@ -229,17 +234,50 @@ class OracleDFlow:
         if decide is not None:
             a, bonus = (int(v) for v in decide(a, bonus, logits))
             committed = [int(x) for x in block[1:a + 1]] + [bonus]
+        f, n_c = self._commit(s, block, a, committed, hcat, ks, vs)
+        return RoundResult(t=t, x_in=x, n_relay=n_relay, draft=d, draft_logits=dlg, block=block, logits=logits,
+                           g=g, hcap=hcat, f=f, a=a, bonus=bonus, committed=committed, n_carry=n_c)
+
+    def _commit(self, s: SeqState, block, a: int, committed, hcat, ks, vs):
+        """Keep positions t..t+a in the caches (t+a+1.. are rolled back),
+        append the committed tokens and record the relay of the suffix."""
         f = self.m.fuse(hcat)
-        # commit: positions t..t+a join the caches; t+a+1.. are rolled back
         for l in range(self.m.dims.n_layers):
             s.k[l] = np.concatenate([s.k[l], ks[l][:a + 1]])
             s.v[l] = np.concatenate([s.v[l], vs[l][:a + 1]])
         self._append_ctx(s, f[:a + 1])
         s.tokens += committed
         n_c, rows = self.carry_map(a)
-        s.carry = Carry(n_c, f[rows].copy(), bonus, int(block[a + 1]) if a < self.K else -1)
-        return RoundResult(t=t, x_in=x, n_relay=n_relay, draft=d, draft_logits=dlg, block=block, logits=logits,
-                           g=g, hcap=hcat, f=f, a=a, bonus=bonus, committed=committed, n_carry=n_c)
+        s.carry = Carry(n_c, f[rows].copy(), committed[-1], int(block[a + 1]) if a < self.K else -1)
+        return f, n_c
+
+    def round_sampled(self, s: SeqState, temperature: float, seed: int, stream: int, carry_on: bool = True,
+                      draft: Optional[Sequence[int]] = None, decide=None):
+        """One round decoded by speculative sampling at temperature T (see
+        oracle.sampling): the drafter samples its block, verification keeps
+        the target's distribution.  `draft` replaces the sampled drafts and
+        `decide(dec)` the (a, token) outcome; parity tests use them to follow
+        the device through decisions within the numerical tolerance.
+        Returns (RoundResult, drafter z-scores, drafter Gumbel noise,
+        SampledDecision)."""
+        t = s.t
+        inv_t = sampling.inv_temperature(temperature)
+        x, n_relay = self.draft_inputs(s, carry_on)
+        dlg = self.m.drafter_block(x, t, s.ck, s.cv)[1:]
+        d, zq, gq = sampling.sample_drafts(dlg, inv_t, seed, stream, t)
+        if draft is not None:
+            d = np.asarray(draft, np.int64)
+        block = np.concatenate([[s.anchor], d]).astype(np.int64)
+        logits, g, hcat, ks, vs = self.verify(s, block)
+        dec = sampling.accept_sampled(block, logits, dlg, inv_t, seed, stream, t)
+        a, bonus = dec.a, dec.bonus
+        if decide is not None:
+            a, bonus = (int(v) for v in decide(dec))
+        committed = [int(v) for v in block[1:a + 1]] + [bonus]
+        f, n_c = self._commit(s, block, a, committed, hcat, ks, vs)
+        res = RoundResult(t=t, x_in=x, n_relay=n_relay, draft=d, draft_logits=dlg, block=block, logits=logits,
+                          g=g, hcap=hcat, f=f, a=a, bonus=bonus, committed=committed, n_carry=n_c)
+        return res, zq, gq, dec
 
     # ------------------------------------------------------------ plain greedy (losslessness reference)
     def greedy_decode(self, prompt: Sequence[int], n_new: int) -> List[int]:
