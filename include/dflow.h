@@ -206,7 +206,9 @@ int dflow_prefill(dflow_ctx* ctx, hipStream_t stream, int seq, const int32_t* to
  * attends to the drafter context (positions < anchor_pos) and to the whole
  * block.  Writes draft_tok [b, K] (argmax of rows 1..K) and, if non-null,
  * block_out [b, B] = [anchor, drafts] and, if non-null, the fp32 drafter
- * logits of every block row, draft_logits [b*B, vocab] (row 0 unused).
+ * logits of every block row, draft_logits [b*B, vocab].  With draft_logits
+ * given, draft_tok and block_out may both be NULL (sampling decoding draws
+ * the drafts with dflow_sample_draft).
  * The block's K/V are written to the drafter context cache at
  * anchor_pos..anchor_pos+K as scratch and are overwritten by kv_commit. */
 int dflow_draft_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* anchor_tok,
@@ -217,7 +219,8 @@ int dflow_draft_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_
  * anchor followed by the K proposals, at positions start_pos[s]..+K.  Writes
  * the target KV of all B positions (speculatively; kv_commit rolls back the
  * rejected ones), the target argmax per row tgt_argmax [b, B] (lowest id on
- * ties), optional fp32 logits [b, B, vocab], and the residual outputs of the
+ * ties), optional fp32 logits [b, B, vocab] (with logits given, tgt_argmax
+ * may be NULL), and the residual outputs of the
  * capture layers, which accept_and_carry projects (hcap: pass NULL to use
  * the internal buffer; otherwise a device [b*B, n_capture*d] copy). */
 int dflow_verify_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,
@@ -240,6 +243,55 @@ int dflow_accept_and_carry(dflow_ctx* ctx, hipStream_t stream, int nseq, const i
  * context K/V of the projected rows 0..accept_len[s] at positions
  * seq_len..seq_len+accept_len (the name follows the paper's round contract). */
 int kv_commit(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* accept_len, int32_t* seq_len);
+
+/* ---- Sampling decoding at temperature T > 0 (Table 1 reports T = 1).
+ * Verification then follows speculative sampling (Leviathan, Kalman and
+ * Matias, ICML 2023, cited in Sec. 1), which keeps the target's output
+ * distribution: with p_j = softmax(target logits of verify row j / T) and
+ * q_i = softmax(drafter logits of block row i / T),
+ *   drafts    d_i ~ q_i (i = 1..K);
+ *   accept    d_i while u_i < p_{i-1}(d_i) / q_i(d_i) (a = leading accepted);
+ *   token     at block index a+1: drawn from max(0, p_a - q_{a+1})
+ *             normalised when a < K, from p_K when a = K.
+ * The round is then: dflow_draft_block (draft_logits non-null), then
+ * dflow_sample_draft, dflow_verify_block (logits non-null),
+ * dflow_accept_sampled, kv_commit.
+ * Random numbers: Philox4x64-10 (Salmon et al., SC 2011) with key (seed,
+ * stream[s]) and counter (anchor_pos[s], block index, purpose, column / 4),
+ * output word column % 4, purposes 0 = draft, 1 = acceptance, 2 = correction
+ * or bonus; a word x gives u = ((x >> 41) + 1/2) * 2^-23.  Draws use
+ * argmax_v (log-weight_v - log(-log u_v)), lowest id on ties.  A sequence's
+ * tokens therefore depend only on (seed, its stream id, its state), never on
+ * its slot or on the other sequences of the batch.  All arithmetic is fp32. */
+typedef struct dflow_sampler {
+  float temperature;        /* T: positive and finite */
+  uint64_t seed;            /* Philox key word 0 */
+  const uint64_t* stream;   /* device [b]: Philox key word 1 of each sequence (e.g. a request id) */
+} dflow_sampler;
+
+/* Draws d_i ~ q_i for rows i = 1..K of every sequence from draft_logits
+ * [b*B, vocab] (fp32, as written by dflow_draft_block; row s*B holds the
+ * anchor row and is not read).  Writes draft_tok [b, K] and, if non-null,
+ * block_out [b, B] = [anchor_tok[s], drafts].  anchor_pos [b] is the round's
+ * anchor position t (the counter word 0).  Host checks: smp non-null with a
+ * valid temperature, vocab a multiple of 4. */
+int dflow_sample_draft(dflow_ctx* ctx, hipStream_t stream, int nseq, const float* draft_logits,
+                       const int32_t* anchor_tok, const int32_t* anchor_pos, const dflow_sampler* smp,
+                       int32_t* draft_tok, int32_t* block_out);
+
+/* Speculative-sampling acceptance: the counterpart of dflow_accept_and_carry
+ * for T > 0, with the same outputs (accept_len, bonus = the token at block
+ * index a+1, committed [b, B], n_carry, the carry record, the projected
+ * features and the optional feat copy).  logits [b*B, vocab]: verify rows of
+ * dflow_verify_block; draft_logits [b*B, vocab]: the drafter logits the drafts
+ * were drawn from (rows 1..K read; every row's log-sum-exp is formed, so row 0
+ * must be finite or -inf too); block_tok [b, B] = [anchor, d_1..d_K];
+ * anchor_pos [b] and smp as in dflow_sample_draft.  A draft id outside
+ * [0, vocab) sets DFLOW_STATUS_BAD_TOKEN and is tested at the nearest valid id. */
+int dflow_accept_sampled(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,
+                         const int32_t* anchor_pos, const float* logits, const float* draft_logits,
+                         const dflow_sampler* smp, int32_t* accept_len, int32_t* bonus, int32_t* committed,
+                         int32_t* n_carry, void* feat);
 
 /* Serving support (continuous batching keeps the active sequences in slots
  * 0..nseq-1): moves the per-sequence state the library keeps between rounds

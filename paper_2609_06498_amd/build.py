@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdflow.so")
-SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "api.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "sampling.hip", "api.cpp"]
 HEADERS = ["common.h", "kernels.h"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # packed fp32 ops stay off (see the design notes on gfx950 code generation)

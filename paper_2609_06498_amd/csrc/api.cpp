@@ -67,6 +67,7 @@ struct dflow_ctx {
   unsigned* counters;    // arrival counters of last-workgroup reductions; every launch leaves them at 0
   void* ctxkv;           // [mmax][n_draft_layers * 2 * kv_dim] drafter-context K/V projections
   const void** dknorm;   // device [n_draft_layers] K-norm gain pointers of the drafter layers
+  void* samp;            // sampling decoding partials
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -182,6 +183,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add(256);                                            // 21 counters (zero between launches)
   add((size_t)mmax * d->n_draft_layers * 2 * kvd * elt);   // 22 ctxkv: drafter-context K/V rows of all drafter layers
   add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
+  add(samp_workspace_bytes(d->vocab, mmax, d->max_batch));   // 24 sampling partials (log-sum-exp, draw keys)
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -275,6 +277,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->counters = (unsigned*)(b + L.off[21]);
   c->ctxkv = b + L.off[22];
   c->dknorm = (const void**)(b + L.off[23]);
+  c->samp = b + L.off[24];
   c->u = c->xn;
   c->hid = c->act;
 
@@ -501,7 +504,7 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
                            pool_layer(c, c->c.v_pool, l), 1, cap)))
       return e;
   }
-  if (!argmax_out) return hipSuccess;
+  if (!argmax_out && !logits) return hipSuccess;
   // LM head (final RMSNorm folded in) over rows lm_row0 .. lm_row0+lm_rows-1 only
   if (lm_rows < 0) lm_rows = M;
   const size_t off = (size_t)lm_row0 * d.d * c->elt;
@@ -510,6 +513,7 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
   if ((e = gemm(c, st, EPI_ARGMAX, (char*)c->x + off, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr,
                 0, nullptr, 0, nullptr, logits, d.vocab, fin)))
     return e;
+  if (!argmax_out) return hipSuccess;
   return launch_argmax_reduce(c->amax, c->lm_groups, lm_rows, c->amax_part, c->counters, argmax_out, nullptr, st);
 }
 
@@ -595,7 +599,7 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
                                  float* draft_logits) {
   int rc = check_nseq(c, nseq);
   if (rc) return rc;
-  if (!anchor_tok || !anchor_pos || (!draft_tok && !block_out))
+  if (!anchor_tok || !anchor_pos || (!draft_tok && !block_out && !draft_logits))
     return fail(DFLOW_EINVAL, "draft_block: null argument");
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
@@ -616,6 +620,7 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   fin.ssq = c->ssq;
   HIPCHK(gemm(c, st, EPI_ARGMAX, c->x, d.d, c->w.draft_lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
               nullptr, draft_logits, d.vocab, fin));
+  if (!draft_tok && !block_out) return DFLOW_OK;
   const DraftOut dr{anchor_tok, B, draft_tok, block_out};
   HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, M, c->amax_part, c->counters, nullptr, &dr, st));
   return DFLOW_OK;
@@ -625,7 +630,7 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
                                   const int32_t* start_pos, int32_t* tgt_argmax, float* logits, void* hcap) {
   int rc = check_nseq(c, nseq);
   if (rc) return rc;
-  if (!block_tok || !start_pos || !tgt_argmax) return fail(DFLOW_EINVAL, "verify_block: null argument");
+  if (!block_tok || !start_pos || (!tgt_argmax && !logits)) return fail(DFLOW_EINVAL, "verify_block: null argument");
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
   HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
@@ -646,6 +651,51 @@ extern "C" int dflow_accept_and_carry(dflow_ctx* c, hipStream_t st, int nseq, co
   const int B = d.block, M = nseq * B;
   HIPCHK(launch_accept(block_tok, tgt_argmax, nseq, B, d.carry_window, accept_len, bonus, committed, n_carry,
                        c->carry_rec, st));
+  HIPCHK(project(c, st, M, c->f));
+  if (feat) HIPCHK(hipMemcpyAsync(feat, c->f, (size_t)M * d.d * c->elt, hipMemcpyDeviceToDevice, st));
+  return DFLOW_OK;
+}
+
+namespace {
+int sampler_args(const dflow_ctx* c, const dflow_sampler* smp, const int32_t* pos, SampleArgs* a) {
+  if (!smp || !smp->stream || !pos) return fail(DFLOW_EINVAL, "sampling: null sampler, stream or position array");
+  const float T = smp->temperature;
+  if (!(T > 0.f) || !std::isfinite(T)) return fail(DFLOW_EINVAL, "sampling: temperature %g (must be positive)", T);
+  a->inv_t = 1.0f / T;
+  a->seed = smp->seed;
+  a->stream = smp->stream;
+  a->pos = pos;
+  a->V = c->dm.vocab;
+  return DFLOW_OK;
+}
+}  // namespace
+
+extern "C" int dflow_sample_draft(dflow_ctx* c, hipStream_t st, int nseq, const float* draft_logits,
+                                  const int32_t* anchor_tok, const int32_t* anchor_pos, const dflow_sampler* smp,
+                                  int32_t* draft_tok, int32_t* block_out) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!draft_logits || !anchor_tok || !draft_tok) return fail(DFLOW_EINVAL, "sample_draft: null argument");
+  SampleArgs a;
+  if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
+  HIPCHK(launch_sample_draft(draft_logits, a, nseq, c->dm.block, anchor_tok, draft_tok, block_out, c->samp, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_accept_sampled(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* block_tok,
+                                    const int32_t* anchor_pos, const float* logits, const float* draft_logits,
+                                    const dflow_sampler* smp, int32_t* accept_len, int32_t* bonus,
+                                    int32_t* committed, int32_t* n_carry, void* feat) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!block_tok || !logits || !draft_logits || !accept_len || !committed)
+    return fail(DFLOW_EINVAL, "accept_sampled: null argument");
+  SampleArgs a;
+  if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
+  const dflow_dims& d = c->dm;
+  const int B = d.block, M = nseq * B;
+  HIPCHK(launch_accept_sampled(logits, draft_logits, block_tok, a, nseq, B, d.carry_window, accept_len, bonus,
+                               committed, n_carry, c->carry_rec, c->status, c->samp, st));
   HIPCHK(project(c, st, M, c->f));
   if (feat) HIPCHK(hipMemcpyAsync(feat, c->f, (size_t)M * d.d * c->elt, hipMemcpyDeviceToDevice, st));
   return DFLOW_OK;

@@ -291,8 +291,7 @@ hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_
 
 // ---------------------------------------------------------------- acceptance scan
 // a = number of leading drafts d_i (block index i) equal to the target argmax of row i-1;
-// bonus = argmax of row a; committed = d_1..d_a, bonus (rest -1).
-// The carried rows are a+1 .. a+n, placed at next-round block indices 1..n.
+// bonus = argmax of row a.
 __global__ void accept_kernel(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
                               int* bonus, int* committed, int* n_carry, int* carry_rec) {
   const int s = blockIdx.x * blockDim.x + threadIdx.x;
@@ -302,18 +301,7 @@ __global__ void accept_kernel(const int* block, const int* g, int nseq, int B, i
   const int* gs = g + (size_t)s * B;
   int a = 0;
   while (a < K && blk[a + 1] == gs[a]) ++a;
-  const int b = gs[a];
-  for (int j = 0; j < B; ++j) committed[(size_t)s * B + j] = j < a ? blk[j + 1] : (j == a ? b : -1);
-  int n = carry_window == 0 ? K - 1 - a : K - a;
-  if (n < 0) n = 0;
-  accept_len[s] = a;
-  if (bonus) bonus[s] = b;
-  if (n_carry) n_carry[s] = n;
-  int* rec = carry_rec + (size_t)s * CARRY_REC;
-  rec[0] = n;
-  rec[1] = a + 1;
-  rec[2] = b;
-  rec[3] = a < K ? blk[a + 1] : -1;
+  write_accept_outcome(s, a, gs[a], blk, B, carry_window, accept_len, bonus, committed, n_carry, carry_rec);
 }
 
 hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,

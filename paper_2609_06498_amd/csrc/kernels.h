@@ -141,7 +141,23 @@ hipError_t launch_force(const int* traj, int traj_stride, int traj_len, const si
 hipError_t launch_set_int(int* dst, int value, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* dst, uint32_t value, size_t n, hipStream_t s);
 
-// carry record per sequence: [n_carry, first source row, bonus, first rejected proposal]
-constexpr int CARRY_REC = 4;
+// ---- speculative sampling (sampling.hip)
+constexpr int SAMP_CHUNK = 4096;   // columns per workgroup of the vocabulary passes
+inline int samp_chunks(int V) { return (V + SAMP_CHUNK - 1) / SAMP_CHUNK; }
+struct SampleArgs {
+  float inv_t;              // 1/T rounded to fp32
+  uint64_t seed;            // Philox key word 0
+  const uint64_t* stream;   // [nseq] Philox key word 1 per sequence
+  const int* pos;           // [nseq] anchor position t of the round
+  int V;                    // vocabulary (multiple of 4); logits rows have stride V
+};
+size_t samp_workspace_bytes(int V, int rows, int nseq);
+// drafts d_i ~ softmax(z_i) of drafter logits rows s*B + i (i = 1..K)
+hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq, int B, const int* anchor,
+                               int* draft_tok, int* block_out, void* ws, hipStream_t st);
+// acceptance, correction / bonus draw and the outcome of every sequence
+hipError_t launch_accept_sampled(const float* logits, const float* dlog, const int* block, const SampleArgs& a,
+                                 int nseq, int B, int carry_window, int* accept_len, int* bonus, int* committed,
+                                 int* n_carry, int* carry_rec, int* status, void* ws, hipStream_t st);
 
 }  // namespace dflow

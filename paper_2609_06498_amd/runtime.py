@@ -58,6 +58,11 @@ class Cache(ctypes.Structure):
                 ("cv_pool", ctypes.c_void_p), ("page_table", ctypes.c_void_p)]
 
 
+class Sampler(ctypes.Structure):
+    """dflow_sampler: temperature, Philox seed, device pointer to the per-sequence stream ids."""
+    _fields_ = [("temperature", ctypes.c_float), ("seed", ctypes.c_uint64), ("stream", ctypes.c_void_p)]
+
+
 EXPORTS = {
     "dflow_last_error": (ctypes.c_char_p, []),
     "dflow_packed_bytes": (ctypes.c_size_t, [ctypes.c_int, ctypes.c_int, ctypes.c_int]),
@@ -77,6 +82,13 @@ EXPORTS = {
     "dflow_accept_and_carry": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_sample_draft": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Sampler),
+                                          ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_accept_sampled": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.POINTER(Sampler), ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "kv_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_qkv_parts": (ctypes.c_int, [ctypes.c_void_p]),
     "dflow_move_slot": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]),
@@ -260,6 +272,23 @@ class Runtime:
         self._check(self.lib.dflow_accept_and_carry(self.ctx, _stream(), nseq, _ptr(block_tok), _ptr(tgt_argmax),
                                                     _ptr(accept_len), _ptr(bonus), _ptr(committed), _ptr(n_carry),
                                                     _ptr(feat)), "dflow_accept_and_carry")
+
+    @staticmethod
+    def sampler(temperature: float, seed: int, stream) -> Sampler:
+        """stream: device uint64 (torch int64) tensor of per-sequence stream ids, kept alive by the caller."""
+        return Sampler(float(temperature), int(seed) & (2**64 - 1), _ptr(stream))
+
+    def sample_draft(self, nseq, draft_logits, anchor_tok, anchor_pos, sampler, draft_tok, block_out=None):
+        self._check(self.lib.dflow_sample_draft(self.ctx, _stream(), nseq, _ptr(draft_logits), _ptr(anchor_tok),
+                                                _ptr(anchor_pos), ctypes.byref(sampler), _ptr(draft_tok),
+                                                _ptr(block_out)), "dflow_sample_draft")
+
+    def accept_sampled(self, nseq, block_tok, anchor_pos, logits, draft_logits, sampler, accept_len, bonus,
+                       committed, n_carry, feat=None):
+        self._check(self.lib.dflow_accept_sampled(self.ctx, _stream(), nseq, _ptr(block_tok), _ptr(anchor_pos),
+                                                  _ptr(logits), _ptr(draft_logits), ctypes.byref(sampler),
+                                                  _ptr(accept_len), _ptr(bonus), _ptr(committed), _ptr(n_carry),
+                                                  _ptr(feat)), "dflow_accept_sampled")
 
     def kv_commit(self, nseq, accept_len, seq_len):
         self._check(self.lib.kv_commit(self.ctx, _stream(), nseq, _ptr(accept_len), _ptr(seq_len)), "kv_commit")

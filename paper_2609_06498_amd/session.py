@@ -3,7 +3,9 @@
 State per sequence slot: seq_len (KV length = anchor position) and the
 anchor token (the previous round's bonus).  One round is
 draft_block -> [measurement-only forcing] -> verify_block ->
-accept_and_carry -> kv_commit.
+accept_and_carry -> kv_commit; at temperature T > 0 (round_sampled) it is
+draft_block (logits) -> sample_draft -> verify_block (logits) ->
+accept_sampled -> kv_commit.
 """
 from __future__ import annotations
 
@@ -28,6 +30,16 @@ class Session:
         self.accept = i32(nseq)
         self.committed = i32(nseq, self.B)
         self.n_carry = i32(nseq)
+        self._dl = self._lg = None
+
+    def logit_buffers(self):
+        """fp32 [b*B, vocab] drafter and verify logits of sampling decoding (allocated once)."""
+        if self._dl is None:
+            torch = self.rt.torch
+            shape = (self.nseq * self.B, self.rt.dims.vocab)
+            self._dl = torch.empty(shape, dtype=torch.float32, device=self.rt.device)
+            self._lg = torch.empty(shape, dtype=torch.float32, device=self.rt.device)
+        return self._dl, self._lg
 
     def prefill(self, prompts: List[np.ndarray]):
         torch = self.rt.torch
@@ -46,4 +58,16 @@ class Session:
             rt.force_drafts(b, traj, traj_len, mode, tok, self.anchor, self.seq_len, self.block)
         rt.verify_block(b, self.block, self.seq_len, self.tgt, logits, hcap)
         rt.accept_and_carry(b, self.block, self.tgt, self.accept, self.anchor, self.committed, self.n_carry, feat)
+        rt.kv_commit(b, self.accept, self.seq_len)
+
+    def round_sampled(self, sampler, carry_on: bool = True, draft_logits=None, logits=None, hcap=None, feat=None):
+        """One round decoded by speculative sampling; `sampler` from Runtime.sampler."""
+        rt, b = self.rt, self.nseq
+        if draft_logits is None or logits is None:
+            draft_logits, logits = self.logit_buffers()
+        rt.draft_block(b, self.anchor, self.seq_len, carry_on, None, None, draft_logits)
+        rt.sample_draft(b, draft_logits, self.anchor, self.seq_len, sampler, self.draft_tok, self.block)
+        rt.verify_block(b, self.block, self.seq_len, None, logits, hcap)
+        rt.accept_sampled(b, self.block, self.seq_len, logits, draft_logits, sampler, self.accept, self.anchor,
+                          self.committed, self.n_carry, feat)
         rt.kv_commit(b, self.accept, self.seq_len)

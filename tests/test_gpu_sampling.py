@@ -1,0 +1,337 @@
+"""GPU parity of sampling decoding (T > 0) through the C-ABI against the
+oracle's speculative sampling (oracle/sampling.py).
+
+Both sides draw the same Philox4x64-10 numbers, so every decision is
+compared one by one:
+  * kernels on seeded synthetic logits (dflow_sample_draft and
+    dflow_accept_sampled with caller logits): drafts, acceptance lengths and
+    correction/bonus tokens bit-exact; a decision may differ only where the
+    oracle's own fp32 margin is within a few ulps (exp/log of different
+    libraries, a different summation order of the log-sum-exp);
+  * whole rounds of the model: the same, with the margins widened by the
+    observed logit difference of the rows involved (max |dz| bounds the
+    change of every Gumbel score, and of log p through the log-sum-exp);
+    the oracle follows the device through an excused decision;
+  * the law on the device: the first token emitted by a round, over many
+    streams from one state, follows the target's softmax(z / T) (chi-square),
+    the property that makes speculative sampling lossless.
+"""
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle.sampling as sp
+from tests.gpu_common import TOL, rel_rows
+from workload import get_config
+from workload.configs import ModelDims
+from workload.synth import make_prompts, make_weights
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SEED = 0x5EED_0001
+ULP = 1e-5
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2609_06498_amd import load_library
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return load_library()
+
+
+def _runtime(dims, block, nseq, max_ctx=256, seed_w=1):
+    from paper_2609_06498_amd import Runtime
+    return Runtime(dims, block, nseq, max_ctx, make_weights(dims, seed_w), "suffix")
+
+
+def _i32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
+
+
+def _streams(n, base=1000):
+    return torch.tensor([base + 7 * s for s in range(n)], dtype=torch.int64, device="cuda")
+
+
+# ------------------------------------------------------------ decision checks
+def _check_draft(d_dev, z, g, slack, ctx):
+    """d_dev drawn by the device; z, g the oracle's scores of the row."""
+    sc = (z + g).astype(np.float32)
+    d_orc = int(np.argmax(sc))
+    if d_dev == d_orc:
+        return 0
+    gap = float(sc[d_orc] - sc[d_dev])
+    assert gap <= slack + ULP * (1 + abs(float(sc[d_orc]))), f"{ctx}: draft {d_dev} vs {d_orc}, margin {gap}"
+    return 1
+
+
+def _check_accept(a_dev, dec, slack, ctx):
+    """a_dev against the oracle's tests: the first test on which the two
+    disagree must be within `slack` (+ ulps) of its threshold."""
+    if a_dev == dec.a:
+        return 0
+    i = min(a_dev, dec.a)
+    gap = abs(float(dec.log_u[i] - dec.ratio[i]))
+    assert gap <= slack + ULP * (1 + abs(float(dec.ratio[i]))), \
+        f"{ctx}: accept length {a_dev} vs {dec.a}, test {i + 1} margin {gap}"
+    return 1
+
+
+def _final_scores(dec, a, zp, seed, stream, t):
+    """Oracle log-weights, noise and (log p, log q) of the draw at block
+    index a+1 for acceptance length a (the device's)."""
+    V = zp.shape[1]
+    K = zp.shape[0] - 1
+    g = sp.gumbel(sp.uniforms(seed, stream, t, a + 1, sp.RESAMPLE, V))
+    if a == K:
+        return zp[K], g, None
+    # dec.lq holds drafter rows 1..K: row a+1 is dec.lq[a]
+    return sp.residual_logw(dec.lp[a], dec.lq[a]), g, (dec.lp[a], dec.lq[a])
+
+
+def _check_token(tok_dev, w, g, pq, dz_p, dz_q, zp_row, ctx):
+    """tok_dev against argmax(w + g).  With pq = (log p, log q) the weights are
+    log(p - q); their device values lie in the interval that log p, log q
+    moved by at most 2 dz give."""
+    sc = (w + g).astype(np.float32)
+    if not np.isfinite(w).any():
+        sc = (zp_row + g).astype(np.float32)
+    t_orc = int(np.argmax(sc))
+    if tok_dev == t_orc:
+        return 0
+    if pq is None or not np.isfinite(w).any():
+        gap = float(sc[t_orc] - sc[tok_dev])
+        assert gap <= 2 * dz_p + ULP * (1 + abs(float(sc[t_orc]))), f"{ctx}: token {tok_dev} vs {t_orc}, margin {gap}"
+        return 1
+    lp, lq = (np.asarray(x, np.float64) for x in pq)
+    ep, eq = 2 * dz_p + ULP, 2 * dz_q + ULP
+
+    def bounds(v):
+        hi = np.exp(lp[v] + ep) - np.exp(lq[v] - eq)
+        lo = np.exp(lp[v] - ep) - np.exp(lq[v] + eq)
+        f = lambda d: np.log(d) if d > 0 else -np.inf
+        return f(lo), f(hi)
+
+    lo_top, _ = bounds(t_orc)
+    _, hi_dev = bounds(tok_dev)
+    assert lo_top + g[t_orc] <= hi_dev + g[tok_dev] + ULP, \
+        f"{ctx}: token {tok_dev} vs {t_orc} outside the error interval"
+    return 1
+
+
+# ------------------------------------------------------------ kernels on synthetic logits
+def _synthetic(nseq, B, V, seed, scale=2.0, noise=1.0):
+    r = np.random.default_rng(seed)
+    tg = (r.normal(size=(nseq, B, V)) * scale).astype(np.float32)
+    dr = np.empty_like(tg)
+    dr[:, 0] = r.normal(size=(nseq, V)) * scale
+    dr[:, 1:] = tg[:, :-1] + r.normal(size=(nseq, B - 1, V)) * noise   # q_i near p_{i-1}
+    if nseq > 1:
+        dr[1, 2:] = tg[1, 1:-1]                      # sequence 1: drafter = target from index 2 on
+        tg[0, 1, :V // 3] = -np.inf                   # sequence 0: a row with zero-probability columns
+    return tg, dr
+
+
+SYN = [("tiny-f32", 1.0), ("small-f32", 0.6), ("wide-vocab", 1.0)]
+
+
+def _dims(name):
+    if name == "wide-vocab":
+        # the Qwen3 vocabulary (38 column chunks, ragged last chunk) on the tiny model
+        return ModelDims("f32", 256, 2, 4, 2, 64, 768, 151936, 1, (0, 1)), 16
+    wl = get_config(name)
+    return wl.dims, wl.block
+
+
+@pytest.mark.parametrize("name,T", SYN)
+def test_sampling_kernels_on_synthetic_logits(lib, name, T):
+    dims, B = _dims(name)
+    V, K = dims.vocab, B - 1
+    nseq = 4
+    print(f"[sampling] kernels {name} V={V} B={B} T={T}", flush=True)
+    rt = _runtime(dims, B, nseq)
+    streams = _streams(nseq)
+    smp = rt.sampler(T, SEED, streams)
+    inv_t = sp.inv_temperature(T)
+    excused = 0
+    for rep in range(3):
+        tg, dr = _synthetic(nseq, B, V, 100 + rep)
+        pos = np.array([17, 200, 5, 63 + rep], np.int32)
+        anchor = np.array([3, 9, 11, 2], np.int32)
+        dl, lg = torch.from_numpy(dr.reshape(nseq * B, V)).cuda(), torch.from_numpy(tg.reshape(nseq * B, V)).cuda()
+        pos_d, anc_d = _i32(pos), _i32(anchor)
+        draft = torch.zeros(nseq, K, dtype=torch.int32, device="cuda")
+        block = torch.zeros(nseq, B, dtype=torch.int32, device="cuda")
+        rt.sample_draft(nseq, dl, anc_d, pos_d, smp, draft, block)
+        acc = torch.zeros(nseq, dtype=torch.int32, device="cuda")
+        bonus, ncar = torch.zeros_like(acc), torch.zeros_like(acc)
+        com = torch.zeros(nseq, B, dtype=torch.int32, device="cuda")
+        rt.accept_sampled(nseq, block, pos_d, lg, dl, smp, acc, bonus, com, ncar)
+        torch.cuda.synchronize()
+        assert rt.status() == 0
+        g_draft, g_block = draft.cpu().numpy(), block.cpu().numpy()
+        g_a, g_b, g_com, g_nc = (x.cpu().numpy() for x in (acc, bonus, com, ncar))
+        for s in range(nseq):
+            st = int(streams[s])
+            ctx = f"{name} rep{rep} s{s}"
+            _, zq, gq = sp.sample_drafts(dr[s, 1:], inv_t, SEED, st, int(pos[s]))
+            for i in range(K):
+                excused += _check_draft(int(g_draft[s, i]), zq[i], gq[i], 0.0, f"{ctx} d{i + 1}")
+            assert g_block[s, 0] == anchor[s] and (g_block[s, 1:] == g_draft[s]).all(), ctx
+            dec = sp.accept_sampled(g_block[s], tg[s], dr[s, 1:], inv_t, SEED, st, int(pos[s]))
+            a = int(g_a[s])
+            excused += _check_accept(a, dec, 0.0, ctx)
+            zp = sp.scaled(tg[s], inv_t)
+            w, g, pq = _final_scores(dec, a, zp, SEED, st, int(pos[s]))
+            excused += _check_token(int(g_b[s]), w, g, pq, 0.0, 0.0, zp[a], ctx)
+            assert list(g_com[s][:a]) == list(g_block[s, 1:a + 1]) and g_com[s][a] == g_b[s], ctx
+            assert (g_com[s][a + 1:] == -1).all() and g_nc[s] == max(0, K - 1 - a), ctx
+            if s == 1:
+                assert a in (0, K), ctx    # q_i = p_{i-1} from index 2 on: only d_1 can be rejected
+            if s == 0:
+                # p_1 is zero on the first third of the vocabulary
+                if a >= 2:
+                    assert g_block[s, 2] >= V // 3, ctx
+                if a == 1:
+                    assert g_b[s] >= V // 3, ctx
+    rt.close()
+    print(f"[sampling] kernels {name}: excused decisions {excused}", flush=True)
+
+
+# ------------------------------------------------------------ whole rounds of the model
+ROUNDS = [("tiny-f32", 1.0), ("small-f32", 0.3), ("small-bf16", 1.0), ("small-bf16", 0.1), ("tiny-f32-b20", 0.5)]
+
+
+@pytest.mark.parametrize("name,T", ROUNDS)
+def test_sampled_round_parity(lib, name, T):
+    from oracle import Mode, OracleDFlow, OracleModel
+    from paper_2609_06498_amd.session import Session
+    wl = get_config(name)
+    dm, B, K, b, V = wl.dims, wl.block, wl.K, wl.batch, wl.dims.vocab
+    tol = TOL[dm.dtype]
+    w = make_weights(dm, wl.seed_w)
+    o = OracleDFlow(OracleModel(dm, w, Mode("fp32" if dm.dtype == "f32" else "bf16")), B, wl.carry_window)
+    prompts = make_prompts(wl)
+    rounds = wl.rounds
+    from paper_2609_06498_amd import Runtime
+    rt = Runtime(dm, B, b, max(len(p) for p in prompts) + (rounds + 1) * B, w, wl.carry_window)
+    print(f"[sampling] rounds {name} T={T} b={b} ctx={[len(p) for p in prompts]}", flush=True)
+    sess = Session(rt, b)
+    states = [o.prefill(p) for p in prompts]
+    sess.prefill(prompts)
+    streams = _streams(b, base=40)
+    smp = rt.sampler(T, SEED, streams)
+    inv_t = sp.inv_temperature(T)
+    anc = sess.anchor.cpu().numpy()
+    for s in range(b):
+        assert anc[s] == states[s].anchor, f"first anchor of seq {s}"
+    dl, lg = sess.logit_buffers()
+    excused, accepted = 0, 0
+    for r in range(rounds):
+        sess.round_sampled(smp, True)
+        torch.cuda.synchronize()
+        g_dl, g_lg = dl.cpu().numpy(), lg.cpu().numpy()
+        g_draft, g_blk = sess.draft_tok.cpu().numpy(), sess.block.cpu().numpy()
+        g_a, g_bonus = sess.accept.cpu().numpy(), sess.anchor.cpu().numpy()
+        g_com, g_nc, g_len = sess.committed.cpu().numpy(), sess.n_carry.cpu().numpy(), sess.seq_len.cpu().numpy()
+        for s in range(b):
+            rows = slice(s * B, (s + 1) * B)
+            st, t = int(streams[s]), states[s].t
+            ctx = f"{name} r{r} s{s}"
+            hold = {}
+
+            def decide(dec, s=s, hold=hold):
+                hold["dec"] = dec
+                return int(g_a[s]), int(g_bonus[s])
+
+            rr, zq, gq, _ = o.round_sampled(states[s], T, SEED, st, True, draft=g_draft[s], decide=decide)
+            dec = hold["dec"]
+            # the oracle's logits of the same rows; max |dz| bounds every score change
+            e = rel_rows(g_dl[rows][1:], rr.draft_logits)
+            assert e.max() <= tol, f"{ctx} draft logits rel err {e.max()}"
+            e = rel_rows(g_lg[rows], rr.logits)
+            assert e.max() <= tol, f"{ctx} verify logits rel err {e.max()}"
+            dzq = np.abs(g_dl[rows][1:] - rr.draft_logits).max(axis=1) * float(inv_t)
+            dzp = np.abs(g_lg[rows] - rr.logits).max(axis=1) * float(inv_t)
+            for i in range(K):
+                excused += _check_draft(int(g_draft[s, i]), zq[i], gq[i], 2 * dzq[i], f"{ctx} d{i + 1}")
+            a = int(g_a[s])
+            i = min(a, dec.a)
+            slack = 2 * (dzp[min(i, K)] + dzq[min(i, K - 1)])
+            excused += _check_accept(a, dec, slack, ctx)
+            zp = sp.scaled(rr.logits, inv_t)
+            wv, g, pq = _final_scores(dec, a, zp, SEED, st, t)
+            excused += _check_token(int(g_bonus[s]), wv, g, pq, dzp[a], dzq[min(a, K - 1)], zp[a], ctx)
+            assert list(g_com[s][:a + 1]) == rr.committed and (g_com[s][a + 1:] == -1).all(), ctx
+            assert int(g_nc[s]) == rr.n_carry and int(g_len[s]) == states[s].t, ctx
+            accepted += a
+        print(f"[sampling] {name} round {r}: a={list(g_a)}", flush=True)
+    assert rt.status() == 0
+    rt.close()
+    print(f"[sampling] rounds {name} T={T}: accepted {accepted}, excused decisions {excused}", flush=True)
+
+
+# ------------------------------------------------------------ the law on the device
+def test_first_token_law_on_device(lib):
+    """64 copies of one prompt in 64 slots; each repetition re-runs the round
+    from the same state (no commit, relay off) with fresh stream ids.  The
+    first emitted token must follow softmax(z_0 / T) of the target at the
+    anchor, and the first draft softmax(z_1 / T) of the drafter."""
+    from oracle import Mode, OracleDFlow, OracleModel
+    from paper_2609_06498_amd import Runtime
+    wl = get_config("small-f32")
+    dm, B, V = wl.dims, wl.block, wl.dims.vocab
+    T, nseq, reps = 0.2, 64, 40
+    w = make_weights(dm, wl.seed_w)
+    prompt = make_prompts(wl)[0][:60]
+    o = OracleDFlow(OracleModel(dm, w, Mode("fp32")), B, wl.carry_window)
+    st0 = o.prefill(prompt)
+    anchor0 = st0.anchor
+    rr = o.round(st0, carry_on=False)          # logits of the anchor row and drafter row 1
+    z0 = rr.logits[0].astype(np.float64) / T
+    q1 = rr.draft_logits[0].astype(np.float64) / T
+    p0 = np.exp(z0 - z0.max()); p0 /= p0.sum()
+    q1 = np.exp(q1 - q1.max()); q1 /= q1.sum()
+    rt = Runtime(dm, B, nseq, len(prompt) + 2 * B, w, wl.carry_window)
+    print(f"[sampling] law small-f32 T={T} slots={nseq} reps={reps}", flush=True)
+    tok = _i32(prompt)
+    anchor = torch.zeros(nseq, dtype=torch.int32, device="cuda")
+    for s in range(nseq):
+        rt.prefill(s, tok, anchor[s:s + 1])
+    seq_len = torch.full((nseq,), len(prompt), dtype=torch.int32, device="cuda")
+    dl = torch.empty(nseq * B, V, dtype=torch.float32, device="cuda")
+    lg = torch.empty_like(dl)
+    draft = torch.zeros(nseq, B - 1, dtype=torch.int32, device="cuda")
+    block = torch.zeros(nseq, B, dtype=torch.int32, device="cuda")
+    acc, bonus, ncar = (torch.zeros(nseq, dtype=torch.int32, device="cuda") for _ in range(3))
+    com = torch.zeros(nseq, B, dtype=torch.int32, device="cuda")
+    first, d1, lens = [], [], []
+    for rep in range(reps):
+        streams = _streams(nseq, base=10_000 + rep * nseq)
+        smp = rt.sampler(T, SEED, streams)
+        rt.draft_block(nseq, anchor, seq_len, False, None, None, dl)
+        rt.sample_draft(nseq, dl, anchor, seq_len, smp, draft, block)
+        rt.verify_block(nseq, block, seq_len, None, lg)
+        rt.accept_sampled(nseq, block, seq_len, lg, dl, smp, acc, bonus, com, ncar)
+        torch.cuda.synchronize()
+        first += list(com[:, 0].cpu().numpy())
+        d1 += list(draft[:, 0].cpu().numpy())
+        lens += list(acc.cpu().numpy())
+    assert rt.status() == 0
+    assert (anchor.cpu().numpy() == anchor0).all()
+    rt.close()
+
+    def pval(samples, probs, top=8):
+        idx = np.argsort(probs)[::-1][:top]
+        counts = np.bincount(np.asarray(samples), minlength=V).astype(np.float64)
+        obs = np.append(counts[idx], counts.sum() - counts[idx].sum())
+        exp = np.append(probs[idx], 1 - probs[idx].sum()) * len(samples)
+        return stats.chisquare(obs, exp).pvalue
+
+    lens = np.array(lens)
+    print(f"[sampling] law: accept-length histogram {np.bincount(lens, minlength=B)}", flush=True)
+    assert (lens == 0).sum() > 100 and (lens > 0).sum() > 100
+    pf, pd = pval(first, p0), pval(d1, q1)
+    print(f"[sampling] law: chi-square p-values first token {pf:.3g}, first draft {pd:.3g}", flush=True)
+    assert pf > 1e-4 and pd > 1e-4
