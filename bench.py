@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--cpu-sample-ctx", type=int, default=48)
     ap.add_argument("--batch", type=int, default=0, help="override the workload's sequence count (batch sweeps)")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="T > 0: sampling decoding (speculative sampling, the drafter's own samples) instead of "
+                         "greedy rounds with forced acceptance")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (calibrates HBM counters)")
     return ap.parse_args()
@@ -99,51 +102,11 @@ def gemm_bytes(rt, nseq):
     return verify + draft + accept + commit, launches
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the DFlow round is a single-GPU "
-              f"data-parallel step; multi-GPU sharding is described in DESIGN.md but not run.", file=sys.stderr)
-        sys.exit(2)
+def build_trajectory(rt, sess, prompts, need, sched, B, b):
+    """Target trajectory T*: the greedy continuation of every prompt, made by
+    junk-draft rounds through the same kernels (each commits at least the
+    bonus token).  Returns (traj [b, L] device, L, mode, tok) for forcing."""
     import torch
-    from paper_2609_06498_amd import Runtime
-    from paper_2609_06498_amd.session import Session
-    from workload import get_config
-    from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
-
-    wl = get_config(args.workload)
-    if args.batch > 0:
-        wl = wl.with_(batch=args.batch)
-    dm, B, b = wl.dims, wl.block, wl.batch
-    K = args.steps
-    log(f"workload {wl.name}: {wl.description}; steps {K} warmup {args.warmup}")
-    t = time.time()
-    w = make_weights(dm, wl.seed_w)
-    log(f"weights generated in {time.time() - t:.1f}s")
-    prompts = make_prompts(wl)
-    sched = make_schedule(wl, max(K, args.warmup))
-    need = trajectory_length_needed(wl, sched)
-    # the junk-draft trajectory rounds advance every sequence together until the
-    # longest continuation is done (checked every 8 rounds, <= B tokens each)
-    P0 = [len(p) for p in prompts]
-    max_ctx = max(P0) + max(n - p for n, p in zip(need, P0)) + 9 * B
-    t = time.time()
-    rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
-    torch.cuda.synchronize()
-    log(f"runtime created (upload + pack) in {time.time() - t:.1f}s")
-    if args.no_cpu_baseline:
-        del w
-    sess = Session(rt, b)
-    if args.calib_copy_mib > 0:   # a plain copy of known size, for the HBM counter calibration
-        n = args.calib_copy_mib << 20
-        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"calibration copy: {n} bytes read, {n} bytes written")
-        del src, dst
-
-    # ---- target trajectory T*: junk-draft rounds through the same kernels
     t = time.time()
     sess.prefill(prompts)
     torch.cuda.synchronize()
@@ -184,17 +147,76 @@ def main():
     traj.copy_(torch.from_numpy(traj_h))
     log(f"trajectory ({len(hist_com)} junk rounds) in {time.time() - t:.1f}s")
     assert rt.status() == 0
+    return traj, L, torch.from_numpy(sched["mode"]).cuda(), torch.from_numpy(sched["tok"]).cuda()
 
-    mode_d = torch.from_numpy(sched["mode"]).cuda()
-    tok_d = torch.from_numpy(sched["tok"]).cuda()
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the DFlow round is a single-GPU "
+              f"data-parallel step; multi-GPU sharding is described in DESIGN.md but not run.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_06498_amd import Runtime
+    from paper_2609_06498_amd.session import Session
+    from workload import get_config
+    from workload.synth import make_prompts, make_schedule, make_weights, trajectory_length_needed
+
+    wl = get_config(args.workload)
+    if args.batch > 0:
+        wl = wl.with_(batch=args.batch)
+    dm, B, b = wl.dims, wl.block, wl.batch
+    K = args.steps
+    log(f"workload {wl.name}: {wl.description}; steps {K} warmup {args.warmup}")
+    t = time.time()
+    w = make_weights(dm, wl.seed_w)
+    log(f"weights generated in {time.time() - t:.1f}s")
+    prompts = make_prompts(wl)
+    sched = make_schedule(wl, max(K, args.warmup))
+    need = trajectory_length_needed(wl, sched)
+    # the junk-draft trajectory rounds advance every sequence together until the
+    # longest continuation is done (checked every 8 rounds, <= B tokens each)
+    P0 = [len(p) for p in prompts]
+    max_ctx = max(P0) + max(n - p for n, p in zip(need, P0)) + 9 * B
+    sampled = args.temperature > 0
+    if sampled:   # every timed phase restarts from the prompts and commits at most B tokens per round
+        max_ctx = max(P0) + (max(K, args.warmup) + 2) * B
+    t = time.time()
+    rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
+    torch.cuda.synchronize()
+    log(f"runtime created (upload + pack) in {time.time() - t:.1f}s")
+    if args.no_cpu_baseline:
+        del w
+    sess = Session(rt, b)
+    if args.calib_copy_mib > 0:   # a plain copy of known size, for the HBM counter calibration
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy: {n} bytes read, {n} bytes written")
+        del src, dst
+
     carry_on = args.carry == "on"
+    if sampled:
+        streams = torch.arange(b, dtype=torch.int64, device="cuda")
+        smp = rt.sampler(args.temperature, 1234, streams)
 
-    def reset():
-        sess.prefill(prompts)
+        def reset():
+            sess.prefill(prompts)
 
-    def run(n):
-        for r in range(n):
-            sess.round(carry_on, force=(traj, L, mode_d[r], tok_d[r]))
+        def run(n):
+            for r in range(n):
+                sess.round_sampled(smp, carry_on)
+    else:
+        traj, L, mode_d, tok_d = build_trajectory(rt, sess, prompts, need, sched, B, b)
+
+        def reset():
+            sess.prefill(prompts)
+
+        def run(n):
+            for r in range(n):
+                sess.round(carry_on, force=(traj, L, mode_d[r], tok_d[r]))
 
     reset()
     run(args.warmup)
@@ -208,14 +230,15 @@ def main():
     dt = time.perf_counter() - t0
     len1 = sess.seq_len.cpu().numpy()
     committed = int((len1 - len0).sum())
-    expect = int((sched["accept"][:K] + 1).sum())
-    diverged = committed != expect
+    expect = None if sampled else int((sched["accept"][:K] + 1).sum())
+    diverged = expect is not None and committed != expect
     status = rt.status()
     tok_s = committed / dt
     ms_round = dt * 1e3 / K
     tau = committed / (K * b)
     log(f"timed {K} rounds: {ms_round:.3f} ms/round, {tok_s:.1f} tok/s, tau {tau:.3f} "
-        f"(schedule {expect / (K * b):.3f}), status {status}")
+        + (f"(sampling T={args.temperature})" if sampled else f"(schedule {expect / (K * b):.3f})")
+        + f", status {status}")
 
     # ---- live per-kernel timing with HIP events on the round's stream
     roofline, kernels = None, None
@@ -260,24 +283,28 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, w, prompts, tau, args.cpu_sample_ctx)
+        cpu = cpu_baseline(wl, w, prompts, tau, args.cpu_sample_ctx, args.temperature)
 
     out = {"metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": K,
            "warmup": args.warmup, "ms_per_step": round(ms_round, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16" if dm.dtype == "bf16" else "f32",
-           "data": "synthetic (seeded random-init weights, uniform prompts, forced geometric acceptance)",
+           "data": ("synthetic (seeded random-init weights, uniform prompts, speculative sampling at "
+                    f"T={args.temperature} with the drafter's own samples)") if sampled else
+                   "synthetic (seeded random-init weights, uniform prompts, forced geometric acceptance)",
            "config": {"workload": wl.name, "batch": b, "block": B, "ctx": list(wl.ctx), "rounds": K,
-                      "carry": args.carry, "schedule": f"{wl.schedule}({wl.sched_param})",
+                      "carry": args.carry,
+                      "schedule": f"sampling T={args.temperature}" if sampled else f"{wl.schedule}({wl.sched_param})",
                       "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
                       "parallelism": "single GPU"},
            "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(wl, w, prompts, tau, ctx_len):
+def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0):
     """The oracle timed on this host on a bounded sample: one full round
-    (draft + verify + accept/project + commit) of the same model after a
-    short prefill; tokens/s = realised tau of the GPU run / oracle round time."""
+    (draft + verify + accept/project + commit, or its sampled form at T > 0)
+    of the same model after a short prefill; tokens/s = realised tau of the
+    GPU run / oracle round time."""
     import threading
     from oracle import Mode, OracleDFlow, OracleModel
     dm = wl.dims
@@ -291,7 +318,10 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len):
     rng = np.random.default_rng(0)
     o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))  # carry present
     t = time.perf_counter()
-    o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))
+    if temperature > 0:
+        o.round_sampled(s, temperature, 1234, 0, True)
+    else:
+        o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))
     t_round = time.perf_counter() - t
     try:
         import threadpoolctl
@@ -301,7 +331,9 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len):
         threads = os.cpu_count()
     log(f"oracle: prefill {len(p)} tokens {t_pre:.1f}s, one round {t_round:.2f}s, {threads} BLAS threads")
     return {"value": round(tau / t_round, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"one {mode} oracle round (draft+verify+accept+commit, relay on) of {wl.name} after a "
+            "sample": f"one {mode} oracle round (draft+verify+accept+commit, relay on"
+                      + (f", speculative sampling T={temperature}" if temperature > 0 else "")
+                      + f") of {wl.name} after a "
                       f"{len(p)}-token prefill; tokens/s = GPU-realised tau {tau:.3f} / {t_round:.2f} s; "
                       f"host cpu_count {os.cpu_count()}"}
 

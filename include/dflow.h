@@ -279,13 +279,20 @@ int dflow_sample_draft(dflow_ctx* ctx, hipStream_t stream, int nseq, const float
                        const int32_t* anchor_tok, const int32_t* anchor_pos, const dflow_sampler* smp,
                        int32_t* draft_tok, int32_t* block_out);
 
+/* Prompt processing for sampling decoding: dflow_prefill, except that the
+ * first token is drawn from softmax(z / T) of the prompt's last row with the
+ * Philox counter (len - 1, 0, 2, column / 4) and key (seed, smp->stream[0]):
+ * pass this sequence's stream id as a one-element device array.  The rounds'
+ * counters start at t = len, so no number is drawn twice. */
+int dflow_prefill_sampled(dflow_ctx* ctx, hipStream_t stream, int seq, const int32_t* tok, int len,
+                          const dflow_sampler* smp, int32_t* first_token);
+
 /* Speculative-sampling acceptance: the counterpart of dflow_accept_and_carry
  * for T > 0, with the same outputs (accept_len, bonus = the token at block
  * index a+1, committed [b, B], n_carry, the carry record, the projected
  * features and the optional feat copy).  logits [b*B, vocab]: verify rows of
  * dflow_verify_block; draft_logits [b*B, vocab]: the drafter logits the drafts
- * were drawn from (rows 1..K read; every row's log-sum-exp is formed, so row 0
- * must be finite or -inf too); block_tok [b, B] = [anchor, d_1..d_K];
+ * were drawn from (rows 1..K read); block_tok [b, B] = [anchor, d_1..d_K];
  * anchor_pos [b] and smp as in dflow_sample_draft.  A draft id outside
  * [0, vocab) sets DFLOW_STATUS_BAD_TOKEN and is tested at the nearest valid id. */
 int dflow_accept_sampled(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,

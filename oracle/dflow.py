@@ -155,16 +155,23 @@ class OracleDFlow:
             s.ck[l] = np.concatenate([s.ck[l], k])
             s.cv[l] = np.concatenate([s.cv[l], v])
 
-    def prefill(self, prompt: Sequence[int]) -> SeqState:
+    def prefill(self, prompt: Sequence[int], sampler=None) -> SeqState:
         """Target KV and fused features for every prompt position; the first
-        anchor is the target's greedy token after the prompt."""
+        anchor is the target's greedy token after the prompt or, with
+        sampler = (T, seed, stream), a draw from softmax(z / T) of the last
+        row (oracle.sampling.sample_first)."""
         s = self.empty_state()
         prompt = [int(x) for x in prompt]
         logits = None
         for c in range(0, len(prompt), self.prefill_chunk):
             chunk = prompt[c:c + self.prefill_chunk]
             logits, _, _ = self._append_target(s, chunk, len(chunk))
-        s.tokens = prompt + [int(argmax_lowest(logits[-1]))]
+        if sampler is None:
+            first = int(argmax_lowest(logits[-1]))
+        else:
+            T, seed, stream = sampler
+            first = sampling.sample_first(logits[-1], sampling.inv_temperature(T), seed, stream, len(prompt) - 1)
+        s.tokens = prompt + [first]
         return s
 
     # ------------------------------------------------------------ round steps

@@ -189,6 +189,14 @@ def sample_drafts(draft_logits: np.ndarray, inv_t, seed: int, stream: int, t: in
     return d, z, g
 
 
+def sample_first(logits_row: np.ndarray, inv_t, seed: int, stream: int, t_last: int) -> int:
+    """The token after a prompt whose last position is t_last, drawn from
+    softmax(z / T) with counter (t_last, 0, correction purpose); rounds
+    address t >= t_last + 1, so no number is reused."""
+    z = scaled(logits_row, inv_t)
+    return gumbel_argmax(z, gumbel(uniforms(seed, stream, t_last, 0, RESAMPLE, z.shape[-1])))
+
+
 def accept_sampled(block: Sequence[int], logits: np.ndarray, draft_logits: np.ndarray, inv_t, seed: int,
                    stream: int, t: int) -> SampledDecision:
     """Speculative-sampling acceptance of block = [anchor, d_1..d_K] with

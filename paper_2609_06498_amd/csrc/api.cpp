@@ -68,6 +68,7 @@ struct dflow_ctx {
   void* ctxkv;           // [mmax][n_draft_layers * 2 * kv_dim] drafter-context K/V projections
   const void** dknorm;   // device [n_draft_layers] K-norm gain pointers of the drafter layers
   void* samp;            // sampling decoding partials
+  float* samp_row;       // [vocab] logits of the last prompt row (dflow_prefill_sampled)
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -184,6 +185,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)mmax * d->n_draft_layers * 2 * kvd * elt);   // 22 ctxkv: drafter-context K/V rows of all drafter layers
   add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
   add(samp_workspace_bytes(d->vocab, mmax, d->max_batch));   // 24 sampling partials (log-sum-exp, draw keys)
+  add((size_t)d->vocab * 4);                           // 25 fp32 logits of a prompt's last row (sampled prefill)
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -278,6 +280,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->ctxkv = b + L.off[22];
   c->dknorm = (const void**)(b + L.off[23]);
   c->samp = b + L.off[24];
+  c->samp_row = (float*)(b + L.off[25]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -570,14 +573,24 @@ int check_nseq(dflow_ctx* c, int nseq) {
 
 }  // namespace
 
-// ------------------------------------------------------------------ entry points
-extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len,
-                             int32_t* first_anchor) {
-  if (!c || !tok || !first_anchor) return fail(DFLOW_EINVAL, "prefill: null argument");
+namespace {
+int sampler_args(const dflow_ctx* c, const dflow_sampler* smp, const int32_t* pos, SampleArgs* a);
+
+// Prompt processing in chunks of max_rows; the last chunk's final row gives
+// the first token: its argmax, or a draw at temperature T when smp is given.
+int prefill_impl(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len, const dflow_sampler* smp,
+                 int32_t* first) {
+  if (!c || !tok || !first) return fail(DFLOW_EINVAL, "prefill: null argument");
   if (seq < 0 || seq >= c->dm.max_batch) return fail(DFLOW_EINVAL, "prefill: seq %d", seq);
   if (len < 1) return fail(DFLOW_ESHAPE, "prefill: len %d", len);
   if ((long long)len + c->dm.block > (long long)c->dm.max_pages * PAGE)
     return fail(DFLOW_ECAPACITY, "prefill: %d tokens exceed the page table (%d)", len, c->dm.max_pages * PAGE);
+  SampleArgs sa;
+  if (smp) {
+    // counter word 0 of the first draw: the prompt's last position (held in tmp_pos[1])
+    int rc = sampler_args(c, smp, c->tmp_pos + 1, &sa);
+    if (rc) return rc;
+  }
   const dflow_dims& d = c->dm;
   const int* pt = c->c.page_table + (size_t)seq * d.max_pages;
   for (int p0 = 0; p0 < len; p0 += d.max_rows) {
@@ -585,13 +598,32 @@ extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_
     const bool last = p0 + n >= len;
     HIPCHK(launch_set_int(c->tmp_pos, p0, st));
     HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
-    HIPCHK(target_forward(c, st, 1, n, c->tmp_pos, pt, last ? c->tmp_argmax : nullptr, nullptr, n - 1, 1));
+    int* amax = last && !smp ? c->tmp_argmax : nullptr;
+    float* lrow = last && smp ? c->samp_row : nullptr;
+    HIPCHK(target_forward(c, st, 1, n, c->tmp_pos, pt, amax, lrow, n - 1, 1));
     HIPCHK(project(c, st, n, c->fpre));
     HIPCHK(ctx_append(c, st, c->fpre, 1, n, c->tmp_pos, nullptr, pt));
-    if (last) HIPCHK(hipMemcpyAsync(first_anchor, c->tmp_argmax, 4, hipMemcpyDeviceToDevice, st));
+    if (last && !smp) HIPCHK(hipMemcpyAsync(first, c->tmp_argmax, 4, hipMemcpyDeviceToDevice, st));
+  }
+  if (smp) {
+    HIPCHK(launch_set_int(c->tmp_pos + 1, len - 1, st));
+    HIPCHK(launch_sample_first(c->samp_row, sa, first, c->samp, st));
   }
   HIPCHK(launch_fill_u32((uint32_t*)(c->carry_rec + (size_t)seq * CARRY_REC), 0u, CARRY_REC, st));
   return DFLOW_OK;
+}
+}  // namespace
+
+// ------------------------------------------------------------------ entry points
+extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len,
+                             int32_t* first_anchor) {
+  return prefill_impl(c, st, seq, tok, len, nullptr, first_anchor);
+}
+
+extern "C" int dflow_prefill_sampled(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len,
+                                     const dflow_sampler* smp, int32_t* first_token) {
+  if (!smp) return fail(DFLOW_EINVAL, "prefill_sampled: null sampler");
+  return prefill_impl(c, st, seq, tok, len, smp, first_token);
 }
 
 extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* anchor_tok,

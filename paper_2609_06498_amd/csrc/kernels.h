@@ -142,7 +142,7 @@ hipError_t launch_set_int(int* dst, int value, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* dst, uint32_t value, size_t n, hipStream_t s);
 
 // ---- speculative sampling (sampling.hip)
-constexpr int SAMP_CHUNK = 4096;   // columns per workgroup of the vocabulary passes
+constexpr int SAMP_CHUNK = 1024;   // columns per workgroup of the vocabulary passes (one 4-column group per lane)
 inline int samp_chunks(int V) { return (V + SAMP_CHUNK - 1) / SAMP_CHUNK; }
 struct SampleArgs {
   float inv_t;              // 1/T rounded to fp32
@@ -155,6 +155,8 @@ size_t samp_workspace_bytes(int V, int rows, int nseq);
 // drafts d_i ~ softmax(z_i) of drafter logits rows s*B + i (i = 1..K)
 hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq, int B, const int* anchor,
                                int* draft_tok, int* block_out, void* ws, hipStream_t st);
+// first token after a prompt: out[0] ~ softmax(row / T), counter (pos[0], 0, 2, column / 4)
+hipError_t launch_sample_first(const float* row, const SampleArgs& a, int* out, void* ws, hipStream_t st);
 // acceptance, correction / bonus draw and the outcome of every sequence
 hipError_t launch_accept_sampled(const float* logits, const float* dlog, const int* block, const SampleArgs& a,
                                  int nseq, int B, int carry_window, int* accept_len, int* bonus, int* committed,

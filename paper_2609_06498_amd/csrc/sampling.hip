@@ -22,8 +22,9 @@
 // log(exp(log p) - exp(log q)) where positive (all non-positive: drawn from z_p).
 //
 // Launch shapes: every kernel over logits takes one workgroup of 256 lanes per
-// (4096-column chunk, row); a lane handles four groups of four columns (one
-// Philox block and one 16-byte load per group).
+// (1024-column chunk, row); a lane handles one group of four columns (one
+// Philox block and one 16-byte load), so a Qwen3 vocabulary row spreads over
+// 149 workgroups.  Chunk partials are folded by one wave per row or sequence.
 #include "common.h"
 #include "kernels.h"
 
@@ -100,19 +101,23 @@ struct SampP {
   int V, B, chunks;
 };
 
-// ---------------------------------------------------------------- drafts
-// grid (chunk, s*K + i-1): partial Gumbel-max key of drafter row i over one chunk
-__global__ void __launch_bounds__(256) draft_gumbel_kernel(const float* dlog, SampP p, uint64_t* part) {
+// rows drawn by draw_kernel: row r is block index i = r % K + i0 of sequence
+// s = r / K, logits row s * B + i, counter (t_s, i, purpose, column / 4)
+struct DrawRows { int K, i0, purpose; };
+
+// ---------------------------------------------------------------- drafts (and the first token)
+// grid (chunk, row r): partial Gumbel-max key of one logits row over one chunk
+__global__ void __launch_bounds__(256) draw_kernel(const float* dlog, SampP p, DrawRows dr, uint64_t* part) {
   __shared__ uint64_t sh[4];
-  const int c = blockIdx.x, r = blockIdx.y, K = p.B - 1;
-  const int s = r / K, i = r - s * K + 1;
+  const int c = blockIdx.x, r = blockIdx.y;
+  const int s = r / dr.K, i = r - s * dr.K + dr.i0;
   const float* row = dlog + (size_t)(s * p.B + i) * p.V;
   const uint64_t key1 = p.stream[s], t = (uint64_t)p.pos[s];
   const int g0 = c * GPW, g1 = min(p.V / 4, g0 + GPW);
   uint64_t best = 0;
   for (int g = g0 + threadIdx.x; g < g1; g += 256) {
     const float4 x = *(const float4*)(row + 4 * (size_t)g);
-    const Words w = philox(p.seed, key1, t, (uint64_t)i, 0, (uint64_t)g);
+    const Words w = philox(p.seed, key1, t, (uint64_t)i, (uint64_t)dr.purpose, (uint64_t)g);
     const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -125,20 +130,24 @@ __global__ void __launch_bounds__(256) draft_gumbel_kernel(const float* dlog, Sa
   if (threadIdx.x == 0) part[(size_t)r * p.chunks + c] = best;
 }
 
-// one lane per drafter row: fold the chunk keys, write the draft and the block
-__global__ void draft_finish_kernel(const uint64_t* part, int rows, int chunks, int B, const int* anchor,
-                                    int* draft_tok, int* block_out) {
-  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+// one wave per drawn row: fold the chunk keys (lanes stride the chunks, then
+// a wave max); out[r] = the token and, for drafts (K = B - 1, i0 = 1),
+// block_out = [anchor, drafts]
+__global__ void __launch_bounds__(256) draw_finish_kernel(const uint64_t* part, int rows, int chunks, int B,
+                                                          const int* anchor, int* draft_tok, int* block_out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (r >= rows) return;
-  const int K = B - 1, s = r / K, i = r - s * K + 1;
   uint64_t best = 0;
-  for (int c = 0; c < chunks; ++c) {
+  for (int c = lane; c < chunks; c += 64) {
     const uint64_t k = part[(size_t)r * chunks + c];
     best = k > best ? k : best;
   }
+  best = wave_max_u64(best);
+  if (lane) return;
   const int v = argmax_key_index(best);
   if (draft_tok) draft_tok[r] = v;
   if (block_out) {
+    const int K = B - 1, s = r / K, i = r - s * K + 1;
     block_out[(size_t)s * B + i] = v;
     if (i == 1) block_out[(size_t)s * B] = anchor[s];
   }
@@ -151,6 +160,7 @@ __global__ void __launch_bounds__(256) lse_part_kernel(const float* logits, cons
                                                        float* ml) {
   __shared__ float sh[4];
   const int c = blockIdx.x, y = blockIdx.y;
+  if (y >= R && (y - R) % p.B == 0) return;   // drafter row 0 (the anchor row) is not used
   const float* row = y < R ? logits + (size_t)y * p.V : dlog + (size_t)(y - R) * p.V;
   const int g0 = c * GPW, g1 = min(p.V / 4, g0 + GPW);
   float z[GPW / 256][4];
@@ -188,14 +198,39 @@ __global__ void __launch_bounds__(256) lse_part_kernel(const float* logits, cons
   }
 }
 
-__device__ inline float fold_lse(const float* ml, int chunks) {
-  float m = -INFINITY;
-  for (int c = 0; c < chunks; ++c) m = fmaxf(m, ml[2 * c]);
-  if (m == -INFINITY) return -INFINITY;
-  float s = 0.f;
-  for (int c = 0; c < chunks; ++c)
-    if (ml[2 * c] != -INFINITY) s += ml[2 * c + 1] * expf(ml[2 * c] - m);
-  return m + logf(s);
+constexpr int FOLD_IT = 4;    // chunk partials per lane: vocabularies up to 64 * 4 * 1024 columns
+constexpr int FOLD_ROWS = 8;  // rows a wave folds at once (their loads issue together)
+
+// log-sum-exp of up to FOLD_ROWS rows (row offsets rowoff[j], j < n) from
+// their chunk partials (max, sum): the row max by a lane-local max over chunks
+// lane + 64 k and a shuffle tree, then the sum of the partial sums rescaled to
+// it, lane-local in k order and by a shuffle tree; lse[j]
+__device__ inline void wave_fold_rows(const float* ml, int chunks, const int* rowoff, int n, float* lse) {
+  const int lane = threadIdx.x & 63;
+  float2 v[FOLD_ROWS][FOLD_IT];
+#pragma unroll
+  for (int j = 0; j < FOLD_ROWS; ++j)
+#pragma unroll
+    for (int k = 0; k < FOLD_IT; ++k) {
+      const int c = lane + 64 * k;
+      v[j][k] = (j < n && c < chunks) ? *(const float2*)(ml + ((size_t)rowoff[j] * chunks + c) * 2)
+                                      : make_float2(-INFINITY, 0.f);
+    }
+#pragma unroll
+  for (int j = 0; j < FOLD_ROWS; ++j) {
+    float m = v[j][0].x;
+#pragma unroll
+    for (int k = 1; k < FOLD_IT; ++k) m = fmaxf(m, v[j][k].x);
+    m = wave_max_f(m);
+    float sum = 0.f;
+    if (m != -INFINITY) {
+#pragma unroll
+      for (int k = 0; k < FOLD_IT; ++k)
+        if (v[j][k].x != -INFINITY) sum += v[j][k].y * expf(v[j][k].x - m);
+    }
+    sum = wave_sum_f(sum);
+    lse[j] = m == -INFINITY ? -INFINITY : m + logf(sum);
+  }
 }
 
 // ---------------------------------------------------------------- acceptance + correction
@@ -211,27 +246,48 @@ __global__ void __launch_bounds__(256) accept_sample_kernel(const float* logits,
   const int c = blockIdx.x, s = blockIdx.y, B = p.B, K = B - 1;
   const uint64_t key1 = p.stream[s], t = (uint64_t)p.pos[s];
   const int tid = threadIdx.x;
-  if (tid < 2 * B) {
-    const int which = tid / B, j = tid - which * B;
-    const float* m = ml + ((size_t)(which ? R : 0) + (size_t)s * B + j) * p.chunks * 2;
-    const float l = fold_lse(m, p.chunks);
-    if (which) lse_q[j] = l;
-    else lse_p[j] = l;
+  // acceptance operands first (they need no log-sum-exp): lane i = 1..K of
+  // wave 0 reads d_i, z_p(d_i) of verify row i-1, z_q(d_i) of drafter row i, u_i
+  float xp = 0.f, xq = 0.f, logu = 0.f;
+  if (tid >= 1 && tid <= K) {
+    int x = block[(size_t)s * B + tid];
+    if (x < 0 || x >= p.V) {
+      if (c == 0) set_status(status, ST_BAD_TOKEN);
+      x = x < 0 ? 0 : p.V - 1;
+    }
+    xp = logits[(size_t)(s * B + tid - 1) * p.V + x];
+    xq = dlog[(size_t)(s * B + tid) * p.V + x];
+    logu = logf(unif(philox(p.seed, key1, t, (uint64_t)tid, 1, 0).w[0]));
+  }
+  // wave w folds rows w, w + 4, ... of [target rows 0..B-1, drafter rows 1..B-1]
+  for (int y0 = tid >> 6; y0 < 2 * B - 1; y0 += 4 * FOLD_ROWS) {
+    int off[FOLD_ROWS];
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < FOLD_ROWS; ++j) {
+      const int y = y0 + 4 * j;
+      if (y < 2 * B - 1) n = j + 1;
+      off[j] = y < B ? s * B + y : R + s * B + (y - B + 1);
+    }
+    float l[FOLD_ROWS];
+    wave_fold_rows(ml, p.chunks, off, n, l);
+    if ((tid & 63) == 0) {
+#pragma unroll
+      for (int j = 0; j < FOLD_ROWS; ++j) {
+        const int y = y0 + 4 * j;
+        if (y < B) lse_p[y] = l[j];
+        else if (y < 2 * B - 1) lse_q[y - B + 1] = l[j];
+      }
+    }
   }
   __syncthreads();
   if (tid < 64) {
-    // lane i (1..K): acceptance test of d_i
+    // lane i (1..K): d_i is kept when log u_i < log p_{i-1}(d_i) - log q_i(d_i)
     bool rej = false;
     if (tid >= 1 && tid <= K) {
-      int x = block[(size_t)s * B + tid];
-      if (x < 0 || x >= p.V) {
-        if (c == 0) set_status(status, ST_BAD_TOKEN);
-        x = x < 0 ? 0 : p.V - 1;
-      }
-      const float lp = logits[(size_t)(s * B + tid - 1) * p.V + x] * p.inv_t - lse_p[tid - 1];
-      const float lq = dlog[(size_t)(s * B + tid) * p.V + x] * p.inv_t - lse_q[tid];
-      const Words w = philox(p.seed, key1, t, (uint64_t)tid, 1, 0);
-      rej = !(logf(unif(w.w[0])) < lp - lq);
+      const float lp = xp * p.inv_t - lse_p[tid - 1];
+      const float lq = xq * p.inv_t - lse_q[tid];
+      rej = !(logu < lp - lq);
     }
     const uint64_t mask = __ballot(rej);
     if (tid == 0) s_a = mask ? __ffsll((unsigned long long)mask) - 2 : K;
@@ -272,19 +328,23 @@ __global__ void __launch_bounds__(256) accept_sample_kernel(const float* logits,
   }
 }
 
-// one lane per sequence: fold the chunk keys into the correction / bonus token
+// one wave per sequence: fold the chunk keys into the correction / bonus token
 // and write the round's outcome and carry record (as the greedy scan does)
-__global__ void accept_finish_kernel(const uint64_t* keys, const int* acc, const int* block, int nseq, int B,
-                                     int chunks, int carry_window, int* accept_len, int* bonus, int* committed,
-                                     int* n_carry, int* carry_rec) {
-  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+__global__ void __launch_bounds__(256) accept_finish_kernel(const uint64_t* keys, const int* acc, const int* block,
+                                                            int nseq, int B, int chunks, int carry_window,
+                                                            int* accept_len, int* bonus, int* committed,
+                                                            int* n_carry, int* carry_rec) {
+  const int s = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (s >= nseq) return;
   uint64_t b1 = 0, b2 = 0;
-  for (int c = 0; c < chunks; ++c) {
+  for (int c = lane; c < chunks; c += 64) {
     const uint64_t k1 = keys[((size_t)s * chunks + c) * 2], k2 = keys[((size_t)s * chunks + c) * 2 + 1];
     b1 = k1 > b1 ? k1 : b1;
     b2 = k2 > b2 ? k2 : b2;
   }
+  b1 = wave_max_u64(b1);
+  b2 = wave_max_u64(b2);
+  if (lane) return;
   const int a = acc[s];
   const bool empty = (uint32_t)(b1 >> 32) <= NEG_INF_ORD;   // every residual weight was -inf
   const int tok = argmax_key_index(empty ? b2 : b1);
@@ -317,13 +377,22 @@ size_t samp_workspace_bytes(int V, int rows, int nseq) {
 hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq, int B, const int* anchor,
                                int* draft_tok, int* block_out, void* ws, hipStream_t st) {
   if (nseq <= 0) return hipSuccess;
-  if (B < 2 || B > 64 || a.V < 4 || (a.V & 3)) return hipErrorInvalidValue;
+  if (B < 2 || B > 64 || a.V < 4 || (a.V & 3) || samp_chunks(a.V) > 64 * FOLD_IT) return hipErrorInvalidValue;
   const SampP p = make_params(a, B);
   const int rows = nseq * (B - 1);
   uint64_t* part = (uint64_t*)ws;
-  hipLaunchKernelGGL(draft_gumbel_kernel, dim3(p.chunks, rows), dim3(256), 0, st, dlog, p, part);
-  hipLaunchKernelGGL(draft_finish_kernel, dim3((rows + 255) / 256), dim3(256), 0, st, part, rows, p.chunks, B,
+  hipLaunchKernelGGL(draw_kernel, dim3(p.chunks, rows), dim3(256), 0, st, dlog, p, DrawRows{B - 1, 1, 0}, part);
+  hipLaunchKernelGGL(draw_finish_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, part, rows, p.chunks, B,
                      anchor, draft_tok, block_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_first(const float* row, const SampleArgs& a, int* out, void* ws, hipStream_t st) {
+  if (a.V < 4 || (a.V & 3) || samp_chunks(a.V) > 64 * FOLD_IT) return hipErrorInvalidValue;
+  const SampP p = make_params(a, 1);
+  uint64_t* part = (uint64_t*)ws;
+  hipLaunchKernelGGL(draw_kernel, dim3(p.chunks, 1), dim3(256), 0, st, row, p, DrawRows{1, 0, 2}, part);
+  hipLaunchKernelGGL(draw_finish_kernel, dim3(1), dim3(256), 0, st, part, 1, p.chunks, 1, nullptr, out, nullptr);
   return hipGetLastError();
 }
 
@@ -331,7 +400,7 @@ hipError_t launch_accept_sampled(const float* logits, const float* dlog, const i
                                  int nseq, int B, int carry_window, int* accept_len, int* bonus, int* committed,
                                  int* n_carry, int* carry_rec, int* status, void* ws, hipStream_t st) {
   if (nseq <= 0) return hipSuccess;
-  if (B < 2 || B > 64 || a.V < 4 || (a.V & 3)) return hipErrorInvalidValue;
+  if (B < 2 || B > 64 || a.V < 4 || (a.V & 3) || samp_chunks(a.V) > 64 * FOLD_IT) return hipErrorInvalidValue;
   const SampP p = make_params(a, B);
   const int R = nseq * B;
   char* b = (char*)ws;
@@ -343,7 +412,7 @@ hipError_t launch_accept_sampled(const float* logits, const float* dlog, const i
   hipLaunchKernelGGL(lse_part_kernel, dim3(p.chunks, 2 * R), dim3(256), 0, st, logits, dlog, p, R, ml);
   hipLaunchKernelGGL(accept_sample_kernel, dim3(p.chunks, nseq), dim3(256), 0, st, logits, dlog, block, p, R, ml,
                      keys, acc, status);
-  hipLaunchKernelGGL(accept_finish_kernel, dim3((nseq + 63) / 64), dim3(64), 0, st, keys, acc, block, nseq, B,
+  hipLaunchKernelGGL(accept_finish_kernel, dim3((nseq + 3) / 4), dim3(256), 0, st, keys, acc, block, nseq, B,
                      p.chunks, carry_window, accept_len, bonus, committed, n_carry, carry_rec);
   return hipGetLastError();
 }

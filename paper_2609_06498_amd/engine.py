@@ -13,6 +13,13 @@ swapped, so the pages stay a permutation; the library's own per-slot state
 moves with dflow_move_slot).  Queued requests are admitted into free slots by
 a prefill, whose argmax is the request's first output token.
 
+With a temperature T > 0 the engine decodes by speculative sampling: the
+first token is drawn at the prefill (dflow_prefill_sampled), and a round is
+draft_block (drafter logits) -> sample_draft -> verify_block (logits) ->
+accept_sampled -> kv_commit.  Each request draws from its own Philox stream
+(its request id under the engine's sampling seed), so its tokens do not
+depend on its slot or on the requests that share its rounds.
+
 Every step runs in the library's kernels; this layer only sequences calls
 and keeps the per-request bookkeeping.  The one host synchronisation per
 round reads the committed tokens, which the retirement decision needs.
@@ -40,7 +47,9 @@ class Request:
 
 
 class Engine:
-    """Greedy DFlow serving of many requests through one Runtime.
+    """DFlow serving of many requests through one Runtime: greedy decoding,
+    or speculative sampling at `temperature` (Philox key (sample_seed,
+    request id)).
 
     max_active caps the concurrently decoded requests (at most the runtime's
     max_batch).  With force_mean set, every round's block is rebuilt from the
@@ -51,7 +60,8 @@ class Engine:
     """
 
     def __init__(self, rt: Runtime, max_active: Optional[int] = None, carry_on: bool = True,
-                 force_mean: Optional[float] = None, seed: int = 0):
+                 force_mean: Optional[float] = None, seed: int = 0, temperature: Optional[float] = None,
+                 sample_seed: int = 0):
         torch = rt.torch
         self.rt, self.B, self.carry_on = rt, rt.block, carry_on
         self.max_active = min(max_active or rt.max_batch, rt.max_batch)
@@ -65,6 +75,17 @@ class Engine:
         self.accept, self.committed, self.n_carry = i32(n), i32(n, B), i32(n)
         self.force_mean = force_mean
         self.seed = seed
+        self.temperature = temperature
+        if temperature is not None:
+            if not temperature > 0:
+                raise DFlowError("temperature must be positive (greedy decoding: temperature=None)")
+            if force_mean is not None:
+                raise DFlowError("forced drafts are a greedy-decoding measurement construct")
+            V = rt.dims.vocab
+            self.streams = torch.zeros(n, dtype=torch.int64, device=dev)
+            self.sampler = rt.sampler(temperature, sample_seed, self.streams)
+            self.dl = torch.empty(n * B, V, dtype=torch.float32, device=dev)
+            self.lg = torch.empty(n * B, V, dtype=torch.float32, device=dev)
         self.traj = None
         self.slots: List[Request] = []
         self.queue: deque = deque()
@@ -112,7 +133,12 @@ class Engine:
             req = self.queue.popleft()
             s = len(self.slots)
             tok = torch.from_numpy(req.prompt).to(rt.device)
-            rt.prefill(s, tok, self.anchor[s:s + 1])
+            if self.temperature is None:
+                rt.prefill(s, tok, self.anchor[s:s + 1])
+            else:
+                self.streams[s:s + 1].fill_(req.rid)
+                one = rt.sampler(self.temperature, self.sampler.seed, self.streams[s:s + 1])
+                rt.prefill_sampled(s, tok, one, self.anchor[s:s + 1])
             self.seq_len[s:s + 1].fill_(int(req.prompt.size))
             if req.traj is not None:
                 self._traj_row(s, req.traj)
@@ -154,6 +180,14 @@ class Engine:
 
     def _round(self):
         rt, torch, n = self.rt, self.rt.torch, len(self.slots)
+        if self.temperature is not None:
+            rt.draft_block(n, self.anchor, self.seq_len, self.carry_on, None, None, self.dl)
+            rt.sample_draft(n, self.dl, self.anchor, self.seq_len, self.sampler, self.draft_tok, self.block)
+            rt.verify_block(n, self.block, self.seq_len, None, self.lg)
+            rt.accept_sampled(n, self.block, self.seq_len, self.lg, self.dl, self.sampler, self.accept, self.anchor,
+                              self.committed, self.n_carry)
+            rt.kv_commit(n, self.accept, self.seq_len)
+            return self._collect(n)
         rt.draft_block(n, self.anchor, self.seq_len, self.carry_on, self.draft_tok, self.block)
         if self.force_mean is not None:
             mode, tok = self._force_plan()
@@ -163,6 +197,9 @@ class Engine:
         rt.verify_block(n, self.block, self.seq_len, self.tgt)
         rt.accept_and_carry(n, self.block, self.tgt, self.accept, self.anchor, self.committed, self.n_carry)
         rt.kv_commit(n, self.accept, self.seq_len)
+        self._collect(n)
+
+    def _collect(self, n: int):
         acc = self.accept[:n].cpu().numpy()
         com = self.committed[:n].cpu().numpy()
         for s, req in enumerate(self.slots):
@@ -193,6 +230,8 @@ class Engine:
             self.anchor[s:s + 1].copy_(self.anchor[last:last + 1])
             if self.traj is not None:
                 self.traj[s].copy_(self.traj[last])
+            if self.temperature is not None:
+                self.streams[s:s + 1].copy_(self.streams[last:last + 1])
             rt.move_slot(last, s)
             self.slots[s] = self.slots[last]
         self.slots.pop()

@@ -82,6 +82,8 @@ EXPORTS = {
     "dflow_accept_and_carry": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_prefill_sampled": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                             ctypes.c_int, ctypes.POINTER(Sampler), ctypes.c_void_p]),
     "dflow_sample_draft": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Sampler),
                                           ctypes.c_void_p, ctypes.c_void_p]),
@@ -277,6 +279,12 @@ class Runtime:
     def sampler(temperature: float, seed: int, stream) -> Sampler:
         """stream: device uint64 (torch int64) tensor of per-sequence stream ids, kept alive by the caller."""
         return Sampler(float(temperature), int(seed) & (2**64 - 1), _ptr(stream))
+
+    def prefill_sampled(self, seq: int, tokens, sampler, first_token):
+        """sampler.stream must point at this sequence's one stream id."""
+        self._check(self.lib.dflow_prefill_sampled(self.ctx, _stream(), seq, _ptr(tokens), int(tokens.numel()),
+                                                   ctypes.byref(sampler), _ptr(first_token)),
+                    "dflow_prefill_sampled")
 
     def sample_draft(self, nseq, draft_logits, anchor_tok, anchor_pos, sampler, draft_tok, block_out=None):
         self._check(self.lib.dflow_sample_draft(self.ctx, _stream(), nseq, _ptr(draft_logits), _ptr(anchor_tok),

@@ -178,3 +178,8 @@ def test_engine_rejects_bad_requests():
         forced.submit(np.zeros(10, np.int32), 4)
     with pytest.raises(DFlowError):
         forced.submit(np.zeros(10, np.int32), 4, traj=np.zeros(12, np.int32))
+    for bad in (0.0, -1.0):
+        with pytest.raises(DFlowError):
+            Engine(rt, temperature=bad)
+    with pytest.raises(DFlowError):
+        Engine(rt, temperature=1.0, force_mean=2.0)

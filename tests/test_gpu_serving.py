@@ -14,6 +14,8 @@ row swaps plus dflow_move_slot).  Bars:
 Both with the drafter's own proposals and with forced acceptances (a
 geometric accepted prefix from the oracle's greedy trajectory), which drives
 multi-token commits, truncation at the token budget and non-empty relays.
+Sampling decoding (T > 0) is served too: per-request Philox streams make its
+tokens independent of concurrency as well.
 """
 import numpy as np
 import pytest
@@ -138,3 +140,53 @@ def test_serving_many_slots_invariant(lib):
     rt.close()
     for i, (a, b) in enumerate(zip(outs[1], outs[24])):
         assert a == b, f"request {i}: outputs differ with 1 and 24 slots"
+
+
+def _serve_sampled(name, slots, T, n_req=None, budgets=None):
+    from paper_2609_06498_amd import Runtime
+    from paper_2609_06498_amd.engine import Engine
+    wl, w, o, prompts, trajs = _setup(name)
+    budgets = budgets or MAX_NEW
+    max_ctx = max(len(p) + n for p, n in zip(prompts, budgets)) + 2 * wl.block
+    rt = Runtime(wl.dims, wl.block, SLOTS, max_ctx, w, wl.carry_window)
+    eng = Engine(rt, max_active=slots, temperature=T, sample_seed=11)
+    rids = [eng.submit(p, n) for p, n in zip(prompts, budgets)]
+    outs = eng.run()
+    torch.cuda.synchronize()
+    assert rt.status() == 0
+    stats = {"rounds": eng.rounds, "max_active": max(eng.active_hist),
+             "accepted": sum(r.accepted for r in eng.done.values())}
+    rt.close()
+    return [outs[i] for i in rids], rids, stats
+
+
+@pytest.mark.parametrize("T", [1.0, 0.3])
+def test_serving_sampled(lib, T):
+    """Speculative-sampling serving: a request's tokens are the same at
+    concurrency 1 and 3 (its own Philox stream, batch-invariant logits), its
+    first token is the oracle's draw from the prompt's last row, and the
+    output is not the greedy one."""
+    import oracle.sampling as sp
+    name = "small-bf16"
+    wl, w, o, prompts, trajs = _setup(name)
+    print(f"[serving] {name} sampled T={T}", flush=True)
+    one, rids, _ = _serve_sampled(name, 1, T)
+    many, _, stats = _serve_sampled(name, SLOTS, T)
+    assert stats["max_active"] == SLOTS
+    for i, (a, b) in enumerate(zip(one, many)):
+        assert a == b, f"request {i}: sampled outputs differ at concurrency 1 and {SLOTS}"
+    tol = TOL[wl.dims.dtype]
+    differs = 0
+    for p, n, y, rid, t in zip(prompts, MAX_NEW, many, rids, trajs):
+        assert len(y) == n
+        lg = o.full_logits(p)[-1]
+        inv_t = sp.inv_temperature(T)
+        z = sp.scaled(lg, inv_t)
+        g = sp.gumbel(sp.uniforms(11, rid, len(p) - 1, 0, sp.RESAMPLE, z.size))
+        sc = z + g
+        ref = int(np.argmax(sc))
+        if y[0] != ref:
+            assert sc[ref] - sc[y[0]] <= 2 * tol * float(np.abs(z).max()), f"request {rid}: first token"
+        differs += int(list(y) != list(t[len(p):len(p) + n]))
+    assert differs > 0, "sampled outputs equal the greedy continuation"
+    print(f"[serving] sampled T={T}: rounds {stats['rounds']} accepted {stats['accepted']}", flush=True)
