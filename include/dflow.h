@@ -219,8 +219,8 @@ int dflow_draft_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_
  * anchor followed by the K proposals, at positions start_pos[s]..+K.  Writes
  * the target KV of all B positions (speculatively; kv_commit rolls back the
  * rejected ones), the target argmax per row tgt_argmax [b, B] (lowest id on
- * ties), optional fp32 logits [b, B, vocab] (with logits given, tgt_argmax
- * may be NULL), and the residual outputs of the
+ * ties), optional fp32 logits [b, B, vocab] (tgt_argmax and logits may each
+ * be NULL; with both NULL the LM head is skipped), and the residual outputs of the
  * capture layers, which accept_and_carry projects (hcap: pass NULL to use
  * the internal buffer; otherwise a device [b*B, n_capture*d] copy). */
 int dflow_verify_block(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* block_tok,
@@ -299,6 +299,39 @@ int dflow_accept_sampled(dflow_ctx* ctx, hipStream_t stream, int nseq, const int
                          const int32_t* anchor_pos, const float* logits, const float* draft_logits,
                          const dflow_sampler* smp, int32_t* accept_len, int32_t* bonus, int32_t* committed,
                          int32_t* n_carry, void* feat);
+
+/* ---- Forward-only multi-round rollout (Sec. 4.3, Multi-Round Self-Conditioned
+ * Training, without the optimizer).  From an anchor on a precomputed target
+ * trajectory, round 0 drafts from mask embeddings (dflow_draft_block with
+ * carry_on = 0) and rounds 1..k are reject-conditioned (carry_on = 1); each
+ * round's actual proposals are verified (dflow_verify_block; with tgt_argmax
+ * and logits both NULL the LM head is skipped: the rollout needs only the KV
+ * and the captured states), and the transition to the next round follows
+ * the trajectory, not the verifier: dflow_trajectory_targets writes the
+ * trajectory tokens as the acceptance targets, so dflow_accept_and_carry
+ * finds a = leading drafts equal to the trajectory and takes the trajectory
+ * token at the first mismatch as the next anchor (Sec. 4.3, target
+ * trajectory transition), while the relayed states still come from the
+ * verification of the actual proposals.  kv_commit then keeps the target KV
+ * of the accepted prefix, which equals the trajectory's.
+ *
+ * traj: device int32 [b, traj_stride], row s = sequence s's trajectory
+ * (tokens at absolute positions 0..traj_len-1).  tgt [b, B]: tgt[s][j] =
+ * traj[s][start_pos[s] + j + 1]; a position at or past traj_len gives -1 and
+ * sets DFLOW_STATUS_CAPACITY. */
+int dflow_trajectory_targets(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* traj, int traj_stride,
+                             int traj_len, const int32_t* start_pos, int32_t* tgt);
+
+/* Decayed cross entropy of one round's drafts against the trajectory
+ * (following DFlash, Sec. 4.3): loss[s] = sum_i w_i CE_i / sum_i w_i over
+ * block rows i = 1..K, w_i = exp(-(i-1)/gamma), CE_i = logsumexp(z_i) -
+ * z_i[traj[s][start_pos[s] + i]], z_i the fp32 drafter logits of row s*B + i
+ * in draft_logits [b*B, vocab] (from dflow_draft_block).  The rollout's
+ * objective is the sum of the rounds' losses (eq. dflow_training_objective).
+ * loss: device float [b].  A label outside [0, vocab) or past traj_len sets
+ * DFLOW_STATUS_BAD_TOKEN and is read at the nearest valid id. */
+int dflow_draft_loss(dflow_ctx* ctx, hipStream_t stream, int nseq, const float* draft_logits, const int32_t* traj,
+                     int traj_stride, int traj_len, const int32_t* start_pos, float gamma, float* loss);
 
 /* Serving support (continuous batching keeps the active sequences in slots
  * 0..nseq-1): moves the per-sequence state the library keeps between rounds

@@ -662,7 +662,7 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
                                   const int32_t* start_pos, int32_t* tgt_argmax, float* logits, void* hcap) {
   int rc = check_nseq(c, nseq);
   if (rc) return rc;
-  if (!block_tok || !start_pos || (!tgt_argmax && !logits)) return fail(DFLOW_EINVAL, "verify_block: null argument");
+  if (!block_tok || !start_pos) return fail(DFLOW_EINVAL, "verify_block: null argument");
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
   HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
@@ -730,6 +730,31 @@ extern "C" int dflow_accept_sampled(dflow_ctx* c, hipStream_t st, int nseq, cons
                                committed, n_carry, c->carry_rec, c->status, c->samp, st));
   HIPCHK(project(c, st, M, c->f));
   if (feat) HIPCHK(hipMemcpyAsync(feat, c->f, (size_t)M * d.d * c->elt, hipMemcpyDeviceToDevice, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_trajectory_targets(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* traj,
+                                        int traj_stride, int traj_len, const int32_t* start_pos, int32_t* tgt) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!traj || !start_pos || !tgt) return fail(DFLOW_EINVAL, "trajectory_targets: null argument");
+  if (traj_len < 1 || traj_stride < traj_len) return fail(DFLOW_ESHAPE, "trajectory_targets: len %d stride %d",
+                                                          traj_len, traj_stride);
+  HIPCHK(launch_traj_targets(traj, traj_stride, traj_len, start_pos, nseq, c->dm.block, tgt, c->status, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_draft_loss(dflow_ctx* c, hipStream_t st, int nseq, const float* draft_logits,
+                                const int32_t* traj, int traj_stride, int traj_len, const int32_t* start_pos,
+                                float gamma, float* loss) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!draft_logits || !traj || !start_pos || !loss) return fail(DFLOW_EINVAL, "draft_loss: null argument");
+  if (traj_len < 1 || traj_stride < traj_len) return fail(DFLOW_ESHAPE, "draft_loss: len %d stride %d", traj_len,
+                                                          traj_stride);
+  if (!(gamma > 0.f) || !std::isfinite(gamma)) return fail(DFLOW_EINVAL, "draft_loss: gamma %g", gamma);
+  HIPCHK(launch_draft_loss(draft_logits, c->dm.vocab, nseq, c->dm.block, traj, traj_stride, traj_len, start_pos,
+                           gamma, loss, c->status, c->samp, st));
   return DFLOW_OK;
 }
 

@@ -157,6 +157,11 @@ hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq,
                                int* draft_tok, int* block_out, void* ws, hipStream_t st);
 // first token after a prompt: out[0] ~ softmax(row / T), counter (pos[0], 0, 2, column / 4)
 hipError_t launch_sample_first(const float* row, const SampleArgs& a, int* out, void* ws, hipStream_t st);
+// rollout: trajectory tokens as acceptance targets, and the decayed drafter loss
+hipError_t launch_traj_targets(const int* traj, int stride, int len, const int* start, int nseq, int B, int* tgt,
+                               int* status, hipStream_t st);
+hipError_t launch_draft_loss(const float* dlog, int V, int nseq, int B, const int* traj, int stride, int len,
+                             const int* start, float gamma, float* loss, int* status, void* ws, hipStream_t st);
 // acceptance, correction / bonus draw and the outcome of every sequence
 hipError_t launch_accept_sampled(const float* logits, const float* dlog, const int* block, const SampleArgs& a,
                                  int nseq, int B, int carry_window, int* accept_len, int* bonus, int* committed,

@@ -364,7 +364,104 @@ SampP make_params(const SampleArgs& a, int B) {
   return p;
 }
 
+// ---------------------------------------------------------------- rollout (trajectory transitions, loss)
+// tgt[s * B + j] = traj[s][start[s] + j + 1], j = 0..B-1: with these as the
+// "target predictions", the acceptance scan's a is the number of leading
+// drafts equal to the trajectory and its bonus the trajectory token at the
+// first mismatch.  Past the trajectory's end: -1 and a status bit.
+__global__ void traj_targets_kernel(const int* traj, int stride, int len, const int* start, int nseq, int B,
+                                    int* tgt, int* status) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= nseq * B) return;
+  const int s = e / B, j = e - s * B;
+  const int p = start[s] + j + 1;
+  int v = -1;
+  if (p >= 0 && p < len) v = traj[(size_t)s * stride + p];
+  else set_status(status, ST_CAPACITY);
+  tgt[e] = v;
+}
+
+// one workgroup per sequence: loss[s] = sum_i w_i CE_i / sum_i w_i over drafter
+// rows i = 1..K, CE_i = lse(z_i) - z_i[traj[s][start[s] + i]], w_i = exp(-(i-1)/gamma);
+// the log-sum-exp rows come from lse_part_kernel's chunk partials
+__global__ void __launch_bounds__(256) draft_loss_kernel(const float* dlog, const float* ml, int chunks, int V,
+                                                         int B, const int* traj, int stride, int len,
+                                                         const int* start, float gamma, float* loss,
+                                                         int* status) {
+  __shared__ float ce[64];
+  const int s = blockIdx.x, K = B - 1, tid = threadIdx.x;
+  // label logits first (lane i of wave 0)
+  float zl = 0.f;
+  if (tid >= 1 && tid <= K) {
+    const int p = start[s] + tid;
+    int lab = (p >= 0 && p < len) ? traj[(size_t)s * stride + p] : -1;
+    if (lab < 0 || lab >= V) {
+      set_status(status, ST_BAD_TOKEN);
+      lab = lab < 0 ? 0 : V - 1;
+    }
+    zl = dlog[(size_t)(s * B + tid) * V + lab];
+  }
+  for (int y0 = tid >> 6; y0 < K; y0 += 4 * FOLD_ROWS) {
+    int off[FOLD_ROWS];
+    int n = 0;
+#pragma unroll
+    for (int j = 0; j < FOLD_ROWS; ++j) {
+      const int y = y0 + 4 * j;
+      if (y < K) n = j + 1;
+      off[j] = s * B + 1 + y;
+    }
+    float l[FOLD_ROWS];
+    wave_fold_rows(ml, chunks, off, n, l);
+    if ((tid & 63) == 0) {
+#pragma unroll
+      for (int j = 0; j < FOLD_ROWS; ++j)
+        if (y0 + 4 * j < K) ce[1 + y0 + 4 * j] = l[j];
+    }
+  }
+  __syncthreads();
+  if (tid >= 1 && tid <= K) ce[tid] -= zl;
+  __syncthreads();
+  if (tid == 0) {
+    float num = 0.f, den = 0.f;
+    for (int i = 1; i <= K; ++i) {
+      const float w = expf(-(float)(i - 1) / gamma);
+      num += w * ce[i];
+      den += w;
+    }
+    loss[s] = num / den;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_traj_targets(const int* traj, int stride, int len, const int* start, int nseq, int B, int* tgt,
+                               int* status, hipStream_t st) {
+  if (nseq <= 0) return hipSuccess;
+  const int n = nseq * B;
+  hipLaunchKernelGGL(traj_targets_kernel, dim3((n + 255) / 256), dim3(256), 0, st, traj, stride, len, start, nseq, B,
+                     tgt, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_draft_loss(const float* dlog, int V, int nseq, int B, const int* traj, int stride, int len,
+                             const int* start, float gamma, float* loss, int* status, void* ws, hipStream_t st) {
+  if (nseq <= 0) return hipSuccess;
+  if (B < 2 || B > 64 || V < 4 || (V & 3) || samp_chunks(V) > 64 * FOLD_IT || !(gamma > 0.f))
+    return hipErrorInvalidValue;
+  SampleArgs a;
+  a.inv_t = 1.f;
+  a.seed = 0;
+  a.stream = nullptr;
+  a.pos = nullptr;
+  a.V = V;
+  const SampP p = make_params(a, B);
+  const int R = nseq * B;
+  float* ml = (float*)ws;
+  hipLaunchKernelGGL(lse_part_kernel, dim3(p.chunks, R), dim3(256), 0, st, dlog, dlog, p, R, ml);
+  hipLaunchKernelGGL(draft_loss_kernel, dim3(nseq), dim3(256), 0, st, dlog, ml, p.chunks, V, B, traj, stride, len,
+                     start, gamma, loss, status);
+  return hipGetLastError();
+}
 
 size_t samp_workspace_bytes(int V, int rows, int nseq) {
   const size_t ch = (size_t)samp_chunks(V);

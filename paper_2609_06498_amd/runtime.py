@@ -91,6 +91,11 @@ EXPORTS = {
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.POINTER(Sampler), ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_trajectory_targets": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                                ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_draft_loss": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_float,
+                                        ctypes.c_void_p]),
     "kv_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_qkv_parts": (ctypes.c_int, [ctypes.c_void_p]),
     "dflow_move_slot": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]),
@@ -297,6 +302,16 @@ class Runtime:
                                                   _ptr(logits), _ptr(draft_logits), ctypes.byref(sampler),
                                                   _ptr(accept_len), _ptr(bonus), _ptr(committed), _ptr(n_carry),
                                                   _ptr(feat)), "dflow_accept_sampled")
+
+    def trajectory_targets(self, nseq, traj, traj_len, start_pos, tgt):
+        self._check(self.lib.dflow_trajectory_targets(self.ctx, _stream(), nseq, _ptr(traj), int(traj.shape[1]),
+                                                      int(traj_len), _ptr(start_pos), _ptr(tgt)),
+                    "dflow_trajectory_targets")
+
+    def draft_loss(self, nseq, draft_logits, traj, traj_len, start_pos, gamma, loss):
+        self._check(self.lib.dflow_draft_loss(self.ctx, _stream(), nseq, _ptr(draft_logits), _ptr(traj),
+                                              int(traj.shape[1]), int(traj_len), _ptr(start_pos), float(gamma),
+                                              _ptr(loss)), "dflow_draft_loss")
 
     def kv_commit(self, nseq, accept_len, seq_len):
         self._check(self.lib.kv_commit(self.ctx, _stream(), nseq, _ptr(accept_len), _ptr(seq_len)), "kv_commit")

@@ -5,7 +5,8 @@ anchor token (the previous round's bonus).  One round is
 draft_block -> [measurement-only forcing] -> verify_block ->
 accept_and_carry -> kv_commit; at temperature T > 0 (round_sampled) it is
 draft_block (logits) -> sample_draft -> verify_block (logits) ->
-accept_sampled -> kv_commit.
+accept_sampled -> kv_commit.  A forward-only multi-round rollout (rollout)
+chains rounds whose transitions follow a target trajectory.
 """
 from __future__ import annotations
 
@@ -71,3 +72,28 @@ class Session:
         rt.accept_sampled(b, self.block, self.seq_len, logits, draft_logits, sampler, self.accept, self.anchor,
                           self.committed, self.n_carry, feat)
         rt.kv_commit(b, self.accept, self.seq_len)
+
+    def rollout(self, traj, traj_len: int, k: int, gamma: float, carry_on: bool = True, draft_logits=None,
+                on_round=None):
+        """Forward-only multi-round rollout (Sec. 4.3) from the current state,
+        whose anchors must be traj[s][seq_len[s]] with no carry (a prefill of
+        the trajectory prefix with the anchor set): round 0 from mask
+        embeddings, rounds 1..k reject-conditioned when carry_on; transitions
+        follow the trajectory.  Returns the losses [k + 1, b] (device fp32);
+        their sum over rounds is the objective.  on_round(q) runs after each
+        round's commit."""
+        rt, b, torch = self.rt, self.nseq, self.rt.torch
+        if draft_logits is None:
+            draft_logits = self.logit_buffers()[0]
+        losses = torch.empty(k + 1, b, dtype=torch.float32, device=rt.device)
+        for q in range(k + 1):
+            rt.draft_block(b, self.anchor, self.seq_len, carry_on and q > 0, self.draft_tok, self.block, draft_logits)
+            rt.draft_loss(b, draft_logits, traj, traj_len, self.seq_len, gamma, losses[q])
+            rt.verify_block(b, self.block, self.seq_len, None, None)
+            rt.trajectory_targets(b, traj, traj_len, self.seq_len, self.tgt)
+            rt.accept_and_carry(b, self.block, self.tgt, self.accept, self.anchor, self.committed, self.n_carry)
+            rt.kv_commit(b, self.accept, self.seq_len)
+            if on_round is not None:
+                on_round(q)
+        return losses
+

@@ -57,6 +57,8 @@ def test_validation_errors_without_device(lib):
     assert lib.dflow_qkv_parts(None) == -1
     assert lib.dflow_sample_draft(None, None, 1, None, None, None, None, None, None) == -1
     assert lib.dflow_accept_sampled(None, None, 1, None, None, None, None, None, None, None, None, None, None) == -1
+    assert lib.dflow_trajectory_targets(None, None, 1, None, 8, 8, None, None) == -1
+    assert lib.dflow_draft_loss(None, None, 1, None, None, 8, 8, None, 7.0, None) == -1
     assert lib.dflow_packed_bytes(1, 32, 64) == 32 * 64 * 2
     assert lib.dflow_packed_bytes(0, 32, 64) == 32 * 64 * 4
 
