@@ -26,7 +26,10 @@
  *    and page-table pointers registered at dflow_create must stay valid until
  *    dflow_destroy.  The library allocates its own workspace at create.
  *  - Every call is asynchronous on the given hipStream_t (0 = null stream) and
- *    performs no host synchronisation, except dflow_read_status.
+ *    performs no host synchronisation, except dflow_read_status.  The calls
+ *    on one context share its workspace and per-sequence state, so they must
+ *    execute in order: issue them on one stream (or order the streams with
+ *    events); contexts are independent of each other.
  *  - Return value: DFLOW_OK (0) or a negative DFLOW_E* code; the thread-local
  *    message of the last failure is available from dflow_last_error().  Host-
  *    checkable errors are reported before any launch.  Conditions that depend
