@@ -102,6 +102,36 @@ def gemm_bytes(rt, nseq):
     return verify + draft + accept + commit, launches
 
 
+def measured_stream_peaks():
+    """Streaming rates of plain library kernels on this device, for context
+    next to the published peak: a 1 GiB device copy (read + write bytes) and
+    a 2 GiB fp32 sum (read bytes), each the best of 5 timed runs."""
+    import torch
+    out = {}
+    n = (1 << 30) // 4
+    src = torch.ones(2 * n, dtype=torch.float32, device="cuda")
+    dst = torch.empty(n, dtype=torch.float32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def best(fn, nbytes):
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(5):
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1) * 1e-3)
+        return round(nbytes / min(t) / 1e9, 1)
+
+    out["copy_GB_s"] = best(lambda: dst.copy_(src[:n]), 2 * n * 4)
+    out["sum_read_GB_s"] = best(lambda: src.sum(), 2 * n * 4)
+    del src, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def build_trajectory(rt, sess, prompts, need, sched, B, b):
     """Target trajectory T*: the greedy continuation of every prompt, made by
     junk-draft rounds through the same kernels (each commits at least the
@@ -276,6 +306,10 @@ def main():
                     "algorithmic_bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_s * 1e6, 3),
                     "gemm_family_GB_s": round(lib_bytes / (fam_ms * 1e-3) / 1e9, 1),
                     "gemm_family_ms_per_round": round(fam_ms / kp, 4)}
+        peaks = measured_stream_peaks()
+        roofline["measured_stream_GB_s"] = peaks
+        roofline["frac_of_measured_copy"] = round(achieved / peaks["copy_GB_s"], 4)
+        log(f"stream rates on this device: {peaks}")
         log(f"dominant {roofline['kernel']}: avg {avg_s * 1e6:.2f} us, {achieved:.1f} GB/s; "
             f"gemm family {roofline['gemm_family_GB_s']} GB/s, {fam_ms / kp:.3f} ms/round")
         for k in kernels:
