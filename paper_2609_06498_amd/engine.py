@@ -41,6 +41,7 @@ class Request:
     prompt: np.ndarray
     max_new: int
     traj: Optional[np.ndarray] = None      # forcing trajectory (measurement construct only)
+    stop: Optional[int] = None             # end-of-sequence token: generation ends after it
     out: List[int] = field(default_factory=list)
     rounds: int = 0
     accepted: int = 0                      # drafted tokens accepted over all rounds
@@ -95,7 +96,9 @@ class Engine:
         self.active_hist: List[int] = []
 
     # ------------------------------------------------------------ requests
-    def submit(self, prompt, max_new: int, traj=None) -> int:
+    def submit(self, prompt, max_new: int, traj=None, stop: Optional[int] = None) -> int:
+        """Queues a request: at most max_new generated tokens, fewer when the
+        `stop` token is generated (it is the last output token then)."""
         prompt = np.ascontiguousarray(prompt, dtype=np.int32).reshape(-1)
         if prompt.size < 1 or max_new < 1:
             raise DFlowError("a request needs at least one prompt token and one new token")
@@ -110,7 +113,7 @@ class Engine:
                 raise DFlowError("forcing trajectory shorter than prompt + max_new + block")
         rid = self._next
         self._next += 1
-        self.queue.append(Request(rid, prompt, int(max_new), traj))
+        self.queue.append(Request(rid, prompt, int(max_new), traj, None if stop is None else int(stop)))
         return rid
 
     def run(self) -> Dict[int, List[int]]:
@@ -147,7 +150,7 @@ class Engine:
         if new:
             first = self.anchor[:len(self.slots)].cpu().numpy()
             for s in new:
-                self.slots[s].out.append(int(first[s]))
+                self._emit(self.slots[s], [int(first[s])])
             self._retire()
 
     def _traj_row(self, s: int, traj: np.ndarray):
@@ -204,16 +207,27 @@ class Engine:
         com = self.committed[:n].cpu().numpy()
         for s, req in enumerate(self.slots):
             a = int(acc[s])
-            req.out.extend(int(x) for x in com[s, :a + 1][:req.max_new - len(req.out)])
+            self._emit(req, [int(x) for x in com[s, :a + 1]])
             req.rounds += 1
             req.accepted += a
         self.rounds += 1
         self.active_hist.append(n)
         self._retire()
 
+    def _emit(self, req: Request, toks: List[int]):
+        """Appends committed tokens up to the budget and the stop token."""
+        for x in toks:
+            if self._finished(req):
+                return
+            req.out.append(x)
+
+    @staticmethod
+    def _finished(req: Request) -> bool:
+        return len(req.out) >= req.max_new or (req.stop is not None and bool(req.out) and req.out[-1] == req.stop)
+
     def _retire(self):
         for s in range(len(self.slots) - 1, -1, -1):
-            if len(self.slots[s].out) >= self.slots[s].max_new:
+            if self._finished(self.slots[s]):
                 self._remove(s)
 
     def _remove(self, s: int):

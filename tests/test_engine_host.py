@@ -162,6 +162,26 @@ def test_engine_forced_acceptance_is_greedy():
     assert sum(r.accepted for r in eng.done.values()) > 0
 
 
+@pytest.mark.parametrize("slots", [1, 3])
+def test_engine_stop_token(slots):
+    """A request ends right after its stop token (first occurrence), or at
+    its budget; a stop token absent from the output changes nothing."""
+    prompts = _prompts(6, seed=4)
+    budgets = [40, 40, 40, 5, 40, 1]
+    rt = FakeRuntime(block=8, max_batch=3, max_ctx=300)
+    eng = Engine(rt, max_active=slots)
+    plan = []
+    for i, (p, n) in enumerate(zip(prompts, budgets)):
+        g = toy_greedy(p, n)
+        stop = g[[7, 0, 22, 2, 0, 0][i]] if i != 4 else -5      # -5 never occurs
+        exp = g[:g.index(stop) + 1] if stop in g else g
+        plan.append((eng.submit(p, n, stop=stop), exp))
+    outs = eng.run()
+    for rid, exp in plan:
+        assert outs[rid] == exp, rid
+    assert not eng.slots and not eng.queue
+
+
 def test_engine_rejects_bad_requests():
     rt = FakeRuntime(block=8, max_batch=2, max_ctx=100)
     eng = Engine(rt)
