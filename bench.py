@@ -9,7 +9,13 @@ nothing.  The trajectory is produced beforehand on the GPU by junk-draft
 rounds through the same kernels.  Inputs (weights, KV cache, trajectory,
 schedule) are resident in HBM before the timed region starts.
 
-Prints one JSON line (see README of the metric in the design doc).
+With --temperature T > 0 a step is the sampling-decoding round instead
+(drafts drawn from the drafter, speculative-sampling acceptance), with no
+forcing.
+
+Prints one JSON line: committed tokens/s and ms per round, the dominant
+kernel's HBM roofline (live HIP-event timing, HBM traffic from the recorded
+counter pass) and the CPU oracle timed on a bounded sample of the workload.
 """
 from __future__ import annotations
 
@@ -184,7 +190,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the DFlow round is a single-GPU "
-              f"data-parallel step; multi-GPU sharding is described in DESIGN.md but not run.", file=sys.stderr)
+              f"data-parallel step (sequences shard across GPUs with no exchange); it runs on one GPU only.", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2609_06498_amd import Runtime
