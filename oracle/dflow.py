@@ -44,15 +44,16 @@ import numpy as np
 from . import sampling
 from .model import OracleModel
 
-CARRY_WINDOWS = ("suffix", "suffix+tail")
+CARRY_WINDOWS = ("suffix", "suffix+tail", "suffix-inputs")
 
 
 @dataclass
 class Carry:
-    n: int                      # number of relayed positions (block indices 1..n)
+    n: int                      # number of relayed positions (block indices i0..i0+n-1)
     h: np.ndarray               # [n, d] aligned verifier representations
     bonus: int                  # b, the target correction at the first rejection
     y_rej: int                  # first rejected proposal d_{a+1}
+    i0: int = 1                 # first relayed block index
 
 
 @dataclass
@@ -186,7 +187,7 @@ class OracleDFlow:
         n_relay = 0
         c = s.carry
         if carry_on and c is not None and c.n > 0:
-            x[1:1 + c.n] = self.m.relay(c.bonus, c.y_rej, c.h)
+            x[c.i0:c.i0 + c.n] = self.m.relay(c.bonus, c.y_rej, c.h)
             n_relay = c.n
         return x, n_relay
 
@@ -214,10 +215,16 @@ class OracleDFlow:
 
     def carry_map(self, a: int):
         """(n_c, source block rows) of the relay for acceptance length a.
-        Next-round block index i receives the verify row a+i."""
+        Next-round block index i takes the verify row a+i (the row whose
+        position predicts the index's position); the window picks the rows:
+        'suffix' a+1..K-1 (predictions of the rejected-suffix positions),
+        'suffix+tail' a+1..K (also the prediction after the block),
+        'suffix-inputs' a+2..K (the rows whose inputs are the rejected suffix;
+        index 1 keeps the mask)."""
         K = self.K
-        n = max(0, K - 1 - a) if self.carry_window == "suffix" else max(0, K - a)
-        return n, [a + i for i in range(1, n + 1)]
+        lo, hi = {"suffix": (a + 1, K - 1), "suffix+tail": (a + 1, K), "suffix-inputs": (a + 2, K)}[self.carry_window]
+        rows = list(range(lo, hi + 1))
+        return len(rows), rows
 
     def round(self, s: SeqState, carry_on: bool = True, block: Optional[Sequence[int]] = None,
               force=None, decide: Optional[Sequence[int]] = None) -> RoundResult:
@@ -255,7 +262,8 @@ class OracleDFlow:
         self._append_ctx(s, f[:a + 1])
         s.tokens += committed
         n_c, rows = self.carry_map(a)
-        s.carry = Carry(n_c, f[rows].copy(), committed[-1], int(block[a + 1]) if a < self.K else -1)
+        s.carry = Carry(n_c, f[rows].copy(), committed[-1], int(block[a + 1]) if a < self.K else -1,
+                        rows[0] - a if rows else 1)
         return f, n_c
 
     def round_sampled(self, s: SeqState, temperature: float, seed: int, stream: int, carry_on: bool = True,

@@ -101,14 +101,16 @@ def test_acceptance_brute_force():
         assert s.k[0].shape[0] == s.t and s.F.shape[0] == s.t and s.ck[0].shape[0] == s.t
 
 
-@pytest.mark.parametrize("window", ["suffix", "suffix+tail"])
+@pytest.mark.parametrize("window", ["suffix", "suffix+tail", "suffix-inputs"])
 def test_carry_index_map_against_positions(window):
     """Next-round block index i sits at position t' + i with t' = t + a + 1.
     The drafter predicts the token at its own position; the verifier row at
     position p predicts p + 1.  So index i must take the row at position
     t' + i - 1, i.e. block row a + i, and only rows whose input was a
     verified proposal (index <= K) qualify; 'suffix' additionally requires
-    the predicted position to lie inside the verified block (<= t + K)."""
+    the predicted position to lie inside the verified block (<= t + K), and
+    'suffix-inputs' requires the row's input to be a rejected-suffix token
+    (after the first rejected proposal d_{a+1})."""
     wl, m, o = _setup("fp64", carry_window=window)
     K, t = wl.K, 100
     for a in range(K + 1):
@@ -122,9 +124,11 @@ def test_carry_index_map_against_positions(window):
                 continue
             if window == "suffix" and src_pos + 1 > t + K:
                 continue
+            if window == "suffix-inputs" and row < a + 2:
+                continue
             expect.append((i, row))
         assert n == len(expect)
-        assert [(i + 1, r) for i, r in enumerate(rows)] == expect
+        assert [(r - a, r) for r in rows] == expect
 
 
 @pytest.mark.parametrize("mode", ["fp64", "fp32"])
@@ -191,3 +195,33 @@ def test_forced_block_rule():
     tok = np.array([0, 0, 0, 5, 7, 8, 0, 0])
     blk = forced_block(42, 10, traj, mode, tok, 4096)
     assert list(blk) == [42, 111, 112, (113 + 1 + 5) % 4096, 7, 8, 116, 117]
+
+
+@pytest.mark.parametrize("window", ["suffix", "suffix+tail", "suffix-inputs"])
+def test_relay_window_placement_and_losslessness(window):
+    """The relayed rows land at the block indices the window names (the
+    others keep the mask embedding), the committed stream stays the plain
+    greedy one, and the relay changes the drafts."""
+    wl, m, o = _setup("fp64", carry_window=window)
+    prompt = make_prompts(wl)[0][:40]
+    ref = o.greedy_decode(prompt, 5 * wl.block)
+    traj = np.array(list(prompt) + ref, np.int64)
+    s = o.prefill(prompt)
+    K = wl.K
+    for a in [1, 3, 0, K - 1]:
+        t = s.t
+        block = np.concatenate([[s.anchor], traj[t + 1:t + 1 + a], [(traj[t + 1 + a] + 1) % wl.dims.vocab],
+                                np.zeros(K - a - 1, np.int64)])[:wl.block]
+        rr = o.round(s, True, block=block)
+        assert rr.a == a
+        n, rows = o.carry_map(a)
+        x, n_relay = o.draft_inputs(s, True)
+        idx = [r - a for r in rows]
+        assert n_relay == n and s.carry.i0 == (idx[0] if idx else 1)
+        mask = m.w("draft.e_mask")
+        for i in range(1, wl.block):
+            if i in idx:
+                assert not np.array_equal(x[i], mask), (window, a, i)
+            else:
+                np.testing.assert_array_equal(x[i], mask)
+    assert s.tokens == [int(v) for v in traj[:s.t + 1]]
