@@ -90,12 +90,16 @@ extern "C" {
 #define DFLOW_F32 0
 #define DFLOW_BF16 1
 
-/* Which verifier rows are relayed (Sec. 4.2).  SUFFIX: rows a+1..K-1, i.e.
- * the states that predict the rejected-suffix positions, placed at next-round
- * block indices 1..K-1-a.  SUFFIX_TAIL: rows a+1..K (also the state after the
- * last draft). */
+/* Which verifier rows are relayed (Sec. 4.2).  Next-round block index i takes
+ * verify row a+i (the state at the position before the index's position).
+ * SUFFIX: rows a+1..K-1, the states that predict the rejected-suffix
+ * positions, at indices 1..K-1-a.  SUFFIX_TAIL: rows a+1..K (also the state
+ * after the last draft), at indices 1..K-a.  SUFFIX_INPUTS: rows a+2..K, the
+ * states whose inputs are the rejected suffix, at indices 2..K-a (index 1
+ * keeps the mask embedding). */
 #define DFLOW_CARRY_SUFFIX 0
 #define DFLOW_CARRY_SUFFIX_TAIL 1
+#define DFLOW_CARRY_SUFFIX_INPUTS 2
 
 /* device status bits */
 #define DFLOW_STATUS_BAD_TOKEN 1

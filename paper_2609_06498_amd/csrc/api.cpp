@@ -132,7 +132,8 @@ int validate(const dflow_dims* d) {
   if (d->max_rows < d->block || d->max_rows > MAX_ROWS)
     return fail(DFLOW_ECAPACITY, "max_rows %d (block..%d)", d->max_rows, MAX_ROWS);
   if (d->max_pages < 1 || d->num_pages < 1) return fail(DFLOW_ECAPACITY, "page counts");
-  if (d->carry_window != DFLOW_CARRY_SUFFIX && d->carry_window != DFLOW_CARRY_SUFFIX_TAIL)
+  if (d->carry_window != DFLOW_CARRY_SUFFIX && d->carry_window != DFLOW_CARRY_SUFFIX_TAIL &&
+      d->carry_window != DFLOW_CARRY_SUFFIX_INPUTS)
     return fail(DFLOW_EINVAL, "carry_window %d", d->carry_window);
   return DFLOW_OK;
 }

@@ -312,15 +312,15 @@ hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int ca
 }
 
 // ---------------------------------------------------------------- relay
-// u[s*B + i] = [E(b); E(y_rej); f[s*B + src + i - 1]] for relayed rows 1..n, else 0.
+// u[s*B + i] = [E(b); E(y_rej); f[s*B + rec[1] + i - 1]] for relayed block indices rec[4]..rec[0], else 0.
 // One workgroup per (row, segment), 16-byte copies (d * sizeof(T) is a multiple of 16).
 template <typename T>
 __global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, const T* f, int B, int d, int V, T* u) {
   const int row = blockIdx.x, seg = blockIdx.y;
   const int s = row / B, i = row - s * B;
   const int* r = rec + (size_t)s * CARRY_REC;
-  const bool valid = carry_on && i >= 1 && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B &&
-                     r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
+  const bool valid = carry_on && i >= 1 && i >= r[4] && i <= r[0] && r[0] < B && r[1] >= 1 &&
+                     r[1] + r[0] <= B && r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
   uint4* dst = reinterpret_cast<uint4*>(u + ((size_t)row * 3 + seg) * d);
   const int nvec = d * (int)sizeof(T) / 16;
   if (!valid) {
@@ -362,8 +362,8 @@ __global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const in
   const int nc = d / 16;
   T* xr = x + (size_t)row * d;
   const int* r = rec + (size_t)s * CARRY_REC;
-  const bool relay = i > 0 && carry_on && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B && r[2] >= 0 &&
-                     r[2] < V && r[3] >= 0 && r[3] < V;
+  const bool relay = i > 0 && carry_on && i >= r[4] && i <= r[0] && r[0] < B && r[1] >= 1 && r[1] + r[0] <= B &&
+                     r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
   int src_tok = -1;                  // row 0: the anchor's embedding
   if (i == 0) {
     src_tok = anchor[s];

@@ -16,7 +16,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 _LIB = None
 
 DFLOW_F32, DFLOW_BF16 = 0, 1
-CARRY_WINDOWS = {"suffix": 0, "suffix+tail": 1}
+CARRY_WINDOWS = {"suffix": 0, "suffix+tail": 1, "suffix-inputs": 2}
 PAGE = 64
 
 

@@ -30,10 +30,12 @@ def lib():
     return load_library()
 
 
-def _setup(name):
+def _setup(name, window=None):
     from oracle import Mode, OracleDFlow, OracleModel
     from paper_2609_06498_amd import Runtime
     wl = get_config(name)
+    if window is not None:
+        wl = wl.with_(carry_window=window)
     dm = wl.dims
     w = make_weights(dm, wl.seed_w)
     mode = "fp32" if dm.dtype == "f32" else "bf16"
@@ -49,11 +51,23 @@ def _setup(name):
 @pytest.mark.parametrize("carry_on", [True, False])
 @pytest.mark.parametrize("name", CASES)
 def test_round_parity(lib, name, carry_on):
+    _round_parity(name, carry_on)
+
+
+@pytest.mark.parametrize("window", ["suffix+tail", "suffix-inputs"])
+@pytest.mark.parametrize("name", ["tiny-f32", "small-bf16"])
+def test_round_parity_carry_windows(lib, name, window):
+    """The alternative readings of the relay window (Sec. 4.2) on the device."""
+    _round_parity(name, True, window)
+
+
+def _round_parity(name, carry_on, window=None):
     from paper_2609_06498_amd.session import Session
-    wl, w, o, prompts, sched, need, rt = _setup(name)
+    wl, w, o, prompts, sched, need, rt = _setup(name, window)
     dm, B, K, b, V = wl.dims, wl.block, wl.K, wl.batch, wl.dims.vocab
     tol = TOL[dm.dtype]
-    print(f"[parity] {name} carry_on={carry_on} b={b} ctx={[len(p) for p in prompts]}", flush=True)
+    print(f"[parity] {name} carry_on={carry_on} window={wl.carry_window} b={b} ctx={[len(p) for p in prompts]}",
+          flush=True)
     sess = Session(rt, b)
     states = [o.prefill(p) for p in prompts]
     sess.prefill(prompts)
