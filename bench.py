@@ -55,7 +55,7 @@ def parse():
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 KERNEL_SOURCES = ("paper_2609_06498_amd/csrc/gemm.hip", "paper_2609_06498_amd/csrc/common.h",
-                  "paper_2609_06498_amd/csrc/kernels.h")
+                  "paper_2609_06498_amd/csrc/gemm.h")
 
 
 def kernel_source_digest():

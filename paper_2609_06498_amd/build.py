@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdflow.so")
 SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "sampling.hip", "api.cpp"]
-HEADERS = ["common.h", "kernels.h"]
+HEADERS = ["common.h", "gemm.h", "kernels.h", "round_state.h"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # packed fp32 ops stay off (see the design notes on gfx950 code generation)
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -13,6 +13,7 @@
 #include "../../include/dflow.h"
 #include "common.h"
 #include "kernels.h"
+#include "round_state.h"
 
 using namespace dflow;
 

@@ -4,6 +4,7 @@
 // measurement-only forced-draft builder.
 #include "common.h"
 #include "kernels.h"
+#include "round_state.h"
 
 namespace dflow {
 

@@ -11,7 +11,7 @@
 #include <cmath>
 
 #include "common.h"
-#include "kernels.h"
+#include "gemm.h"
 
 namespace dflow {
 

@@ -3,52 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace dflow {
-
-enum Epi : int {
-  EPI_STORE_T = 0,   // Y = acc                       (storage type)
-  EPI_STORE_F32,     // Y = acc                       (fp32)
-  EPI_RESID,         // Y = R + acc; optional copy Y2 (storage type)
-  EPI_SWIGLU,        // Y = silu(gate) * up           (gate/up tiles interleaved)
-  EPI_BIAS_SILU,     // Y = silu(acc + bias)          (storage type)
-  EPI_BIAS_F32,      // Y = acc + bias                (fp32)
-  EPI_ARGMAX,        // per-row best (value, lowest index) over the group's columns
-  EPI_COUNT
-};
-
-struct GemmParams {
-  const void* A; int lda;           // activations [M, lda], storage type
-  const void* W;                    // packed weight tiles of this column range
-  int M, ntiles, ktiles;            // ntiles = N/16 of the range, ktiles = K/KT
-  void* Y; int ldy;
-  const void* R; int ldr;
-  void* Y2; int ldy2;
-  const void* bias;
-  uint64_t* amax; int amax_ld;      // [workgroup][amax_ld] argmax keys
-  float* logits; int ldl;           // optional fp32 logits
-  int col0;                         // first output column of this range (argmax indices, bias)
-  // RMSNorm row scale (norm = 1): A rows are the raw x, the norm gain is
-  // folded into W, and every output of row m is scaled by rs[m] =
-  // (sum_c ssq[m * ssq_ld + c] / (16 ssq_parts) + eps)^(-1/2).  Rows are
-  // padded: ssq_ld >= max(256, ssq_parts) entries are readable.
-  int norm;
-  const float* ssq; int ssq_ld; int ssq_parts;
-  float eps;
-  // EPI_RESID: per-16-column-strip sums of squares of the stored rows, [m * ssq_out_ld + strip]
-  float* ssq_out; int ssq_out_ld;
-  // EPI_STORE_F32 only: K split into ksplit parts; part h writes its partial
-  // sums at Y + h * y_part (floats), and the consumer adds the parts
-  int ksplit; size_t y_part;
-};
-
-struct GemmShape { int ng; int waves; int groups; };
-GemmShape gemm_shape(int ntiles, int ktiles, int epi, int ksplit = 1);
-int gemm_ksplit(int ntiles, int ktiles, int cus);
-hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
-hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
-                       hipStream_t s);
-
-}  // namespace dflow
+#include "gemm.h"
 
 namespace dflow {
 

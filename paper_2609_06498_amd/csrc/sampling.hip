@@ -27,6 +27,7 @@
 // 149 workgroups.  Chunk partials are folded by one wave per row or sequence.
 #include "common.h"
 #include "kernels.h"
+#include "round_state.h"
 
 #pragma clang fp contract(off)
 
