@@ -335,3 +335,31 @@ def test_first_token_law_on_device(lib):
     pf, pd = pval(first, p0), pval(d1, q1)
     print(f"[sampling] law: chi-square p-values first token {pf:.3g}, first draft {pd:.3g}", flush=True)
     assert pf > 1e-4 and pd > 1e-4
+
+
+def test_sampling_calls_reject_bad_arguments(lib):
+    """Host-checkable errors are reported before any launch."""
+    from paper_2609_06498_amd import DFlowError
+    wl = get_config("tiny-f32")
+    dims, B = wl.dims, wl.block
+    rt = _runtime(dims, B, 2)
+    streams = _streams(2)
+    dl = torch.zeros(2 * B, dims.vocab, dtype=torch.float32, device="cuda")
+    pos, anc = _i32([10, 20]), _i32([1, 2])
+    draft = torch.zeros(2, B - 1, dtype=torch.int32, device="cuda")
+    for T in (0.0, -1.0, float("nan"), float("inf")):
+        with pytest.raises(DFlowError, match="temperature"):
+            rt.sample_draft(2, dl, anc, pos, rt.sampler(T, SEED, streams), draft)
+    with pytest.raises(DFlowError, match="stream"):
+        rt.sample_draft(2, dl, anc, pos, rt.sampler(1.0, SEED, None), draft)
+    with pytest.raises(DFlowError):
+        rt.sample_draft(3, dl, anc, pos, rt.sampler(1.0, SEED, streams), draft)    # nseq > max_batch
+    acc = torch.zeros(2, dtype=torch.int32, device="cuda")
+    com = torch.zeros(2, B, dtype=torch.int32, device="cuda")
+    with pytest.raises(DFlowError, match="null"):
+        rt.accept_sampled(2, draft, pos, None, dl, rt.sampler(1.0, SEED, streams), acc, None, com, None)
+    with pytest.raises(DFlowError, match="gamma"):
+        rt.draft_loss(2, dl, _i32(np.zeros((2, 64))), 64, pos, 0.0, torch.zeros(2, device="cuda"))
+    torch.cuda.synchronize()
+    assert rt.status() == 0
+    rt.close()
