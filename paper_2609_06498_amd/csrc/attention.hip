@@ -513,13 +513,11 @@ template <typename T, int DH, int NW, bool FUSED, int NPART>
 static hipError_t launch_k(const AttnParams& p, hipStream_t st) {
   const size_t lds = attn_lds<T, DH>(FUSED, p.Bq, p.Hq / p.Hkv);
   if (lds > ATTN_LDS_MAX) return hipErrorInvalidConfiguration;
-  static bool lds_set = false;   // allow the largest dynamic LDS once per instantiation
-  if (!lds_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATTN_LDS_MAX);
-    if (e != hipSuccess) return e;
-    lds_set = true;
-  }
+  // allow the largest dynamic LDS, once per instantiation (thread-safe static initialisation)
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)ATTN_LDS_MAX);
+  if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -543,13 +543,12 @@ template <typename T, int EPI, bool NORM, int BS>
 static hipError_t launch_tile_bs(const GemmParams& p, const GemmShape& sh, int ks, int mt, hipStream_t st) {
   const int units = (p.ntiles + BS - 1) / BS * ks;
   const int blocks = (units + 7) / 8 * 8 * mt;
-  static bool lds_set = false;   // the C tile needs more than the default dynamic LDS
-  if (!lds_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_tile_kernel<T, EPI, NORM, BS>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)TILE_LDS);
-    if (e != hipSuccess) return e;
-    lds_set = true;
-  }
+  // the C tile needs more than the default dynamic LDS; set once per
+  // instantiation (thread-safe static initialisation)
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&gemm_tile_kernel<T, EPI, NORM, BS>), hipFuncAttributeMaxDynamicSharedMemorySize,
+      (int)TILE_LDS);
+  if (attr != hipSuccess) return attr;
   const size_t lds = (size_t)TILE_BM * (BS * 16 + 4) * sizeof(float);
   hipLaunchKernelGGL((gemm_tile_kernel<T, EPI, NORM, BS>), dim3(blocks), dim3(256), lds, st, p, sh.waves, mt, units);
   return hipGetLastError();
