@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "committed tokens/s + ms/round, Qwen3-8B-shape B=16; % HBM roofline"
 HBM_PEAK_GBS = 8000.0
+ROLLOUT_GAMMA = 7.0   # decay of the rollout loss over draft positions
 
 
 def parse():
@@ -45,6 +46,9 @@ def parse():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--cpu-sample-ctx", type=int, default=48)
     ap.add_argument("--batch", type=int, default=0, help="override the workload's sequence count (batch sweeps)")
+    ap.add_argument("--rollout", type=int, default=0,
+                    help="k > 0: time forward-only multi-round rollouts (a mask round and k relay rounds, "
+                         "transitions on the target's greedy trajectory); a step is one rollout")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="T > 0: sampling decoding (speculative sampling, the drafter's own samples) instead of "
                          "greedy rounds with forced acceptance")
@@ -86,9 +90,11 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def gemm_bytes(rt, nseq):
+def gemm_bytes(rt, nseq, verify_lm_head=True, relay=True):
     """Algorithmic bytes of every weight-streaming GEMM launch of one round:
-    each weight byte once, the A operand once, the output once."""
+    each weight byte once, the A operand once, the output once.  A rollout
+    round verifies without the LM head; a round without relay runs no relay
+    MLP."""
     dm, B = rt.dims, rt.block
     elt = 2 if dm.dtype == "bf16" else 4
     M = nseq * B
@@ -100,11 +106,11 @@ def gemm_bytes(rt, nseq):
 
     # the QKV projection writes its fp32 partial sums, one per K part
     layer = g(qkv, d, 4 * rt.qkv_parts) + g(d, qd) + g(2 * F, d, n_out=F) + g(d, F)
-    verify = dm.n_layers * layer + g(V, d, 0)
-    draft = dm.n_draft_layers * layer + g(V, d, 0) + g(dm.d_h, 3 * d) + g(2 * d, dm.d_h, 4)
+    verify = dm.n_layers * layer + (g(V, d, 0) if verify_lm_head else 0)
+    draft = dm.n_draft_layers * layer + g(V, d, 0) + ((g(dm.d_h, 3 * d) + g(2 * d, dm.d_h, 4)) if relay else 0)
     accept = g(d, dm.m * d, 4)
     commit = g(dm.n_draft_layers * 2 * kvd, d)   # the drafter layers' context K/V in one GEMM
-    launches = (dm.n_layers + dm.n_draft_layers) * 4 + 2 + 2 + 1 + 1
+    launches = (dm.n_layers + dm.n_draft_layers) * 4 + (2 if verify_lm_head else 1) + (2 if relay else 0) + 1 + 1
     return verify + draft + accept + commit, launches
 
 
@@ -215,8 +221,16 @@ def main():
     P0 = [len(p) for p in prompts]
     max_ctx = max(P0) + max(n - p for n, p in zip(need, P0)) + 9 * B
     sampled = args.temperature > 0
+    kr = args.rollout
+    if sampled and kr > 0:
+        print("--temperature and --rollout are exclusive", file=sys.stderr)
+        sys.exit(2)
     if sampled:   # every timed phase restarts from the prompts and commits at most B tokens per round
         max_ctx = max(P0) + (max(K, args.warmup) + 2) * B
+    if kr > 0:    # rollout rounds advance a + 1 tokens along the trajectory; random drafts match it rarely
+        roll_rounds = max(K, args.warmup) * (kr + 1)
+        need = [p + 2 * roll_rounds + 2 * B for p in P0]
+        max_ctx = max(need) + 10 * B
     t = time.time()
     rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
     torch.cuda.synchronize()
@@ -234,7 +248,16 @@ def main():
         del src, dst
 
     carry_on = args.carry == "on"
-    if sampled:
+    if kr > 0:
+        traj, L, _, _ = build_trajectory(rt, sess, prompts, need, sched, B, b)
+
+        def reset():
+            sess.prefill(prompts)   # the prefill's anchor is the trajectory's token after the prompt
+
+        def run(n):
+            for r in range(n):
+                sess.rollout(traj, L, kr, ROLLOUT_GAMMA, carry_on)
+    elif sampled:
         streams = torch.arange(b, dtype=torch.int64, device="cuda")
         smp = rt.sampler(args.temperature, 1234, streams)
 
@@ -266,21 +289,32 @@ def main():
     dt = time.perf_counter() - t0
     len1 = sess.seq_len.cpu().numpy()
     committed = int((len1 - len0).sum())
-    expect = None if sampled else int((sched["accept"][:K] + 1).sum())
+    expect = None if (sampled or kr > 0) else int((sched["accept"][:K] + 1).sum())
     diverged = expect is not None and committed != expect
     status = rt.status()
     tok_s = committed / dt
     ms_round = dt * 1e3 / K
-    tau = committed / (K * b)
-    log(f"timed {K} rounds: {ms_round:.3f} ms/round, {tok_s:.1f} tok/s, tau {tau:.3f} "
-        + (f"(sampling T={args.temperature})" if sampled else f"(schedule {expect / (K * b):.3f})")
+    rounds_per_step = kr + 1 if kr > 0 else 1
+    tau = committed / (K * b * rounds_per_step)
+    if kr > 0:
+        assert int(len1.max()) + B <= L, "the rollouts ran past the trajectory"
+    log(f"timed {K} {'rollouts' if kr > 0 else 'rounds'}: {ms_round:.3f} ms/step, {tok_s:.1f} tok/s, "
+        f"tau {tau:.3f} per round "
+        + (f"(sampling T={args.temperature})" if sampled else
+           f"(rollout k={kr}, {ms_round / rounds_per_step:.3f} ms/round)" if kr > 0 else
+           f"(schedule {expect / (K * b):.3f})")
         + f", status {status}")
 
     # ---- live per-kernel timing with HIP events on the round's stream
     roofline, kernels = None, None
-    gb, nl = gemm_bytes(rt, b)
+    if kr > 0:   # per rollout: the mask round, then k relay rounds, all verifying without the LM head
+        g0, n0 = gemm_bytes(rt, b, verify_lm_head=False, relay=False)
+        g1, n1 = gemm_bytes(rt, b, verify_lm_head=False, relay=carry_on)
+        gb, nl = g0 + kr * g1, n0 + kr * n1
+    else:
+        gb, nl = gemm_bytes(rt, b, relay=carry_on)
     if not args.no_kernel_timing:
-        kp = min(K, 64)
+        kp = min(K, max(1, 64 // rounds_per_step))   # about 64 rounds: within the library's event record
         reset()
         torch.cuda.synchronize()
         rt.profile(True)
@@ -323,24 +357,27 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, w, prompts, tau, args.cpu_sample_ctx, args.temperature)
+        cpu = cpu_baseline(wl, w, prompts, tau, args.cpu_sample_ctx, args.temperature, kr)
 
     out = {"metric": METRIC, "value": round(tok_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": K,
            "warmup": args.warmup, "ms_per_step": round(ms_round, 4), "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16" if dm.dtype == "bf16" else "f32",
            "data": ("synthetic (seeded random-init weights, uniform prompts, speculative sampling at "
                     f"T={args.temperature} with the drafter's own samples)") if sampled else
+                   ("synthetic (seeded random-init weights, uniform prompts, forward-only rollouts on the "
+                    "target's greedy trajectory with the drafter's own proposals)") if kr > 0 else
                    "synthetic (seeded random-init weights, uniform prompts, forced geometric acceptance)",
            "config": {"workload": wl.name, "batch": b, "block": B, "ctx": list(wl.ctx), "rounds": K,
                       "carry": args.carry,
-                      "schedule": f"sampling T={args.temperature}" if sampled else f"{wl.schedule}({wl.sched_param})",
+                      "schedule": f"sampling T={args.temperature}" if sampled else
+                      f"rollout k={kr}, gamma {ROLLOUT_GAMMA}" if kr > 0 else f"{wl.schedule}({wl.sched_param})",
                       "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
                       "parallelism": "single GPU"},
            "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0):
+def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0, rollout_k=0):
     """The oracle timed on this host on a bounded sample: one full round
     (draft + verify + accept/project + commit, or its sampled form at T > 0)
     of the same model after a short prefill; tokens/s = realised tau of the
@@ -358,13 +395,23 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0):
     rng = np.random.default_rng(0)
     o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))  # carry present
     n_rounds = 3
+    if rollout_k > 0:   # one rollout of k + 1 rounds on a random trajectory (its cost does not depend on the tokens)
+        import oracle.rollout as ro
+        p = prompts[0][:ctx_len]
+        traj = np.concatenate([p, rng.integers(0, dm.vocab, (rollout_k + 1) * wl.block + 2)])
+        st = ro.anchor_state(o, traj, len(p))
+        t = time.perf_counter()
+        ro.rollout(o, st, traj, rollout_k, ROLLOUT_GAMMA)
+        t_round = (time.perf_counter() - t) / (rollout_k + 1)
+        n_rounds = rollout_k + 1
     t = time.perf_counter()
-    for _ in range(n_rounds):
+    for _ in range(n_rounds if rollout_k == 0 else 0):
         if temperature > 0:
             o.round_sampled(s, temperature, 1234, 0, True)
         else:
             o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))
-    t_round = (time.perf_counter() - t) / n_rounds
+    if rollout_k == 0:
+        t_round = (time.perf_counter() - t) / n_rounds
     try:
         import threadpoolctl
         info = threadpoolctl.threadpool_info()
@@ -375,6 +422,7 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0):
     return {"value": round(tau / t_round, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"mean of {n_rounds} {mode} oracle rounds (draft+verify+accept+commit, relay on"
                       + (f", speculative sampling T={temperature}" if temperature > 0 else "")
+                      + (f", one forward-only rollout k={rollout_k}" if rollout_k > 0 else "")
                       + f") of {wl.name} after a "
                       f"{len(p)}-token prefill; tokens/s = GPU-realised tau {tau:.3f} / {t_round:.2f} s; "
                       f"host cpu_count {os.cpu_count()}"}
