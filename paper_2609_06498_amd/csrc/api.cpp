@@ -70,6 +70,7 @@ struct dflow_ctx {
   const void** dknorm;   // device [n_draft_layers] K-norm gain pointers of the drafter layers
   void* samp;            // sampling decoding partials
   float* samp_row;       // [vocab] logits of the last prompt row (dflow_prefill_sampled)
+  float* kpart;          // K-part partial sums of the residual GEMMs above RESID_SPLIT_ROWS rows
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -188,6 +189,11 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
   add(samp_workspace_bytes(d->vocab, mmax, d->max_batch));   // 24 sampling partials (log-sum-exp, draw keys)
   add((size_t)d->vocab * 4);                           // 25 fp32 logits of a prompt's last row (sampled prefill)
+  {                                                    // 26 K-part partial sums of the residual GEMMs (O, down)
+    const int kt = d->dtype == DFLOW_BF16 ? TT<bf16>::KT : TT<float>::KT;
+    const int po = resid_parts(d->d / 16, qd / kt), pd = resid_parts(d->d / 16, d->ffn / kt);
+    add((size_t)(po > pd ? po : pd) * mmax * d->d * 4);
+  }
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
   if (part_items_out) *part_items_out = items;
@@ -283,6 +289,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->dknorm = (const void**)(b + L.off[23]);
   c->samp = b + L.off[24];
   c->samp_row = (float*)(b + L.off[25]);
+  c->kpart = (float*)(b + L.off[26]);
   c->u = c->xn;
   c->hid = c->act;
 
@@ -364,6 +371,7 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
   p.logits = logits;
   p.ldl = ldl;
   p.col0 = 0;
+  p.part_ws = epi == EPI_RESID ? c->kpart : nullptr;
   const bool rec = c->prof && c->n_ev < PROF_MAX;
   if (rec) {
     hipError_t e = hipEventRecord(c->ev0[c->n_ev], st);

@@ -638,9 +638,80 @@ static hipError_t launch_ng(const GemmParams& p, const GemmShape& sh, hipStream_
   return sh.ng == 2 ? launch_mt<T, 2, EPI>(p, sh, st) : launch_mt<T, 1, EPI>(p, sh, st);
 }
 
+// Residual epilogue of the K-split path: one thread per (row, 16-column
+// strip) adds the fp32 parts in part order from +0 -- the order in which the
+// weight-streaming kernel adds its waves' ranges, so each row is bit-identical
+// to that kernel's -- then applies its EPI_RESID epilogue: rnd(sum + R) to Y
+// (and Y2) and the strip's sum of squares of the stored values.
+template <typename T>
+__global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, size_t part_stride, int ks, int M,
+                                                           int N, const T* R, int ldr, T* Y, int ldy, T* Y2, int ldy2,
+                                                           float* ssq_out, int ssq_ld, int strip0) {
+  const int nstrips = N / 16;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= M * nstrips) return;
+  const int m = e / nstrips, j = e - m * nstrips;
+  float s[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) s[c] = 0.f;
+  for (int h = 0; h < ks; ++h) {
+    const float4* src = reinterpret_cast<const float4*>(part + h * part_stride + (size_t)m * N + j * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = src[q];
+      s[4 * q] += v.x;
+      s[4 * q + 1] += v.y;
+      s[4 * q + 2] += v.z;
+      s[4 * q + 3] += v.w;
+    }
+  }
+  float sq = 0.f;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const int col = j * 16 + c;
+    const float v = TT<T>::rnd(s[c] + TT<T>::ld(R, (size_t)m * ldr + col));
+    TT<T>::st(Y, (size_t)m * ldy + col, v);
+    if (Y2) TT<T>::st(Y2, (size_t)m * ldy2 + col, v);
+    sq += v * v;
+  }
+  if (ssq_out) ssq_out[(size_t)m * ssq_ld + strip0 + j] = sq;
+}
+
+int resid_parts(int ntiles, int ktiles) { return gemm_shape(ntiles, ktiles, EPI_RESID, 1).waves; }
+
+// A narrow weight (O, down) at more than RESID_SPLIT_ROWS rows: the weight-
+// streaming kernel would re-read the whole A block from L2 for every strip
+// group, so the tiled kernel computes each of the weight-streaming kernel's K
+// ranges as a part of its own (fp32 partial sums, no row scale), and the
+// reduce kernel adds them and applies the residual epilogue.
+template <typename T>
+static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
+  const int ks = resid_parts(p.ntiles, p.ktiles);
+  GemmParams q = p;
+  q.ksplit = ks;
+  q.Y = p.part_ws;
+  q.ldy = p.ntiles * 16;
+  q.y_part = (size_t)p.M * q.ldy;
+  q.R = nullptr;
+  q.Y2 = nullptr;
+  q.ssq_out = nullptr;
+  q.col0 = 0;
+  GemmShape sh{};
+  sh.waves = 1;   // one K range per part
+  hipError_t e = launch_tile<T, EPI_STORE_F32, false>(q, sh, ks, st);
+  if (e != hipSuccess) return e;
+  const int items = p.M * p.ntiles;
+  hipLaunchKernelGGL(resid_reduce_kernel<T>, dim3((items + 255) / 256), dim3(256), 0, st, p.part_ws, q.y_part, ks,
+                     p.M, q.ldy, reinterpret_cast<const T*>(p.R), p.ldr, reinterpret_cast<T*>(p.Y), p.ldy,
+                     reinterpret_cast<T*>(p.Y2), p.ldy2, p.ssq_out, p.ssq_out_ld, 0);
+  return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  if (epi == EPI_RESID && p.M > RESID_SPLIT_ROWS && p.part_ws && !p.norm && p.col0 == 0)
+    return launch_resid_split<T>(p, st);
   if (ks > 1 && epi != EPI_STORE_F32) return hipErrorInvalidValue;   // only partial fp32 outputs are split
   const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi, ks);
   switch (epi) {
