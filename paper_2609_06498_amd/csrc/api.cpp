@@ -49,6 +49,7 @@ struct dflow_ctx {
   int G, nsplit, part_items;
   int lm_groups;
   int qkv_ks;                // K parts of the QKV projection (fp32 partial sums, added by the consumers)
+  int cus;                   // compute units of the device (launch balance decisions)
 
   dflow_weights w;
   std::vector<dflow_layer> layers, dlayers;
@@ -70,7 +71,7 @@ struct dflow_ctx {
   const void** dknorm;   // device [n_draft_layers] K-norm gain pointers of the drafter layers
   void* samp;            // sampling decoding partials
   float* samp_row;       // [vocab] logits of the last prompt row (dflow_prefill_sampled)
-  float* kpart;          // K-part partial sums of the residual GEMMs above RESID_SPLIT_ROWS rows
+  float* kpart;          // K-part partial sums of the split residual and gate/up GEMMs
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -189,10 +190,13 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
   add(samp_workspace_bytes(d->vocab, mmax, d->max_batch));   // 24 sampling partials (log-sum-exp, draw keys)
   add((size_t)d->vocab * 4);                           // 25 fp32 logits of a prompt's last row (sampled prefill)
-  {                                                    // 26 K-part partial sums of the residual GEMMs (O, down)
+  {   // 26 K-part partial sums of the split GEMMs: residual (O, down) and gate/up up to SWIGLU_SPLIT_MAX_ROWS rows
     const int kt = d->dtype == DFLOW_BF16 ? TT<bf16>::KT : TT<float>::KT;
-    const int po = resid_parts(d->d / 16, qd / kt), pd = resid_parts(d->d / 16, d->ffn / kt);
-    add((size_t)(po > pd ? po : pd) * mmax * d->d * 4);
+    const int po = split_parts(EPI_RESID, d->d / 16, qd / kt), pd = split_parts(EPI_RESID, d->d / 16, d->ffn / kt);
+    const size_t resid = (size_t)(po > pd ? po : pd) * mmax * d->d * 4;
+    const int ps = split_parts(EPI_SWIGLU, 2 * d->ffn / 16, d->d / kt);
+    const size_t swiglu = (size_t)ps * (mmax < SWIGLU_SPLIT_MAX_ROWS ? mmax : SWIGLU_SPLIT_MAX_ROWS) * 2 * d->ffn * 4;
+    add(resid > swiglu ? resid : swiglu);
   }
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
@@ -246,6 +250,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
       return fail(DFLOW_EHIP, "create: no device attributes");
     }
     c->qkv_ks = gemm_ksplit(c->qkv_n / 16, dims->d / c->KT, cus);
+    c->cus = cus;
   }
   c->w = *w;
   c->layers.assign(w->layers, w->layers + dims->n_layers);
@@ -371,7 +376,8 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
   p.logits = logits;
   p.ldl = ldl;
   p.col0 = 0;
-  p.part_ws = epi == EPI_RESID ? c->kpart : nullptr;
+  p.part_ws = (epi == EPI_RESID || epi == EPI_SWIGLU) ? c->kpart : nullptr;
+  p.cus = c->cus;
   const bool rec = c->prof && c->n_ev < PROF_MAX;
   if (rec) {
     hipError_t e = hipEventRecord(c->ev0[c->n_ev], st);

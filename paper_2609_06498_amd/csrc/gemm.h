@@ -39,20 +39,21 @@ struct GemmParams {
   // EPI_STORE_F32 only: K split into ksplit parts; part h writes its partial
   // sums at Y + h * y_part (floats), and the consumer adds the parts
   int ksplit; size_t y_part;
-  // EPI_RESID at more than RESID_SPLIT_ROWS rows: fp32 scratch of
-  // resid_parts(ntiles, ktiles) x M x N floats for the K-part partial sums
-  // (null: no split)
+  // EPI_RESID above SPLIT_MIN_ROWS rows, EPI_SWIGLU from SPLIT_MIN_ROWS + 1
+  // to SWIGLU_SPLIT_MAX_ROWS rows: fp32 scratch of split_parts(epi, ntiles,
+  // ktiles) x M x N floats for the K-part partial sums (null: no split)
   float* part_ws;
+  int cus;                          // compute units (0: unknown, no balance-driven split)
 };
 
-constexpr int RESID_SPLIT_ROWS = 48;
+constexpr int SPLIT_MIN_ROWS = 48, SWIGLU_SPLIT_MAX_ROWS = 256;
 
 struct GemmShape { int ng; int waves; int groups; };
 GemmShape gemm_shape(int ntiles, int ktiles, int epi, int ksplit = 1);
 int gemm_ksplit(int ntiles, int ktiles, int cus);
-// K parts of a residual GEMM above RESID_SPLIT_ROWS rows (the weight-streaming
-// kernel's wave count for (N, K), so every part is one of its K ranges)
-int resid_parts(int ntiles, int ktiles);
+// K parts of a split residual or SwiGLU GEMM (the weight-streaming kernel's
+// wave count for (N, K), so every part is one of its K ranges)
+int split_parts(int epi, int ntiles, int ktiles);
 hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
 hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
                        hipStream_t s);

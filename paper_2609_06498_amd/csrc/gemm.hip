@@ -677,16 +677,82 @@ __global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, si
   if (ssq_out) ssq_out[(size_t)m * ssq_ld + strip0 + j] = sq;
 }
 
-int resid_parts(int ntiles, int ktiles) { return gemm_shape(ntiles, ktiles, EPI_RESID, 1).waves; }
+int split_parts(int epi, int ntiles, int ktiles) { return gemm_shape(ntiles, ktiles, epi, 1).waves; }
 
-// A narrow weight (O, down) at more than RESID_SPLIT_ROWS rows: the weight-
+// SwiGLU epilogue of the K-split path: one thread per (row, 16-column strip of
+// 8 gate + 8 up columns), parts added in part order from +0, then the
+// weight-streaming kernel's epilogue (row scale, silu(gate) * up, rounding).
+// Every 16-lane group computes the row scale (the same value) before any lane
+// leaves.
+template <typename T, bool NORM>
+__global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const float* part, size_t part_stride,
+                                                            int ks, int N) {
+  const int m = blockIdx.y;
+  float rs = 1.f;
+  if constexpr (NORM) rs = norm_row_scale(p, m, threadIdx.x & 15);
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= N / 16) return;
+  float s[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) s[c] = 0.f;
+  for (int h = 0; h < ks; ++h) {
+    const float4* src = reinterpret_cast<const float4*>(part + h * part_stride + (size_t)m * N + j * 16);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 v = src[q];
+      s[4 * q] += v.x;
+      s[4 * q + 1] += v.y;
+      s[4 * q + 2] += v.z;
+      s[4 * q + 3] += v.w;
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    float gt = s[c], up = s[8 + c];
+    if constexpr (NORM) {
+      gt *= rs;
+      up *= rs;
+    }
+    TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + j * 8 + c, silu(gt) * up);
+  }
+}
+
+// The gate/up projection between SPLIT_MIN_ROWS and SWIGLU_SPLIT_MAX_ROWS
+// rows, when K parts (the weight-streaming kernel's ranges) lower the bytes
+// the busiest compute unit streams by a sixth or more: for the 8B shape at
+// 64-256 rows the single-part launch puts two 4-strip workgroups on half the
+// units, the split one two 8-strip half-K workgroups on every unit (a third
+// fewer bytes each, against the parts' round trip).
+template <typename T>
+static hipError_t launch_swiglu_split(const GemmParams& p, hipStream_t st) {
+  const int ks = split_parts(EPI_SWIGLU, p.ntiles, p.ktiles);
+  GemmParams q = p;
+  q.ksplit = ks;
+  q.norm = 0;
+  q.Y = p.part_ws;
+  q.ldy = p.ntiles * 16;
+  q.y_part = (size_t)p.M * q.ldy;
+  q.col0 = 0;
+  GemmShape sh{};
+  sh.waves = 1;   // one K range per part
+  hipError_t e = launch_tile<T, EPI_STORE_F32, false>(q, sh, ks, st);
+  if (e != hipSuccess) return e;
+  const dim3 grid((p.ntiles + 255) / 256, p.M);
+  if (p.norm)
+    hipLaunchKernelGGL((swiglu_reduce_kernel<T, true>), grid, dim3(256), 0, st, p, p.part_ws, q.y_part, ks, q.ldy);
+  else
+    hipLaunchKernelGGL((swiglu_reduce_kernel<T, false>), grid, dim3(256), 0, st, p, p.part_ws, q.y_part, ks, q.ldy);
+  return hipGetLastError();
+}
+
+// A narrow weight (O, down) at more than SPLIT_MIN_ROWS rows: the weight-
 // streaming kernel would re-read the whole A block from L2 for every strip
 // group, so the tiled kernel computes each of the weight-streaming kernel's K
 // ranges as a part of its own (fp32 partial sums, no row scale), and the
 // reduce kernel adds them and applies the residual epilogue.
 template <typename T>
 static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
-  const int ks = resid_parts(p.ntiles, p.ktiles);
+  const int ks = split_parts(EPI_RESID, p.ntiles, p.ktiles);
   GemmParams q = p;
   q.ksplit = ks;
   q.Y = p.part_ws;
@@ -707,11 +773,36 @@ static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Bytes the busiest compute unit streams in a tiled launch with ks K parts:
+// workgroups per unit (rounded up) x (A and W bytes of one workgroup's k
+// tiles), with the strip count launch_tile would pick.
+static double tile_unit_bytes(int ntiles, int ktiles, int M, int ks, int cus, int kt_bytes) {
+  const int mt = (M + TILE_BM - 1) / TILE_BM;
+  const int bs = (ntiles + TILE_BS - 1) / TILE_BS * ks * mt < 256 ? 4 : 8;
+  const long long wgs = (long long)((ntiles + bs - 1) / bs) * ks * mt;
+  const int kpart = (ktiles + ks - 1) / ks;
+  const double per_wg = (double)kpart * (TILE_BM + bs * 16) * kt_bytes;
+  return (double)((wgs + cus - 1) / cus) * per_wg;
+}
+
+template <typename T>
+static bool swiglu_split_pays(const GemmParams& p) {
+  if (p.cus < 1) return false;
+  const int ks = split_parts(EPI_SWIGLU, p.ntiles, p.ktiles);
+  if (ks < 2) return false;
+  const int ktb = TT<T>::KT * (int)sizeof(T);   // bytes of one row's k tile
+  return tile_unit_bytes(p.ntiles, p.ktiles, p.M, ks, p.cus, ktb) <
+         (5.0 / 6.0) * tile_unit_bytes(p.ntiles, p.ktiles, p.M, 1, p.cus, ktb);
+}
+
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   const int ks = p.ksplit > 1 ? p.ksplit : 1;
-  if (epi == EPI_RESID && p.M > RESID_SPLIT_ROWS && p.part_ws && !p.norm && p.col0 == 0)
+  if (epi == EPI_RESID && p.M > SPLIT_MIN_ROWS && p.part_ws && !p.norm && p.col0 == 0)
     return launch_resid_split<T>(p, st);
+  if (epi == EPI_SWIGLU && p.M > SPLIT_MIN_ROWS && p.M <= SWIGLU_SPLIT_MAX_ROWS && p.part_ws && p.col0 == 0 &&
+      swiglu_split_pays<T>(p))
+    return launch_swiglu_split<T>(p, st);
   if (ks > 1 && epi != EPI_STORE_F32) return hipErrorInvalidValue;   // only partial fp32 outputs are split
   const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi, ks);
   switch (epi) {
