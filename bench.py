@@ -58,30 +58,23 @@ def parse():
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
-KERNEL_SOURCES = ("paper_2609_06498_amd/csrc/gemm.hip", "paper_2609_06498_amd/csrc/common.h",
-                  "paper_2609_06498_amd/csrc/gemm.h")
-
-
-def kernel_source_digest():
-    import hashlib
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()
 
 
 def measured_traffic(kernel_name):
     """HBM bytes per launch of the dominant kernel from the committed counter
     record (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading
     for a copy of known size), or None when the record is absent, is for
-    another kernel, or the GEMM sources changed since it was taken."""
+    another kernel, or the kernel's machine code in the loaded library differs
+    from the code the counters were taken on."""
+    from paper_2609_06498_amd import library_path
+    from paper_2609_06498_amd.codeobj import kernel_code_digest
     try:
         with open(TRAFFIC_FILE) as fh:
             rec = json.load(fh)
-    except (OSError, ValueError):
-        return None
-    if rec.get("kernel") != kernel_name or rec.get("source_sha256") != kernel_source_digest():
+        if rec.get("kernel") != kernel_name or \
+                rec.get("code_sha256") != kernel_code_digest(library_path(), rec.get("symbol", "")):
+            return None
+    except (OSError, ValueError, KeyError):
         return None
     return int(rec["fetch_bytes"] + rec["write_bytes"])
 
