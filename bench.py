@@ -58,6 +58,7 @@ def parse():
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+NSEG = 4   # timed segments (median and min per-step time besides the whole-run value)
 
 
 def measured_traffic(kernel_name):
@@ -247,8 +248,8 @@ def main():
         def reset():
             sess.prefill(prompts)   # the prefill's anchor is the trajectory's token after the prompt
 
-        def run(n):
-            for r in range(n):
+        def run(n, r0=0):
+            for r in range(r0, r0 + n):
                 sess.rollout(traj, L, kr, ROLLOUT_GAMMA, carry_on)
     elif sampled:
         streams = torch.arange(b, dtype=torch.int64, device="cuda")
@@ -257,8 +258,8 @@ def main():
         def reset():
             sess.prefill(prompts)
 
-        def run(n):
-            for r in range(n):
+        def run(n, r0=0):
+            for r in range(r0, r0 + n):
                 sess.round_sampled(smp, carry_on)
     else:
         traj, L, mode_d, tok_d = build_trajectory(rt, sess, prompts, need, sched, B, b)
@@ -266,8 +267,8 @@ def main():
         def reset():
             sess.prefill(prompts)
 
-        def run(n):
-            for r in range(n):
+        def run(n, r0=0):
+            for r in range(r0, r0 + n):
                 sess.round(carry_on, force=(traj, L, mode_d[r], tok_d[r]))
 
     reset()
@@ -276,10 +277,18 @@ def main():
     reset()
     torch.cuda.synchronize()
     len0 = sess.seq_len.cpu().numpy().copy()
+    # the K timed steps in NSEG consecutive segments, each bracketed by HIP
+    # events on the round stream (no synchronisation inside the timed region)
+    nseg = NSEG if K % NSEG == 0 and K >= 2 * NSEG else 1
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(nseg + 1)]
     t0 = time.perf_counter()
-    run(K)
+    ev[0].record()
+    for i in range(nseg):
+        run(K // nseg, i * K // nseg)
+        ev[i + 1].record()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    seg_ms = [ev[i].elapsed_time(ev[i + 1]) / (K // nseg) for i in range(nseg)]
     len1 = sess.seq_len.cpu().numpy()
     committed = int((len1 - len0).sum())
     expect = None if (sampled or kr > 0) else int((sched["accept"][:K] + 1).sum())
@@ -296,7 +305,7 @@ def main():
         + (f"(sampling T={args.temperature})" if sampled else
            f"(rollout k={kr}, {ms_round / rounds_per_step:.3f} ms/round)" if kr > 0 else
            f"(schedule {expect / (K * b):.3f})")
-        + f", status {status}")
+        + f", status {status}; {nseg} segments: median {np.median(seg_ms):.3f}, min {min(seg_ms):.3f} ms/step")
 
     # ---- live per-kernel timing with HIP events on the round's stream
     roofline, kernels = None, None
@@ -366,6 +375,8 @@ def main():
                       f"rollout k={kr}, gamma {ROLLOUT_GAMMA}" if kr > 0 else f"{wl.schedule}({wl.sched_param})",
                       "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
                       "parallelism": "single GPU"},
+           "segments_ms_per_step": {"n": nseg, "each": [round(x, 4) for x in seg_ms],
+                                    "median": round(float(np.median(seg_ms)), 4), "min": round(min(seg_ms), 4)},
            "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
     print(json.dumps(out), flush=True)
 
