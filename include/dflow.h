@@ -360,8 +360,11 @@ int dflow_bench_force_drafts(dflow_ctx* ctx, hipStream_t stream, int nseq, const
 
 /* Kernel timing (tracing aid, not part of the method).  While enabled, every
  * weight-streaming GEMM launch and every attention launch is bracketed by HIP
- * events recorded on the launch's stream (up to 16384 launches between reads).
- * dflow_profile_read waits for the recorded events and aggregates them per
+ * events recorded on the launch's stream (up to 16384 launches between reads;
+ * timing-only events, created without the system-scope fence, so a record
+ * adds no cache writeback to the launch it brackets).  Synchronise the
+ * stream before reading.  dflow_profile_read waits for the recorded events
+ * and aggregates them per
  * kernel class (GEMM epilogue and shape, or attention): summed elapsed
  * milliseconds, launches and algorithmic bytes (GEMM: each weight, input and
  * output byte once; attention: 0, its key count is device-resident).  Writes

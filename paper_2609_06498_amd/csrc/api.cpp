@@ -818,9 +818,11 @@ extern "C" int dflow_profile(dflow_ctx* c, int enable) {
     c->ev0.resize(PROF_MAX);
     c->ev1.resize(PROF_MAX);
     c->ev_rec.resize(PROF_MAX);
+    // timing-only events: no system-scope fence (cache writeback and
+    // invalidation) at each record, which would lengthen the bracketed launch
     for (int i = 0; i < PROF_MAX; ++i) {
-      HIPCHK(hipEventCreate(&c->ev0[i]));
-      HIPCHK(hipEventCreate(&c->ev1[i]));
+      HIPCHK(hipEventCreateWithFlags(&c->ev0[i], hipEventDisableSystemFence));
+      HIPCHK(hipEventCreateWithFlags(&c->ev1[i], hipEventDisableSystemFence));
     }
   }
   c->prof = enable != 0;
