@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "committed tokens/s + ms/round, Qwen3-8B-shape B=16; % HBM roofline"
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # dense matrix-core peaks of the MI355X
 ROLLOUT_GAMMA = 7.0   # decay of the rollout loss over draft positions
 
 
@@ -335,6 +336,8 @@ def main():
                  "avg_us": round(avg_us, 3), "ms_per_round": round(e["ms"] / kp, 4)}
             if e["bytes"]:
                 k["GB_s"] = round(e["bytes"] / e["launches"] / (avg_us * 1e-6) / 1e9, 1)
+            if e["name"].startswith("gemm"):   # matrix-core rate: 2 M N K flops per launch
+                k["TFLOP_s"] = round(2.0 * e["M"] * e["N"] * e["K"] / (avg_us * 1e-6) / 1e12, 2)
             kernels.append(k)
         dom = max(gemms, key=lambda e: e["ms"])
         avg_s = dom["ms"] * 1e-3 / dom["launches"]
@@ -348,6 +351,9 @@ def main():
                     "algorithmic_bytes_per_launch": int(per_launch), "avg_launch_us": round(avg_s * 1e6, 3),
                     "gemm_family_GB_s": round(lib_bytes / (fam_ms * 1e-3) / 1e9, 1),
                     "gemm_family_ms_per_round": round(fam_ms / kp, 4)}
+        tflops = 2.0 * dom["M"] * dom["N"] * dom["K"] / avg_s / 1e12     # the secondary (matrix-core) bound
+        roofline["mfma_TFLOP_s"] = round(tflops, 2)
+        roofline["mfma_frac"] = round(tflops / MFMA_PEAK_TFLOPS[dm.dtype], 4)
         peaks = measured_stream_peaks()
         roofline["measured_stream_GB_s"] = peaks
         roofline["frac_of_measured_copy"] = round(achieved / peaks["copy_GB_s"], 4)
