@@ -361,7 +361,10 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   }
 
   // staging: A chunk c (row c/4, quarter c%4 of its KT values) goes to the
-  // fragment slot of its m tile; W chunk c is lane c%64 of strip c/64
+  // fragment slot of its m tile, XOR-swizzled within the quarter's 16 slots
+  // (slot q*16 + (r ^ 2q)) so that the eight lanes of one 16-byte LDS write
+  // pass (two rows x four quarters) hit distinct banks; the reader undoes the
+  // swizzle.  W chunk c is lane c%64 of strip c/64.
   u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [buffer][8 m tiles][64]
   u32x4_t* sw = sa + 2 * 512;                                 // [buffer][BS strips][64]
   const gu4* asrc[2];
@@ -372,7 +375,7 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     const int c = threadIdx.x + 256 * i;
     const int r = c >> 2, q = c & 3;
     asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
-    adst[i] = (r >> 4) * 64 + q * 16 + (r & 15);
+    adst[i] = (r >> 4) * 64 + q * 16 + ((r & 15) ^ (2 * q));
   }
 #pragma unroll
   for (int i = 0; i < NWC; ++i) {
@@ -414,8 +417,9 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   };
   auto compute = [&](int buf) {
     u32x4_t a[4], b[WS];
+    const int aslot = (lane & 48) | ((lane & 15) ^ (2 * (lane >> 4)));   // fragment lane -> swizzled slot
 #pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = sa[buf * 512 + (wm * 4 + i) * 64 + lane];
+    for (int i = 0; i < 4; ++i) a[i] = sa[buf * 512 + (wm * 4 + i) * 64 + aslot];
 #pragma unroll
     for (int j = 0; j < WS; ++j) b[j] = sw[buf * BS * 64 + (wn * WS + j) * 64 + lane];
 #pragma unroll
