@@ -190,13 +190,26 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)(d->n_draft_layers > 0 ? d->n_draft_layers : 1) * sizeof(void*));   // 23 drafter K-norm gain pointers
   add(samp_workspace_bytes(d->vocab, mmax, d->max_batch));   // 24 sampling partials (log-sum-exp, draw keys)
   add((size_t)d->vocab * 4);                           // 25 fp32 logits of a prompt's last row (sampled prefill)
-  {   // 26 K-part partial sums of the split GEMMs: residual (O, down) and gate/up up to SWIGLU_SPLIT_MAX_ROWS rows
+  {   // 26 K-part partial sums of the split GEMMs: residual (O, down), gate/up and the range-split projections
     const int kt = d->dtype == DFLOW_BF16 ? TT<bf16>::KT : TT<float>::KT;
     const int po = split_parts(EPI_RESID, d->d / 16, qd / kt), pd = split_parts(EPI_RESID, d->d / 16, d->ffn / kt);
     const size_t resid = (size_t)(po > pd ? po : pd) * mmax * d->d * 4;
     const int ps = split_parts(EPI_SWIGLU, 2 * d->ffn / 16, d->d / kt);
-    const size_t swiglu = (size_t)ps * (mmax < SWIGLU_SPLIT_MAX_ROWS ? mmax : SWIGLU_SPLIT_MAX_ROWS) * 2 * d->ffn * 4;
-    add(resid > swiglu ? resid : swiglu);
+    const size_t rows_split = mmax < SWIGLU_SPLIT_MAX_ROWS ? mmax : SWIGLU_SPLIT_MAX_ROWS;
+    const size_t swiglu = (size_t)ps * rows_split * 2 * d->ffn * 4;
+    size_t need = resid > swiglu ? resid : swiglu;
+    // range split of the narrow plain / fp32 / bias projections: QKV (when in
+    // one part), W_c, drafter context K/V, relay MLP
+    const int nc = d->n_draft_layers * 2 * kvd;
+    const int rs_epi[5] = {EPI_STORE_F32, EPI_STORE_F32, EPI_STORE_T, EPI_BIAS_SILU, EPI_BIAS_F32};
+    const int rs_n[5] = {qkvn, d->d, nc, d->relay_hidden, 2 * d->d};
+    const int rs_k[5] = {d->d, d->n_capture * d->d, d->d, 3 * d->d, d->relay_hidden};
+    for (int i = 0; i < 5; ++i) {
+      if (rs_n[i] <= 0 || rs_k[i] <= 0) continue;
+      const size_t r = (size_t)split_parts(rs_epi[i], rs_n[i] / 16, rs_k[i] / kt) * rows_split * rs_n[i] * 4;
+      if (r > need) need = r;
+    }
+    add(need);
   }
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
@@ -376,7 +389,8 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
   p.logits = logits;
   p.ldl = ldl;
   p.col0 = 0;
-  p.part_ws = (epi == EPI_RESID || epi == EPI_SWIGLU) ? c->kpart : nullptr;
+  p.part_ws = (epi == EPI_RESID || epi == EPI_SWIGLU || range_split_applies(epi, M, N / 16, ksplit)) ? c->kpart
+                                                                                                    : nullptr;
   p.cus = c->cus;
   const bool rec = c->prof && c->n_ev < PROF_MAX;
   if (rec) {

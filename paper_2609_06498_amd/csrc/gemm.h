@@ -41,7 +41,9 @@ struct GemmParams {
   int ksplit; size_t y_part;
   // EPI_RESID above SPLIT_MIN_ROWS rows, EPI_SWIGLU from SPLIT_MIN_ROWS + 1
   // to SWIGLU_SPLIT_MAX_ROWS rows: fp32 scratch of split_parts(epi, ntiles,
-  // ktiles) x M x N floats for the K-part partial sums (null: no split)
+  // ktiles) x M x N floats for the K-part partial sums; the narrow plain,
+  // fp32 and bias projections under range_split_applies the same (null: no
+  // split)
   float* part_ws;
   int cus;                          // compute units (0: unknown, no balance-driven split)
 };
@@ -54,6 +56,11 @@ int gemm_ksplit(int ntiles, int ktiles, int cus);
 // K parts of a split residual or SwiGLU GEMM (the weight-streaming kernel's
 // wave count for (N, K), so every part is one of its K ranges)
 int split_parts(int epi, int ntiles, int ktiles);
+// Whether a plain, fp32, bias + SiLU or bias projection (no K parts) of M rows
+// takes the range split: SPLIT_MIN_ROWS < M <= SWIGLU_SPLIT_MAX_ROWS and a
+// weight too narrow for the tiled kernel's workgroup count; it needs
+// split_parts(epi, ntiles, ktiles) x M x N floats of part_ws
+bool range_split_applies(int epi, int M, int ntiles, int ksplit);
 hipError_t launch_gemm(bool bf16, int epi, const GemmParams& p, hipStream_t s);
 hipError_t launch_pack(bool bf16, const void* w, int N, int K, int gate_up, const void* col_gain, void* out,
                        hipStream_t s);

@@ -777,6 +777,95 @@ static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Range split of the narrow drafter-side projections (W_c, relay MLP,
+// drafter context K/V: plain, fp32, bias + SiLU and bias epilogues) between
+// SPLIT_MIN_ROWS + 1 and SWIGLU_SPLIT_MAX_ROWS rows, where a tiled launch
+// would have too few workgroups and the weight-streaming kernel re-reads the
+// whole A block for every strip group: the tiled kernel computes each of the
+// weight-streaming kernel's wave ranges as a part of its own, and this kernel
+// folds the parts in range order from +0 -- that kernel's wave fold -- and
+// applies its epilogue.  One workgroup row per output row (every 16-lane group
+// computes the row scale); four columns per thread.
+template <typename T, int EPI, bool NORM>
+__global__ void __launch_bounds__(256) range_reduce_kernel(GemmParams p, const float* part, size_t part_stride,
+                                                           int nw, int N) {
+  const int m = blockIdx.y;
+  float rs = 1.f;
+  if constexpr (NORM) rs = norm_row_scale(p, m, threadIdx.x & 15);
+  const int c4 = blockIdx.x * 256 + threadIdx.x;
+  if (c4 >= N / 4) return;
+  float s[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int w = 0; w < nw; ++w) {
+    const float4 v = *reinterpret_cast<const float4*>(part + (size_t)w * part_stride + (size_t)m * N + 4 * c4);
+    s[0] += v.x;
+    s[1] += v.y;
+    s[2] += v.z;
+    s[3] += v.w;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int col = 4 * c4 + i;
+    float v = s[i];
+    if constexpr (NORM) v *= rs;
+    if constexpr (EPI == EPI_STORE_T) {
+      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
+    } else if constexpr (EPI == EPI_STORE_F32) {
+      reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
+    } else if constexpr (EPI == EPI_BIAS_SILU) {
+      v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, silu(v));
+    } else if constexpr (EPI == EPI_BIAS_F32) {
+      v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+      reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
+    }
+  }
+}
+
+bool range_split_applies(int epi, int M, int ntiles, int ksplit) {
+  return (epi == EPI_STORE_T || epi == EPI_STORE_F32 || epi == EPI_BIAS_SILU || epi == EPI_BIAS_F32) &&
+         ksplit <= 1 && M > SPLIT_MIN_ROWS && M <= SWIGLU_SPLIT_MAX_ROWS && (ntiles + TILE_BS - 1) / TILE_BS < 96;
+}
+
+template <typename T, int EPI, bool NORM>
+static hipError_t launch_range_reduce(const GemmParams& p, size_t part_stride, int nw, int N, hipStream_t st) {
+  const dim3 grid((N / 4 + 255) / 256, p.M);
+  hipLaunchKernelGGL((range_reduce_kernel<T, EPI, NORM>), grid, dim3(256), 0, st, p, p.part_ws, part_stride, nw, N);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_range_split(int epi, const GemmParams& p, hipStream_t st) {
+  const int nw = split_parts(epi, p.ntiles, p.ktiles);
+  GemmParams q = p;
+  q.ksplit = nw;
+  q.norm = 0;
+  q.Y = p.part_ws;
+  q.ldy = p.ntiles * 16;
+  q.y_part = (size_t)p.M * q.ldy;
+  q.R = nullptr;
+  q.Y2 = nullptr;
+  q.ssq_out = nullptr;
+  q.col0 = 0;
+  GemmShape sh{};
+  sh.waves = 1;   // one range per part
+  hipError_t e = launch_tile<T, EPI_STORE_F32, false>(q, sh, nw, st);
+  if (e != hipSuccess) return e;
+  const bool n = p.norm != 0;
+  switch (epi) {
+    case EPI_STORE_T:
+      return n ? launch_range_reduce<T, EPI_STORE_T, true>(p, q.y_part, nw, q.ldy, st)
+               : launch_range_reduce<T, EPI_STORE_T, false>(p, q.y_part, nw, q.ldy, st);
+    case EPI_STORE_F32:
+      return n ? launch_range_reduce<T, EPI_STORE_F32, true>(p, q.y_part, nw, q.ldy, st)
+               : launch_range_reduce<T, EPI_STORE_F32, false>(p, q.y_part, nw, q.ldy, st);
+    case EPI_BIAS_SILU:
+      return n ? hipErrorInvalidValue : launch_range_reduce<T, EPI_BIAS_SILU, false>(p, q.y_part, nw, q.ldy, st);
+    case EPI_BIAS_F32:
+      return n ? hipErrorInvalidValue : launch_range_reduce<T, EPI_BIAS_F32, false>(p, q.y_part, nw, q.ldy, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 // Bytes the busiest compute unit streams in a tiled launch with ks K parts:
 // workgroups per unit (rounded up) x (A and W bytes of one workgroup's k
 // tiles), with the strip count launch_tile would pick.
@@ -807,6 +896,7 @@ static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   if (epi == EPI_SWIGLU && p.M > SPLIT_MIN_ROWS && p.M <= SWIGLU_SPLIT_MAX_ROWS && p.part_ws && p.col0 == 0 &&
       swiglu_split_pays<T>(p))
     return launch_swiglu_split<T>(p, st);
+  if (p.part_ws && p.col0 == 0 && range_split_applies(epi, p.M, p.ntiles, ks)) return launch_range_split<T>(epi, p, st);
   if (ks > 1 && epi != EPI_STORE_F32) return hipErrorInvalidValue;   // only partial fp32 outputs are split
   const GemmShape sh = gemm_shape(p.ntiles, p.ktiles, epi, ks);
   switch (epi) {
