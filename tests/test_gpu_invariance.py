@@ -5,7 +5,9 @@
 * qwen3-32b: the Qwen3-32B shape (64 + 5 layers, d 5120, GQA group 8),
   4 sequences of 16384 positions;
 * small-bf16-b24: 24 sequences, M = 384 rows, so the batched run takes the
-  tiled GEMM and each sequence alone the weight-streaming one.
+  tiled GEMM and each sequence alone the weight-streaming one; the same model
+  at 4 and 16 sequences (M = 64 and 256, the first row counts above and the
+  last row count within the K-split and range-split paths).
 
 Batch invariance: every kernel's arithmetic for a row depends only on that
 row's own data (K reductions split by (N, K) only, attention splits at fixed
@@ -30,13 +32,17 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("name, rounds, alone", [("qwen3-8b-b8", 3, "extremes"), ("qwen3-32b", 2, "extremes"),
-                                                 ("small-bf16-b24", 3, "all")])
+                                                 ("small-bf16-b24", 3, "all"), ("small-bf16-b24@4", 3, "all"),
+                                                 ("small-bf16-b24@16", 2, "extremes")])
 def test_batch_invariance(name, rounds, alone):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2609_06498_amd import Runtime
     from paper_2609_06498_amd.session import Session
-    wl = get_config(name)
+    base, _, nb = name.partition("@")
+    wl = get_config(base)
+    if nb:   # the same workload at another sequence count
+        wl = wl.with_(name=name, batch=int(nb))
     dm, B, b, V = wl.dims, wl.block, wl.batch, wl.dims.vocab
     prompts = make_prompts(wl)
     sched = make_schedule(wl, rounds)
