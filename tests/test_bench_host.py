@@ -1,0 +1,55 @@
+"""bench.py's host-side contract (CPU only): the multi-GPU refusal, the
+counter record lookup and the algorithmic byte model of the round."""
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_counter_record_is_keyed_to_the_kernel():
+    with open(bench.TRAFFIC_FILE) as fh:
+        rec = json.load(fh)
+    assert bench.measured_traffic("gemm.swiglu N=1 K=1 M=1") is None     # another kernel: no record
+    t = bench.measured_traffic(rec["kernel"])
+    if t is not None:                                                     # the built library's code matches
+        assert t == rec["fetch_bytes"] + rec["write_bytes"]
+        assert 1.0 <= t / 201850880 < 1.02                               # within 2 % of the algorithmic bytes
+
+
+class _Dims:
+    """The runtime's dimension record, as the byte model reads it."""
+    def __init__(self, dtype, d, n_layers, q_dim, kv_dim, ffn, vocab, m, n_draft, d_h):
+        self.dtype, self.d, self.n_layers, self.q_dim, self.kv_dim = dtype, d, n_layers, q_dim, kv_dim
+        self.ffn, self.vocab, self.m, self.n_draft_layers, self.d_h = ffn, vocab, m, n_draft, d_h
+
+
+class _Rt:
+    def __init__(self, dims, block, qkv_parts=2):
+        self.dims, self.block, self._qp = dims, block, qkv_parts
+
+    @property
+    def qkv_parts(self):
+        return self._qp
+
+
+def test_gemm_byte_model_at_the_8b_shape():
+    """The per-round GEMM bytes at the Qwen3-8B shape, b = 1, B = 16, against
+    the weight sizes written out: every weight streamed once per round."""
+    dm = _Dims("bf16", 4096, 36, 4096, 1024, 12288, 151936, 5, 5, 4096)
+    gb, nl = bench.gemm_bytes(_Rt(dm, 16), 1)
+    d, L, Ld, f, V = 4096, 36, 5, 12288, 151936
+    qkv, o, gu, dn = d * (d + 2 * 1024), d * d, 2 * f * d, f * d
+    weights = (L + Ld) * (qkv + o + gu + dn) * 2 + 2 * V * d * 2 + 5 * d * d * 2 \
+        + (3 * d * 4096 + 4096 * 2 * d) * 2 + Ld * 2 * 1024 * d * 2
+    assert weights <= gb <= weights * 1.01, (gb, weights)
+    assert nl == (L + Ld) * 4 + 2 + 1 + 2 + 1
