@@ -275,8 +275,12 @@ def main():
     reset()
     run(args.warmup)
     torch.cuda.synchronize()
+    t_pre = time.perf_counter()   # the prompts' prefill (set-up, outside the timed rounds)
     reset()
     torch.cuda.synchronize()
+    t_pre = time.perf_counter() - t_pre
+    n_pre = int(sum(len(p) for p in prompts))
+    log(f"prefill of {n_pre} prompt tokens: {t_pre * 1e3:.1f} ms ({n_pre / t_pre:.0f} tokens/s, 128-row chunks)")
     len0 = sess.seq_len.cpu().numpy().copy()
     # the K timed steps in NSEG consecutive segments, each bracketed by HIP
     # events on the round stream (no synchronisation inside the timed region)
@@ -381,6 +385,7 @@ def main():
                       f"rollout k={kr}, gamma {ROLLOUT_GAMMA}" if kr > 0 else f"{wl.schedule}({wl.sched_param})",
                       "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
                       "parallelism": "single GPU"},
+           "prefill": {"tokens": n_pre, "ms": round(t_pre * 1e3, 2), "tokens_per_s": round(n_pre / t_pre, 1)},
            "segments_ms_per_step": {"n": nseg, "each": [round(x, 4) for x in seg_ms],
                                     "median": round(float(np.median(seg_ms)), 4), "min": round(min(seg_ms), 4)},
            "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
