@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--cpu-sample-ctx", type=int, default=48)
     ap.add_argument("--batch", type=int, default=0, help="override the workload's sequence count (batch sweeps)")
+    ap.add_argument("--prefill-rows", type=int, default=512,
+                    help="prompt rows per prefill chunk (the library's max_rows; set-up only, the rounds are unchanged)")
     ap.add_argument("--rollout", type=int, default=0,
                     help="k > 0: time forward-only multi-round rollouts (a mask round and k relay rounds, "
                          "transitions on the target's greedy trajectory); a step is one rollout")
@@ -227,7 +229,7 @@ def main():
         need = [p + 2 * roll_rounds + 2 * B for p in P0]
         max_ctx = max(need) + 10 * B
     t = time.time()
-    rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window)
+    rt = Runtime(dm, B, b, max_ctx, w, wl.carry_window, max_rows=args.prefill_rows)
     torch.cuda.synchronize()
     log(f"runtime created (upload + pack) in {time.time() - t:.1f}s")
     if args.no_cpu_baseline:
@@ -280,7 +282,8 @@ def main():
     torch.cuda.synchronize()
     t_pre = time.perf_counter() - t_pre
     n_pre = int(sum(len(p) for p in prompts))
-    log(f"prefill of {n_pre} prompt tokens: {t_pre * 1e3:.1f} ms ({n_pre / t_pre:.0f} tokens/s, 128-row chunks)")
+    log(f"prefill of {n_pre} prompt tokens: {t_pre * 1e3:.1f} ms ({n_pre / t_pre:.0f} tokens/s, "
+        f"{args.prefill_rows}-row chunks)")
     len0 = sess.seq_len.cpu().numpy().copy()
     # the K timed steps in NSEG consecutive segments, each bracketed by HIP
     # events on the round stream (no synchronisation inside the timed region)
@@ -385,7 +388,8 @@ def main():
                       f"rollout k={kr}, gamma {ROLLOUT_GAMMA}" if kr > 0 else f"{wl.schedule}({wl.sched_param})",
                       "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
                       "parallelism": "single GPU"},
-           "prefill": {"tokens": n_pre, "ms": round(t_pre * 1e3, 2), "tokens_per_s": round(n_pre / t_pre, 1)},
+           "prefill": {"tokens": n_pre, "chunk_rows": args.prefill_rows, "ms": round(t_pre * 1e3, 2),
+                       "tokens_per_s": round(n_pre / t_pre, 1)},
            "segments_ms_per_step": {"n": nseg, "each": [round(x, 4) for x in seg_ms],
                                     "median": round(float(np.median(seg_ms)), 4), "min": round(min(seg_ms), 4)},
            "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels}
