@@ -45,7 +45,9 @@ def parse():
     ap.add_argument("--carry", choices=["on", "off"], default="on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
-    ap.add_argument("--cpu-sample-ctx", type=int, default=48)
+    ap.add_argument("--cpu-sample-ctx", type=int, default=48,
+                    help="prompt tokens of the oracle rollout sample (--rollout); greedy and sampled rounds are "
+                         "timed at the workload's own context")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's sequence count (batch sweeps)")
     ap.add_argument("--prefill-rows", type=int, default=512,
                     help="prompt rows per prefill chunk (the library's max_rows; set-up only, the rounds are unchanged)")
@@ -55,6 +57,8 @@ def parse():
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="T > 0: sampling decoding (speculative sampling, the drafter's own samples) instead of "
                          "greedy rounds with forced acceptance")
+    ap.add_argument("--eager", action="store_true",
+                    help="issue the greedy round's launches one by one instead of replaying its recorded HIP graph")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (calibrates HBM counters)")
     return ap.parse_args()
@@ -69,14 +73,16 @@ def measured_traffic(kernel_name):
     record (FETCH_SIZE + WRITE_SIZE, each scaled by the same counter's reading
     for a copy of known size), or None when the record is absent, is for
     another kernel, or the kernel's machine code in the loaded library differs
-    from the code the counters were taken on."""
+    from the code the counters were taken on (the record's measured_on digest
+    when it has one: the code that actually ran under the counters)."""
     from paper_2609_06498_amd import library_path
     from paper_2609_06498_amd.codeobj import kernel_code_digest
     try:
         with open(TRAFFIC_FILE) as fh:
             rec = json.load(fh)
+        measured = (rec.get("measured_on") or {}).get("code_sha256", rec.get("code_sha256"))
         if rec.get("kernel") != kernel_name or \
-                rec.get("code_sha256") != kernel_code_digest(library_path(), rec.get("symbol", "")):
+                measured != kernel_code_digest(library_path(), rec.get("symbol", "")):
             return None
     except (OSError, ValueError, KeyError):
         return None
@@ -109,6 +115,17 @@ def gemm_bytes(rt, nseq, verify_lm_head=True, relay=True):
     commit = g(dm.n_draft_layers * 2 * kvd, d)   # the drafter layers' context K/V in one GEMM
     launches = (dm.n_layers + dm.n_draft_layers) * 4 + (2 if verify_lm_head else 1) + (2 if relay else 0) + 1 + 1
     return verify + draft + accept + commit, launches
+
+
+def attention_bytes(rt, start_pos, n_layers):
+    """Algorithmic bytes of the attention launches of one round over n_layers
+    layers: every visible key and value once (t_s context positions plus the
+    B block rows of each sequence), the block's queries once and the
+    attention output once.  start_pos: host [b] anchor positions t_s."""
+    dm, B = rt.dims, rt.block
+    elt = 2 if dm.dtype == "bf16" else 4
+    per_layer = sum((int(t) + B) * 2 * dm.kv_dim * elt + 2 * B * dm.q_dim * elt for t in start_pos)
+    return n_layers * per_layer
 
 
 def measured_stream_peaks():
@@ -254,6 +271,7 @@ def main():
         def run(n, r0=0):
             for r in range(r0, r0 + n):
                 sess.rollout(traj, L, kr, ROLLOUT_GAMMA, carry_on)
+        run_eager = run
     elif sampled:
         streams = torch.arange(b, dtype=torch.int64, device="cuda")
         smp = rt.sampler(args.temperature, 1234, streams)
@@ -264,15 +282,26 @@ def main():
         def run(n, r0=0):
             for r in range(r0, r0 + n):
                 sess.round_sampled(smp, carry_on)
+        run_eager = run
     else:
         traj, L, mode_d, tok_d = build_trajectory(rt, sess, prompts, need, sched, B, b)
 
         def reset():
             sess.prefill(prompts)
 
-        def run(n, r0=0):
+        def run_eager(n, r0=0):
             for r in range(r0, r0 + n):
                 sess.round(carry_on, force=(traj, L, mode_d[r], tok_d[r]))
+
+        run = run_eager
+        if not args.eager:   # the round as one recorded HIP graph, replayed with each round's forcing plan
+            reset()
+            run_eager(1)      # first launches (launch-attribute set-up) outside the capture
+            replay = sess.capture_round(carry_on, force=(traj, L))
+
+            def run(n, r0=0):
+                for r in range(r0, r0 + n):
+                    replay(mode_d[r], tok_d[r])
 
     reset()
     run(args.warmup)
@@ -302,6 +331,10 @@ def main():
     expect = None if (sampled or kr > 0) else int((sched["accept"][:K] + 1).sum())
     diverged = expect is not None and committed != expect
     status = rt.status()
+    tau_cfg = None
+    if not sampled and kr == 0 and wl.schedule == "geometric":   # E[min(G, K)] + 1 of the forcing law
+        q = wl.sched_param / (1.0 + wl.sched_param)
+        tau_cfg = round(1.0 + sum(min(k, wl.K) * (1 - q) * q ** k for k in range(4000)), 4)
     tok_s = committed / dt
     ms_round = dt * 1e3 / K
     rounds_per_step = kr + 1 if kr > 0 else 1
@@ -328,10 +361,20 @@ def main():
         reset()
         torch.cuda.synchronize()
         rt.profile(True)
-        run(kp)
+        pos_hist = []
+        for r in range(kp):   # the anchor positions of every round (device copies; no synchronisation)
+            pos_hist.append(sess.seq_len.clone())
+            run_eager(1, r)
         torch.cuda.synchronize()
         entries = rt.profile_read()
         rt.profile(False)
+        pos_hist = [p.cpu().numpy() for p in pos_hist]
+        # attention: algorithmic bytes from the host-known positions (the library records 0)
+        attn_bytes = {"verify": sum(attention_bytes(rt, p, dm.n_layers) for p in pos_hist),
+                      "draft": sum(attention_bytes(rt, p, dm.n_draft_layers) for p in pos_hist)}
+        for e in entries:
+            if e["name"] == "attention" and e["phase"] in attn_bytes:
+                e["bytes"] = attn_bytes[e["phase"]]
         gemms = [e for e in entries if e["name"].startswith("gemm")]
         assert sum(e["launches"] for e in gemms) == kp * nl, (entries, kp, nl)
         lib_bytes = sum(e["bytes"] for e in gemms)
@@ -339,8 +382,8 @@ def main():
         kernels = []
         for e in sorted(entries, key=lambda e: -e["ms"]):
             avg_us = e["ms"] * 1e3 / e["launches"]
-            k = {"kernel": e["name"], "N": e["N"], "K": e["K"], "M": e["M"], "per_round": e["launches"] / kp,
-                 "avg_us": round(avg_us, 3), "ms_per_round": round(e["ms"] / kp, 4)}
+            k = {"kernel": e["name"], "phase": e["phase"], "N": e["N"], "K": e["K"], "M": e["M"],
+                 "per_round": e["launches"] / kp, "avg_us": round(avg_us, 3), "ms_per_round": round(e["ms"] / kp, 4)}
             if e["bytes"]:
                 k["GB_s"] = round(e["bytes"] / e["launches"] / (avg_us * 1e-6) / 1e9, 1)
             if e["name"].startswith("gemm"):   # matrix-core rate: 2 M N K flops per launch
@@ -364,6 +407,28 @@ def main():
         peaks = measured_stream_peaks()
         roofline["measured_stream_GB_s"] = peaks
         roofline["frac_of_measured_copy"] = round(achieved / peaks["copy_GB_s"], 4)
+
+        def path(sel):   # algorithmic bytes over the summed live kernel time of the selected launches
+            es = [e for e in entries if sel(e)]
+            nb, ms = sum(e["bytes"] for e in es), sum(e["ms"] for e in es)
+            if ms <= 0:
+                return None
+            gbs = nb / (ms * 1e-3) / 1e9
+            return {"GB_per_round": round(nb / kp / 1e9, 4), "ms_per_round": round(ms / kp, 4),
+                    "GB_s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+        # the verify path of the round (its GEMMs, attention and LM head), the
+        # verify attention alone, and the drafter's forward
+        roofline["verify_path"] = path(lambda e: e["phase"] == "verify")
+        roofline["verify_gemms"] = path(lambda e: e["phase"] == "verify" and e["name"].startswith("gemm"))
+        roofline["verify_attention"] = path(lambda e: e["phase"] == "verify" and e["name"] == "attention")
+        roofline["draft_path"] = path(lambda e: e["phase"] == "draft")
+        round_gb = sum(e["bytes"] for e in entries) / kp
+        roofline["round"] = {"GB_per_round": round(round_gb / 1e9, 4),
+                             "GB_s_at_ms_per_step": round(round_gb / (ms_round * 1e-3) / 1e9, 1),
+                             "frac": round(round_gb / (ms_round * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"verify path {roofline['verify_path']}; verify attention {roofline['verify_attention']}; "
+            f"round {roofline['round']}")
         log(f"stream rates on this device: {peaks}")
         log(f"dominant {roofline['kernel']}: avg {avg_s * 1e6:.2f} us, {achieved:.1f} GB/s; "
             f"gemm family {roofline['gemm_family_GB_s']} GB/s, {fam_ms / kp:.3f} ms/round")
@@ -386,7 +451,11 @@ def main():
                       "carry": args.carry,
                       "schedule": f"sampling T={args.temperature}" if sampled else
                       f"rollout k={kr}, gamma {ROLLOUT_GAMMA}" if kr > 0 else f"{wl.schedule}({wl.sched_param})",
-                      "tau_realised": round(tau, 4), "trajectory_diverged": diverged, "status": status,
+                      "tau_realised": round(tau, 4), "tau_configured": tau_cfg,
+                      "tokens_per_s_at_configured_tau": (round(tau_cfg * b / (ms_round * 1e-3), 2)
+                                                         if tau_cfg is not None else None),
+                      "trajectory_diverged": diverged, "status": status,
+                      "launch": "eager" if (args.eager or sampled or kr > 0) else "hip_graph",
                       "parallelism": "single GPU"},
            "prefill": {"tokens": n_pre, "chunk_rows": args.prefill_rows, "ms": round(t_pre * 1e3, 2),
                        "tokens_per_s": round(n_pre / t_pre, 1)},
@@ -396,24 +465,41 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def synthetic_oracle_state(o, prompt, anchor, seed=7):
+    """An oracle sequence state at the prompt's full length whose caches (target
+    K/V, fused features, drafter context K/V) hold seeded random values of the
+    right sizes.  A round's cost depends only on these sizes, and the oracle
+    cannot prefill thousands of tokens within a benchmark's time; the values
+    are for timing only and are never compared with anything."""
+    dm = o.m.dims
+    dt = o.m.mode.dt
+    t = len(prompt)
+    g = np.random.default_rng(seed)
+    kv = lambda: (g.random((t, dm.n_kv_heads, dm.head_dim), dtype=np.float32) - 0.5).astype(dt)
+    st = o.empty_state()
+    st.k = [kv() for _ in range(dm.n_layers)]
+    st.v = [kv() for _ in range(dm.n_layers)]
+    st.F = (g.random((t, dm.d), dtype=np.float32) - 0.5).astype(dt)
+    st.ck = [kv() for _ in range(dm.n_draft_layers)]
+    st.cv = [kv() for _ in range(dm.n_draft_layers)]
+    st.tokens = [int(x) for x in prompt] + [int(anchor)]
+    return st
+
+
 def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0, rollout_k=0):
-    """The oracle timed on this host on a bounded sample: one full round
-    (draft + verify + accept/project + commit, or its sampled form at T > 0)
-    of the same model after a short prefill; tokens/s = realised tau of the
-    GPU run / oracle round time."""
-    import threading
+    """The oracle timed on this host on a bounded sample of the workload: one
+    sequence at its full context length (the first prompt's), one untimed
+    round (it converts the weights and leaves a carry record), then the mean
+    of two timed rounds (draft + verify + accept + commit, or their sampled
+    form at T > 0); tokens/s = the GPU run's realised tau per sequence / the
+    oracle's round time.  A rollout sample prefills ctx_len tokens instead."""
     from oracle import Mode, OracleDFlow, OracleModel
     dm = wl.dims
     mode = "bf16" if dm.dtype == "bf16" else "fp32"
     m = OracleModel(dm, w, Mode(mode), cache=True)
     o = OracleDFlow(m, wl.block, wl.carry_window)
-    p = prompts[0][:ctx_len]
-    t = time.time()
-    s = o.prefill(p)
-    t_pre = time.time() - t
     rng = np.random.default_rng(0)
-    o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))  # carry present
-    n_rounds = 3
+    n_rounds = 2
     if rollout_k > 0:   # one rollout of k + 1 rounds on a random trajectory (its cost does not depend on the tokens)
         import oracle.rollout as ro
         p = prompts[0][:ctx_len]
@@ -422,14 +508,22 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0, rollout_k=0):
         t = time.perf_counter()
         ro.rollout(o, st, traj, rollout_k, ROLLOUT_GAMMA)
         t_round = (time.perf_counter() - t) / (rollout_k + 1)
-        n_rounds = rollout_k + 1
-    t = time.perf_counter()
-    for _ in range(n_rounds if rollout_k == 0 else 0):
-        if temperature > 0:
-            o.round_sampled(s, temperature, 1234, 0, True)
-        else:
-            o.round(s, True, block=np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)]))
-    if rollout_k == 0:
+        n_rounds, ctx = rollout_k + 1, len(p)
+    else:
+        p = prompts[0]
+        ctx = len(p)
+        s = synthetic_oracle_state(o, p, int(rng.integers(0, dm.vocab)))
+        blk = lambda: np.concatenate([[s.anchor], rng.integers(0, dm.vocab, wl.K)])
+
+        def one():
+            if temperature > 0:
+                o.round_sampled(s, temperature, 1234, 0, True)
+            else:
+                o.round(s, True, block=blk())
+        one()   # untimed: weight conversion, carry record
+        t = time.perf_counter()
+        for _ in range(n_rounds):
+            one()
         t_round = (time.perf_counter() - t) / n_rounds
     try:
         import threadpoolctl
@@ -437,14 +531,15 @@ def cpu_baseline(wl, w, prompts, tau, ctx_len, temperature=0.0, rollout_k=0):
         threads = max([i.get("num_threads", 1) for i in info] or [1])
     except Exception:
         threads = os.cpu_count()
-    log(f"oracle: prefill {len(p)} tokens {t_pre:.1f}s, {n_rounds} rounds at {t_round:.2f}s each, {threads} BLAS threads")
+    log(f"oracle: {n_rounds} rounds at context {ctx}, {t_round:.2f}s each, {threads} BLAS threads")
     return {"value": round(tau / t_round, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "ctx": ctx,
             "sample": f"mean of {n_rounds} {mode} oracle rounds (draft+verify+accept+commit, relay on"
                       + (f", speculative sampling T={temperature}" if temperature > 0 else "")
-                      + (f", one forward-only rollout k={rollout_k}" if rollout_k > 0 else "")
-                      + f") of {wl.name} after a "
-                      f"{len(p)}-token prefill; tokens/s = GPU-realised tau {tau:.3f} / {t_round:.2f} s; "
-                      f"host cpu_count {os.cpu_count()}"}
+                      + (f", one forward-only rollout k={rollout_k} after a {ctx}-token prefill" if rollout_k > 0
+                         else f", one sequence at its full {ctx}-position context, caches of seeded random "
+                              f"values") + f") of {wl.name}; tokens/s = GPU-realised tau {tau:.3f} per sequence / "
+                      f"{t_round:.2f} s; host cpu_count {os.cpu_count()}"}
 
 
 if __name__ == "__main__":

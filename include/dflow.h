@@ -22,9 +22,9 @@
  *
  * Conventions
  *  - Every data pointer argument is a DEVICE pointer owned by the caller unless
- *    stated otherwise; the library never frees caller memory.  Weight, cache
- *    and page-table pointers registered at dflow_create must stay valid until
- *    dflow_destroy.  The library allocates its own workspace at create.
+ *    stated otherwise; the library never allocates or frees device memory.
+ *    Weight, cache, page-table, workspace and status pointers registered at
+ *    dflow_create must stay valid until dflow_destroy.
  *  - Every call is asynchronous on the given hipStream_t (0 = null stream) and
  *    performs no host synchronisation, except dflow_read_status.  The calls
  *    on one context share its workspace and per-sequence state, so they must
@@ -185,12 +185,22 @@ size_t dflow_packed_bytes(int dtype, int N, int K);
 int dflow_pack_linear(hipStream_t stream, int dtype, const void* w, int N, int K, int gate_up, const void* col_gain,
                       void* out);
 
-/* Bytes of device workspace that dflow_create allocates for these dims. */
+/* Bytes of device workspace a context needs for these dims (0 if the dims are
+ * invalid).  The workspace holds the round's activations, the carry record
+ * between rounds, split partials, the RoPE table and reduction counters. */
 size_t dflow_workspace_bytes(const dflow_dims* dims);
 
-/* Validates dims, copies the (device) weight/cache pointers, allocates the
- * workspace and the RoPE table.  *out receives the context. */
-int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache, dflow_ctx** out);
+/* Validates dims and registers the (device) weight and cache pointers, the
+ * caller's workspace (device, at least dflow_workspace_bytes(dims) bytes,
+ * 256-byte aligned) and the caller's status word (device int32, the
+ * DFLOW_STATUS_* bits of device-detected conditions).  Set-up: clears the
+ * workspace and the status word and uploads the RoPE table (angles
+ * p * theta^(-2i/head_dim) evaluated in double) on `stream`, then waits for
+ * that stream.  The library allocates no device memory, here or in any
+ * other call.  *out receives the context (host memory, freed by
+ * dflow_destroy; the workspace and status stay the caller's). */
+int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache, void* workspace,
+                 size_t workspace_bytes, int32_t* status, hipStream_t stream, dflow_ctx** out);
 int dflow_destroy(dflow_ctx* ctx);
 
 /* Number of K parts the context streams each QKV projection in (1 or 2):
@@ -205,6 +215,14 @@ int dflow_qkv_parts(const dflow_ctx* ctx);
  * for the same positions, and first_anchor[0] = the target's greedy token
  * after the prompt.  Clears the slot's carry record.  tok: device [len]. */
 int dflow_prefill(dflow_ctx* ctx, hipStream_t stream, int seq, const int32_t* tok, int len, int32_t* first_anchor);
+
+/* Prompt processing of nseq sequences in slots 0..nseq-1: dflow_prefill of
+ * each.  tok: device, the prompts back to back (sum of len tokens); len: HOST
+ * [nseq] prompt lengths (the host plans the row chunks, so the lengths are
+ * host values); first_anchor: device [nseq].  Every length is checked before
+ * anything is launched. */
+int dflow_prefill_batch(dflow_ctx* ctx, hipStream_t stream, int nseq, const int32_t* tok, const int32_t* len,
+                        int32_t* first_anchor);
 
 /* Block drafting (Sec. 3 eq. dflash_drafting; Sec. 4.2 eq. dflow_input).
  * Block row 0 is anchor_tok[s] at position anchor_pos[s]; rows 1..K start
@@ -367,11 +385,19 @@ int dflow_bench_force_drafts(dflow_ctx* ctx, hipStream_t stream, int nseq, const
  * and aggregates them per
  * kernel class (GEMM epilogue and shape, or attention): summed elapsed
  * milliseconds, launches and algorithmic bytes (GEMM: each weight, input and
- * output byte once; attention: 0, its key count is device-resident).  Writes
- * up to max_entries entries, sets *n_entries, then clears the record. */
+ * output byte once; attention: 0, its key count is device-resident), and
+ * the entry point that issued them (phase).  Writes up to max_entries
+ * entries, sets *n_entries, then clears the record. */
+#define DFLOW_PHASE_OTHER 0
+#define DFLOW_PHASE_DRAFT 1     /* dflow_draft_block */
+#define DFLOW_PHASE_VERIFY 2    /* dflow_verify_block */
+#define DFLOW_PHASE_ACCEPT 3    /* dflow_accept_and_carry, dflow_accept_sampled */
+#define DFLOW_PHASE_COMMIT 4    /* kv_commit */
+#define DFLOW_PHASE_PREFILL 5   /* dflow_prefill, dflow_prefill_batch, dflow_prefill_sampled */
 typedef struct dflow_prof_entry {
   char name[32];   /* "gemm.store", "gemm.resid", "gemm.swiglu", "gemm.argmax", ..., "attention" */
   int N, K, M;     /* GEMM shape (0 for attention) */
+  int phase;       /* DFLOW_PHASE_* */
   int launches;
   double ms;
   double bytes;
@@ -380,7 +406,7 @@ int dflow_profile(dflow_ctx* ctx, int enable);
 int dflow_profile_read(dflow_ctx* ctx, dflow_prof_entry* out, int max_entries, int* n_entries);
 
 /* Synchronises `stream`, copies the device status word to *host_status and,
- * if clear != 0, resets it. */
+ * if clear != 0, resets it (on `stream`, then waits for it). */
 int dflow_read_status(dflow_ctx* ctx, hipStream_t stream, int32_t* host_status, int clear);
 
 #ifdef __cplusplus

@@ -65,6 +65,7 @@ class SeqState:
     ck: List[np.ndarray]        # per drafter layer [t, Hkv, Dh] context keys
     cv: List[np.ndarray]
     carry: Optional[Carry] = None
+    last_logits: Optional[np.ndarray] = None   # [V] logits of the prompt's last row (set by prefill)
 
     @property
     def t(self) -> int:
@@ -134,11 +135,11 @@ class OracleDFlow:
                         F=np.zeros((0, dm.d), dt), ck=[e() for _ in range(dm.n_draft_layers)],
                         cv=[e() for _ in range(dm.n_draft_layers)])
 
-    def _append_target(self, s: SeqState, tokens: Sequence[int], keep: int):
+    def _append_target(self, s: SeqState, tokens: Sequence[int], keep: int, logit_rows: slice = slice(None)):
         """Run the target over tokens at positions t.. and keep the first
-        `keep` rows in the caches; returns (logits, hcat, fused f)."""
+        `keep` rows in the caches; returns (logits of logit_rows, hcat, fused f)."""
         pos0 = s.k[0].shape[0]
-        logits, ks, vs, hid = self.m.target_block(tokens, pos0, s.k, s.v)
+        logits, ks, vs, hid = self.m.target_block(tokens, pos0, s.k, s.v, logit_rows)
         hcat = np.concatenate([hid[l] for l in self.m.dims.capture_layers], axis=1)
         f = self.m.fuse(hcat)
         for l in range(self.m.dims.n_layers):
@@ -166,13 +167,15 @@ class OracleDFlow:
         logits = None
         for c in range(0, len(prompt), self.prefill_chunk):
             chunk = prompt[c:c + self.prefill_chunk]
-            logits, _, _ = self._append_target(s, chunk, len(chunk))
+            last = c + self.prefill_chunk >= len(prompt)   # only the prompt's last row is scored
+            logits, _, _ = self._append_target(s, chunk, len(chunk), slice(-1, None) if last else slice(0, 0))
         if sampler is None:
             first = int(argmax_lowest(logits[-1]))
         else:
             T, seed, stream = sampler
             first = sampling.sample_first(logits[-1], sampling.inv_temperature(T), seed, stream, len(prompt) - 1)
         s.tokens = prompt + [first]
+        s.last_logits = np.asarray(logits[-1])
         return s
 
     # ------------------------------------------------------------ round steps

@@ -6,8 +6,8 @@ The target is the Qwen3 decoder evaluated in the paper (Sec. 5.1): RMSNorm,
 per-head RMSNorm of q and k (QK-norm), rotate-half RoPE with theta = 1e6 at
 absolute positions, grouped-query attention, SwiGLU feed-forward, no biases.
 The drafter is the block-diffusion drafter of Sec. 3 (eq. dflash_drafting)
-with the fused target feature injected into the key and value projections of
-every draft layer (Sec. 3, text after eq. dflash_context).
+whose key and value projections in every layer also take the fused target
+feature (Sec. 3, text after eq. dflash_context).
 
 Pins (tests/test_oracle_pins.py, tests/test_oracle_primitives.py):
   * target_block / logits: transformers.Qwen3ForCausalLM on CPU with the same
@@ -86,21 +86,26 @@ class OracleModel:
 
     def attention(self, q: np.ndarray, k: np.ndarray, v: np.ndarray, visible: np.ndarray) -> np.ndarray:
         """softmax(q k^T / sqrt(Dh)) v per query head; head h reads KV head
-        floor(h * Hkv / Hq).  q: [n, Hq, Dh]; k, v: [m, Hkv, Dh];
-        visible: [n, m] bool.  Returns [n, Hq * Dh]."""
+        floor(h * Hkv / Hq), i.e. the G = Hq / Hkv consecutive query heads of
+        a group share one KV head.  q: [n, Hq, Dh]; k, v: [m, Hkv, Dh];
+        visible: [n, m] bool.  Returns [n, Hq * Dh].  Evaluated one KV head
+        at a time (one group of query heads) to bound the score arrays."""
         dm = self.dims
         dt = self.mode.dt
         n, Hq, Dh = q.shape
-        kv_of = (np.arange(Hq) * dm.n_kv_heads) // Hq
-        kh = k[:, kv_of, :]                                  # [m, Hq, Dh]
-        vh = v[:, kv_of, :]
-        s = np.einsum("nhd,mhd->hnm", q, kh) / dt(np.sqrt(Dh))
-        s = np.where(visible[None, :, :], s, -np.inf)
-        s = s - s.max(axis=-1, keepdims=True)
-        p = np.exp(s)
-        p = p / p.sum(axis=-1, keepdims=True)
-        o = np.einsum("hnm,mhd->nhd", p, vh)
-        return o.reshape(n, Hq * Dh).astype(dt)
+        G = Hq // dm.n_kv_heads
+        hidden = ~np.asarray(visible, bool)
+        out = np.empty((n, Hq, Dh), dt)
+        for j in range(dm.n_kv_heads):
+            qj = np.ascontiguousarray(q[:, j * G:(j + 1) * G, :].transpose(1, 0, 2))   # [G, n, Dh]
+            s = np.matmul(qj, np.ascontiguousarray(k[:, j, :].T))                      # [G, n, m]
+            np.divide(s, dt(np.sqrt(Dh)), out=s)
+            s[:, hidden] = -np.inf
+            s -= s.max(axis=-1, keepdims=True)
+            np.exp(s, out=s)
+            s /= s.sum(axis=-1, keepdims=True)
+            out[:, j * G:(j + 1) * G, :] = np.matmul(s, np.ascontiguousarray(v[:, j, :])).transpose(1, 0, 2)
+        return out.reshape(n, Hq * Dh)
 
     # ------------------------------------------------------------ decoder layer pieces
     def _qkv(self, prefix: str, h: np.ndarray, pos: np.ndarray):
@@ -150,10 +155,11 @@ class OracleModel:
         return self.linear(h, "lm_head")
 
     def target_block(self, tokens: Sequence[int], pos0: int,
-                     k_cache: List[np.ndarray], v_cache: List[np.ndarray]):
+                     k_cache: List[np.ndarray], v_cache: List[np.ndarray], logit_rows: slice = slice(None)):
         """Causal target forward of rows tokens[j] at positions pos0 + j against
         a cache holding positions 0..pos0-1 of every layer.
-        Returns (logits [n,V], k_rows[L], v_rows[L], hidden[L] residual outputs)."""
+        Returns (logits of the rows logit_rows selects (all by default) [n', V],
+        k_rows[L], v_rows[L], hidden[L] residual outputs)."""
         dm = self.dims
         n = len(tokens)
         pos = np.arange(pos0, pos0 + n)
@@ -165,7 +171,7 @@ class OracleModel:
             ks.append(k)
             vs.append(v)
             hid.append(x)
-        return self.logits(x, "final_norm"), ks, vs, hid
+        return self.logits(x[logit_rows], "final_norm"), ks, vs, hid
 
     # ------------------------------------------------------------ drafter
     def fuse(self, hcat: np.ndarray) -> np.ndarray:

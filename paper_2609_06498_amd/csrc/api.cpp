@@ -56,8 +56,9 @@ struct dflow_ctx {
   dflow_cache c;
   size_t pool_layer_elems;   // elements of one layer pool (K or V)
 
-  void* ws = nullptr;
+  void* ws = nullptr;         // caller-owned workspace (dflow_workspace_bytes)
   size_t ws_bytes = 0;
+  int phase = DFLOW_PHASE_OTHER;   // entry point being issued (tags the kernel-timing record)
   // workspace views
   void *x, *xn, *qkv, *q, *attn, *act, *hcap, *f, *fpre, *u, *hid;
   float *fproj, *bg, *part_o, *part_ml;
@@ -76,7 +77,7 @@ struct dflow_ctx {
   // kernel timing record (dflow_profile)
   bool prof = false;
   std::vector<hipEvent_t> ev0, ev1;
-  struct Rec { int cls, N, K, M; double bytes; };
+  struct Rec { int cls, N, K, M, phase; double bytes; };
   std::vector<Rec> ev_rec;
   int n_ev = 0;
 };
@@ -180,7 +181,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   add((size_t)d->max_pages * PAGE * (d->head_dim / 2) * sizeof(float2));  // 13 rope
   add((size_t)lm_groups * mmax * 8);                   // 14 amax: [lm_groups][rows] argmax keys
   add((size_t)d->max_batch * CARRY_REC * 4);           // 15 carry_rec
-  add(4);                                              // 16 status
+  add(4);                                              // 16 unused (the status word is the caller's)
   add((size_t)(d->max_batch + 1) * 4);                 // 17 tmp_pos
   add((size_t)mmax * 4);                               // 18 tmp_argmax
   add((size_t)mmax * SSQ_LD * 4);                      // 19 ssq: per-strip sums of squares of the residual rows
@@ -226,10 +227,18 @@ extern "C" size_t dflow_workspace_bytes(const dflow_dims* dims) {
 }
 
 extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, const dflow_cache* cache,
+                            void* workspace, size_t workspace_bytes, int32_t* status, hipStream_t stream,
                             dflow_ctx** out) {
   int rc = validate(dims);
   if (rc) return rc;
-  if (!w || !cache || !out) return fail(DFLOW_EINVAL, "create: null argument");
+  if (!w || !cache || !out || !workspace || !status) return fail(DFLOW_EINVAL, "create: null argument");
+  if (((uintptr_t)workspace & 255) || ((uintptr_t)status & 3))
+    return fail(DFLOW_EINVAL, "create: workspace must be 256-byte and status 4-byte aligned");
+  {
+    const size_t need = plan(dims, nullptr, nullptr, nullptr).total;
+    if (workspace_bytes < need)
+      return fail(DFLOW_ECAPACITY, "create: workspace of %zu bytes, %zu needed", workspace_bytes, need);
+  }
   const void* req[] = {w->embed, w->lm_head, w->layers, w->draft_layers, w->draft_lm_head, w->draft_wkv_ctx,
                        w->e_mask, w->w_c, w->g_c, w->relay_w1, w->relay_c1, w->relay_w2, w->relay_c2,
                        w->relay_ln_g, w->relay_ln_b, cache->k_pool, cache->v_pool, cache->ck_pool, cache->cv_pool,
@@ -274,12 +283,8 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->pool_layer_elems = (size_t)dims->num_pages * dims->n_kv_heads * PAGE * dims->head_dim;
 
   Layout L = plan(dims, &c->nsplit, &c->part_items, &c->lm_groups);
+  c->ws = workspace;
   c->ws_bytes = L.total;
-  hipError_t e = hipMalloc(&c->ws, c->ws_bytes);
-  if (e != hipSuccess) {
-    delete c;
-    return fail(DFLOW_EHIP, "workspace hipMalloc(%zu): %s", L.total, hipGetErrorString(e));
-  }
   char* b = (char*)c->ws;
   c->x = b + L.off[0];
   c->xn = b + L.off[1];
@@ -297,7 +302,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->rope = (float2*)(b + L.off[13]);
   c->amax = (uint64_t*)(b + L.off[14]);
   c->carry_rec = (int*)(b + L.off[15]);
-  c->status = (int*)(b + L.off[16]);
+  c->status = status;
   c->tmp_pos = (int*)(b + L.off[17]);
   c->tmp_argmax = (int*)(b + L.off[18]);
   c->ssq = (float*)(b + L.off[19]);
@@ -322,15 +327,19 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
       tab[p * half + i] = make_float2((float)std::cos(a), (float)std::sin(a));
     }
   }
-  e = hipMemset(c->ws, 0, c->ws_bytes);
-  if (e == hipSuccess) e = hipMemcpy(c->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
-  if (e == hipSuccess && dims->n_draft_layers > 0) {
-    std::vector<const void*> kn(dims->n_draft_layers);
-    for (int l = 0; l < dims->n_draft_layers; ++l) kn[l] = c->dlayers[l].k_norm;
-    e = hipMemcpy(c->dknorm, kn.data(), kn.size() * sizeof(void*), hipMemcpyHostToDevice);
-  }
+  // set-up on the caller's stream: clear the workspace and the status word,
+  // upload the RoPE table and the drafter K-norm pointers, then wait for it
+  // (the host buffers are local)
+  std::vector<const void*> kn(dims->n_draft_layers > 0 ? dims->n_draft_layers : 0);
+  for (int l = 0; l < dims->n_draft_layers; ++l) kn[l] = c->dlayers[l].k_norm;
+  hipError_t e = launch_fill_u32((uint32_t*)c->ws, 0u, c->ws_bytes / 4, stream);
+  if (e == hipSuccess) e = launch_fill_u32((uint32_t*)c->status, 0u, 1, stream);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(c->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess && !kn.empty())
+    e = hipMemcpyAsync(c->dknorm, kn.data(), kn.size() * sizeof(void*), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) {
-    (void)hipFree(c->ws);
     delete c;
     return fail(DFLOW_EHIP, "create: %s", hipGetErrorString(e));
   }
@@ -342,9 +351,7 @@ extern "C" int dflow_destroy(dflow_ctx* c) {
   if (!c) return fail(DFLOW_EINVAL, "destroy: null context");
   for (auto ev : c->ev0) (void)hipEventDestroy(ev);
   for (auto ev : c->ev1) (void)hipEventDestroy(ev);
-  hipError_t e = hipFree(c->ws);
-  delete c;
-  if (e != hipSuccess) return fail(DFLOW_EHIP, "destroy: %s", hipGetErrorString(e));
+  delete c;   // the workspace and the status word belong to the caller
   return DFLOW_OK;
 }
 
@@ -403,7 +410,7 @@ hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, c
     if ((e = hipEventRecord(c->ev1[c->n_ev], st)) != hipSuccess) return e;
     const double out_elt = (epi == EPI_ARGMAX) ? 0.0 : ((epi == EPI_STORE_F32 || epi == EPI_BIAS_F32) ? 4.0 : c->elt);
     const double n_out = (epi == EPI_SWIGLU) ? N / 2.0 : N;
-    c->ev_rec[c->n_ev] = {epi, N, K, M,
+    c->ev_rec[c->n_ev] = {epi, N, K, M, c->phase,
                           (double)N * K * c->elt + (double)M * K * c->elt + (double)M * n_out * out_elt * ksplit};
     ++c->n_ev;
   }
@@ -452,7 +459,7 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
   if ((e = launch_attention(c->bf, a, st)) != hipSuccess) return e;
   if (rec) {
     if ((e = hipEventRecord(c->ev1[c->n_ev], st)) != hipSuccess) return e;
-    c->ev_rec[c->n_ev++] = {CLS_ATTN, 0, 0, nseq * Bq, 0.0};
+    c->ev_rec[c->n_ev++] = {CLS_ATTN, 0, 0, nseq * Bq, c->phase, 0.0};
   }
   return hipSuccess;
 }
@@ -615,6 +622,7 @@ int prefill_impl(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int 
   if (len < 1) return fail(DFLOW_ESHAPE, "prefill: len %d", len);
   if ((long long)len + c->dm.block > (long long)c->dm.max_pages * PAGE)
     return fail(DFLOW_ECAPACITY, "prefill: %d tokens exceed the page table (%d)", len, c->dm.max_pages * PAGE);
+  c->phase = DFLOW_PHASE_PREFILL;
   SampleArgs sa;
   if (smp) {
     // counter word 0 of the first draw: the prompt's last position (held in tmp_pos[1])
@@ -650,6 +658,22 @@ extern "C" int dflow_prefill(dflow_ctx* c, hipStream_t st, int seq, const int32_
   return prefill_impl(c, st, seq, tok, len, nullptr, first_anchor);
 }
 
+extern "C" int dflow_prefill_batch(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* tok, const int32_t* len,
+                                   int32_t* first_anchor) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!tok || !len || !first_anchor) return fail(DFLOW_EINVAL, "prefill_batch: null argument");
+  for (int s = 0; s < nseq; ++s)   // every length is checked before anything is launched
+    if (len[s] < 1 || (long long)len[s] + c->dm.block > (long long)c->dm.max_pages * PAGE)
+      return fail(len[s] < 1 ? DFLOW_ESHAPE : DFLOW_ECAPACITY, "prefill_batch: sequence %d has %d tokens", s, len[s]);
+  size_t off = 0;
+  for (int s = 0; s < nseq; ++s) {
+    if ((rc = prefill_impl(c, st, s, tok + off, len[s], nullptr, first_anchor + s))) return rc;
+    off += (size_t)len[s];
+  }
+  return DFLOW_OK;
+}
+
 extern "C" int dflow_prefill_sampled(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int len,
                                      const dflow_sampler* smp, int32_t* first_token) {
   if (!smp) return fail(DFLOW_EINVAL, "prefill_sampled: null sampler");
@@ -663,6 +687,7 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   if (rc) return rc;
   if (!anchor_tok || !anchor_pos || (!draft_tok && !block_out && !draft_logits))
     return fail(DFLOW_EINVAL, "draft_block: null argument");
+  c->phase = DFLOW_PHASE_DRAFT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
   if (carry_on) {
@@ -693,6 +718,7 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
   int rc = check_nseq(c, nseq);
   if (rc) return rc;
   if (!block_tok || !start_pos) return fail(DFLOW_EINVAL, "verify_block: null argument");
+  c->phase = DFLOW_PHASE_VERIFY;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
   HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
@@ -709,6 +735,7 @@ extern "C" int dflow_accept_and_carry(dflow_ctx* c, hipStream_t st, int nseq, co
   if (rc) return rc;
   if (!block_tok || !tgt_argmax || !accept_len || !committed)
     return fail(DFLOW_EINVAL, "accept_and_carry: null argument");
+  c->phase = DFLOW_PHASE_ACCEPT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
   HIPCHK(launch_accept(block_tok, tgt_argmax, nseq, B, d.carry_window, accept_len, bonus, committed, n_carry,
@@ -752,6 +779,7 @@ extern "C" int dflow_accept_sampled(dflow_ctx* c, hipStream_t st, int nseq, cons
   if (rc) return rc;
   if (!block_tok || !logits || !draft_logits || !accept_len || !committed)
     return fail(DFLOW_EINVAL, "accept_sampled: null argument");
+  c->phase = DFLOW_PHASE_ACCEPT;
   SampleArgs a;
   if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
   const dflow_dims& d = c->dm;
@@ -792,6 +820,7 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
   int rc = check_nseq(c, nseq);
   if (rc) return rc;
   if (!accept_len || !seq_len) return fail(DFLOW_EINVAL, "kv_commit: null argument");
+  c->phase = DFLOW_PHASE_COMMIT;
   HIPCHK(ctx_append(c, st, c->f, nseq, c->dm.block, seq_len, accept_len, c->c.page_table));
   HIPCHK(launch_commit(accept_len, nseq, seq_len, st));
   return DFLOW_OK;
@@ -853,13 +882,16 @@ extern "C" int dflow_profile_read(dflow_ctx* c, dflow_prof_entry* out, int max_e
     const auto& r = c->ev_rec[i];
     size_t k = 0;
     for (; k < agg.size(); ++k)
-      if (!strcmp(agg[k].name, kClassName[r.cls]) && agg[k].N == r.N && agg[k].K == r.K && agg[k].M == r.M) break;
+      if (!strcmp(agg[k].name, kClassName[r.cls]) && agg[k].N == r.N && agg[k].K == r.K && agg[k].M == r.M &&
+          agg[k].phase == r.phase)
+        break;
     if (k == agg.size()) {
       dflow_prof_entry e{};
       snprintf(e.name, sizeof(e.name), "%s", kClassName[r.cls]);
       e.N = r.N;
       e.K = r.K;
       e.M = r.M;
+      e.phase = r.phase;
       agg.push_back(e);
     }
     agg[k].launches += 1;
@@ -877,6 +909,9 @@ extern "C" int dflow_read_status(dflow_ctx* c, hipStream_t st, int32_t* host_sta
   if (!c || !host_status) return fail(DFLOW_EINVAL, "read_status: null argument");
   HIPCHK(hipStreamSynchronize(st));
   HIPCHK(hipMemcpy(host_status, c->status, 4, hipMemcpyDeviceToHost));
-  if (clear) HIPCHK(hipMemset(c->status, 0, 4));
+  if (clear) {
+    HIPCHK(launch_fill_u32((uint32_t*)c->status, 0u, 1, st));
+    HIPCHK(hipStreamSynchronize(st));
+  }
   return DFLOW_OK;
 }

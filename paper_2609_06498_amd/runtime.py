@@ -70,10 +70,13 @@ EXPORTS = {
                                          ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(Dims)]),
     "dflow_create": (ctypes.c_int, [ctypes.POINTER(Dims), ctypes.POINTER(Weights), ctypes.POINTER(Cache),
+                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.POINTER(ctypes.c_void_p)]),
     "dflow_destroy": (ctypes.c_int, [ctypes.c_void_p]),
     "dflow_prefill": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                                      ctypes.c_void_p]),
+    "dflow_prefill_batch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                           ctypes.POINTER(ctypes.c_int32), ctypes.c_void_p]),
     "dflow_draft_block": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_void_p]),
@@ -112,7 +115,11 @@ EXPORTS = {
 
 class ProfEntry(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32), ("N", ctypes.c_int), ("K", ctypes.c_int), ("M", ctypes.c_int),
-                ("launches", ctypes.c_int), ("ms", ctypes.c_double), ("bytes", ctypes.c_double)]
+                ("phase", ctypes.c_int), ("launches", ctypes.c_int), ("ms", ctypes.c_double),
+                ("bytes", ctypes.c_double)]
+
+
+PHASES = {0: "other", 1: "draft", 2: "verify", 3: "accept", 4: "commit", 5: "prefill"}
 
 
 def load_library(path: Optional[str] = None):
@@ -213,10 +220,17 @@ class Runtime:
         C.ck_pool, C.cv_pool = self.ck_pool.data_ptr(), self.cv_pool.data_ptr()
         C.page_table = self.page_table.data_ptr()
         self.ccache = C
+        # workspace and status word: device memory owned here (torch), registered with the context
+        ws_bytes = int(self.lib.dflow_workspace_bytes(ctypes.byref(d)))
+        if ws_bytes == 0:
+            self._check(-2, "dflow_workspace_bytes")
+        self.workspace = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=self.device)
+        self.status_word = torch.zeros(1, dtype=torch.int32, device=self.device)
+        ws_ptr = (self.workspace.data_ptr() + 255) // 256 * 256
         torch.cuda.synchronize(self.device)
         ctx = ctypes.c_void_p()
-        self._check(self.lib.dflow_create(ctypes.byref(d), ctypes.byref(W), ctypes.byref(C), ctypes.byref(ctx)),
-                    "dflow_create")
+        self._check(self.lib.dflow_create(ctypes.byref(d), ctypes.byref(W), ctypes.byref(C), ws_ptr, ws_bytes,
+                                          self.status_word.data_ptr(), _stream(), ctypes.byref(ctx)), "dflow_create")
         self.ctx = ctx
 
     # ------------------------------------------------------------ weights
@@ -265,6 +279,13 @@ class Runtime:
     def prefill(self, seq: int, tokens, first_anchor):
         self._check(self.lib.dflow_prefill(self.ctx, _stream(), seq, _ptr(tokens), int(tokens.numel()),
                                            _ptr(first_anchor)), "dflow_prefill")
+
+    def prefill_batch(self, tokens, lengths, first_anchor):
+        """tokens: device int32 prompts back to back; lengths: host ints; first_anchor: device int32 [nseq]."""
+        n = len(lengths)
+        lens = (ctypes.c_int32 * n)(*[int(x) for x in lengths])
+        self._check(self.lib.dflow_prefill_batch(self.ctx, _stream(), n, _ptr(tokens), lens, _ptr(first_anchor)),
+                    "dflow_prefill_batch")
 
     def draft_block(self, nseq, anchor_tok, anchor_pos, carry_on, draft_tok=None, block_out=None, draft_logits=None):
         self._check(self.lib.dflow_draft_block(self.ctx, _stream(), nseq, _ptr(anchor_tok), _ptr(anchor_pos),
@@ -339,12 +360,12 @@ class Runtime:
         self._check(self.lib.dflow_profile(self.ctx, int(bool(enable))), "dflow_profile")
 
     def profile_read(self):
-        """List of dicts (name, N, K, M, launches, ms, bytes) per kernel class."""
-        buf = (ProfEntry * 64)()
+        """List of dicts (name, N, K, M, phase, launches, ms, bytes) per kernel class and issuing entry point."""
+        buf = (ProfEntry * 128)()
         n = ctypes.c_int(0)
-        self._check(self.lib.dflow_profile_read(self.ctx, buf, 64, ctypes.byref(n)), "dflow_profile_read")
-        return [{"name": e.name.decode(), "N": e.N, "K": e.K, "M": e.M, "launches": e.launches, "ms": e.ms,
-                 "bytes": e.bytes} for e in buf[:min(n.value, 64)]]
+        self._check(self.lib.dflow_profile_read(self.ctx, buf, 128, ctypes.byref(n)), "dflow_profile_read")
+        return [{"name": e.name.decode(), "N": e.N, "K": e.K, "M": e.M, "phase": PHASES.get(e.phase, str(e.phase)),
+                 "launches": e.launches, "ms": e.ms, "bytes": e.bytes} for e in buf[:min(n.value, 128)]]
 
     def close(self):
         if getattr(self, "ctx", None):

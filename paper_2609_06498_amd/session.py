@@ -45,9 +45,8 @@ class Session:
     def prefill(self, prompts: List[np.ndarray]):
         torch = self.rt.torch
         assert len(prompts) == self.nseq
-        for s, p in enumerate(prompts):
-            tok = torch.from_numpy(np.ascontiguousarray(p, dtype=np.int32)).to(self.rt.device)
-            self.rt.prefill(s, tok, self.anchor[s:s + 1])
+        tok = torch.from_numpy(np.concatenate([np.asarray(p, dtype=np.int32) for p in prompts])).to(self.rt.device)
+        self.rt.prefill_batch(tok, [len(p) for p in prompts], self.anchor)
         self.seq_len.copy_(torch.tensor([len(p) for p in prompts], dtype=torch.int32))
 
     def round(self, carry_on: bool = True, force=None, draft_logits=None, logits=None, hcap=None, feat=None):
@@ -60,6 +59,38 @@ class Session:
         rt.verify_block(b, self.block, self.seq_len, self.tgt, logits, hcap)
         rt.accept_and_carry(b, self.block, self.tgt, self.accept, self.anchor, self.committed, self.n_carry, feat)
         rt.kv_commit(b, self.accept, self.seq_len)
+
+    def capture_round(self, carry_on: bool = True, force=None):
+        """Records one greedy round (the launches of `round`) into a HIP graph
+        and returns replay(mode=None, tok=None), which re-issues the whole
+        round as one graph launch on the current stream: no per-kernel host
+        launch cost.  With force = (traj, traj_len) the round is recorded with
+        the forcing step reading fixed plan buffers, and replay first copies
+        that round's plan (mode, tok; device [b, B]) into them.  The graph
+        holds kernel launches only (no memset nodes); the recorded state
+        buffers are the session's own, so replays continue from whatever
+        state the session is in.  Run one eager round first: launch-attribute
+        set-up happens at a kernel's first launch, outside any capture."""
+        torch = self.rt.torch
+        f = None
+        if force is not None:
+            traj, traj_len = force
+            self._gmode = torch.zeros(self.nseq, self.B, dtype=torch.int8, device=self.rt.device)
+            self._gtok = torch.zeros(self.nseq, self.B, dtype=torch.int32, device=self.rt.device)
+            f = (traj, traj_len, self._gmode, self._gtok)
+        graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize(self.rt.device)
+        with torch.cuda.graph(graph):
+            self.round(carry_on, force=f)
+        torch.cuda.synchronize(self.rt.device)
+
+        def replay(mode=None, tok=None):
+            if f is not None:
+                self._gmode.copy_(mode, non_blocking=True)
+                self._gtok.copy_(tok, non_blocking=True)
+            graph.replay()
+        replay.graph = graph
+        return replay
 
     def round_sampled(self, sampler, carry_on: bool = True, draft_logits=None, logits=None, hcap=None, feat=None):
         """One round decoded by speculative sampling; `sampler` from Runtime.sampler."""

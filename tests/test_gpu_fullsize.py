@@ -1,30 +1,33 @@
 """GPU parity at full model widths in the launch configuration bench.py
-times (b = 1, B = 16, bf16), on the benchmark's seeded weights:
+times (b = 1, B = 16, bf16, prompts prefilled in 512-row chunks), on the
+benchmark's seeded weights:
 
 * qwen3-8b  -- the benchmarked shape (36 + 5 layers, d 4096, 32/8 heads,
-  FFN 12288, vocab 151936);
+  FFN 12288, vocab 151936) at a 640-token context: the prefill runs a
+  512-row chunk (tiled GEMMs, the unfused attention) and a 128-row chunk, and
+  every round's attention spans three 256-key splits plus the block, merged
+  by the split combine, with the QKV projection in two K parts and QK-norm,
+  RoPE and the block's KV write fused into the attention;
 * qwen3-1.7b -- 28 + 5 layers, d 2048, 16/8 heads, FFN 6144;
 * qwen3-32b-d5 -- the Qwen3-32B widths (d 5120, 64/8 heads: GQA group 8,
   which takes the attention path without the fused QK-norm/RoPE, FFN 25600)
   at 5 target layers, since the oracle cannot hold the 64-layer model; the
   full-depth 32B shape is covered by the batch-invariance test.
 
-The oracle cannot prefill thousands of tokens in a test, so the context is the
-first 48 prompt tokens (one attention split; the multi-split path and ragged
-batches are covered by the small workloads and the invariance tests).  Drafts
-are seeded random tokens, so nearly every round rejects at the first draft
-and relays K - 1 verifier states: round 0 has no carry yet, rounds 1 and 2
-exercise the relay.
+Drafts are seeded random tokens, so nearly every round rejects at the first
+draft and relays K - 1 verifier states: round 0 has no carry yet, rounds 1
+and 2 exercise the relay.
 
 Bar.  At these depths the bf16 storage noise of the random-init models is
-larger than 2e-2 (the oracle's own bf16 mode differs from its fp32 mode by
-about 5 % in the 8B logits).  So the device is compared with the fp32 oracle,
+larger than 2e-2 (the oracle's bf16 mode differs from its fp32 mode by a few
+per cent in the 8B logits).  So the device is compared with the fp32 oracle,
 and each quantity must be within max(2e-2, 1.5 x the bf16 oracle's distance
-to the fp32 oracle, capped at 0.15) per row -- the cap matters for the 1.7B
-model, whose bf16 oracle drifts from its fp32 mode by more than 100 % while
-the device stays within 3 %; decisions (acceptance, bonus, argmax) must match
-the fp32 oracle wherever its top-1 margin exceeds that bound (near ties
-follow the device's decision in both oracles, and are counted)."""
+to the fp32 oracle) per row, the bf16 oracle verifying exactly the device's
+blocks: from the first anchor on, both oracles follow the device's decisions
+(the bf16 oracle always, as the noise reference; the fp32 oracle only where
+its own top-1 margin is within the bound, a counted near tie).  Decisions
+(first anchor, acceptance, bonus, argmax) must match the fp32 oracle wherever
+its top-1 margin exceeds that bound."""
 import numpy as np
 import pytest
 
@@ -35,10 +38,10 @@ from workload.synth import make_prompts, make_weights
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-CTX = 48
+CTX = {"qwen3-8b": 640, "qwen3-1.7b": 48, "qwen3-32b-d5": 48}
+PREFILL_ROWS = 512   # bench.py's prefill chunk
 ROUNDS = 3
 NOISE_FACTOR = 1.5
-NOISE_CAP = 0.15     # a chaotic bf16 oracle (1.7B: >100 %) must not make the bound vacuous
 
 
 def _workload(name):
@@ -51,6 +54,12 @@ def _workload(name):
     return get_config(name)
 
 
+def bound_from_noise(dtype, ref16, ref32):
+    """max(tolerance, 1.5 x the bf16 oracle's largest per-row distance to the fp32 oracle)."""
+    noise = float(rel_rows(ref16, ref32).max())
+    return max(TOL[dtype], NOISE_FACTOR * noise), noise
+
+
 @pytest.mark.parametrize("name", ["qwen3-8b", "qwen3-1.7b", "qwen3-32b-d5"])
 def test_round_parity_full_width(name):
     if not torch.cuda.is_available():
@@ -60,23 +69,39 @@ def test_round_parity_full_width(name):
     from paper_2609_06498_amd.session import Session
     wl = _workload(name)
     dm, B, K, V = wl.dims, wl.block, wl.K, wl.dims.vocab
-    prompt = make_prompts(wl)[0][:CTX]
-    print(f"[fullsize] {wl.name} ctx {CTX} rounds {ROUNDS}", flush=True)
+    ctx = CTX[name]
+    prompt = make_prompts(wl)[0][:ctx]
+    print(f"[fullsize] {wl.name} ctx {ctx} rounds {ROUNDS}", flush=True)
     w = make_weights(dm, wl.seed_w)
-    rt = Runtime(dm, B, 1, CTX + (ROUNDS + 1) * B, w, wl.carry_window)
+    rt = Runtime(dm, B, 1, ctx + (ROUNDS + 1) * B, w, wl.carry_window, max_rows=PREFILL_ROWS)
     o32 = OracleDFlow(OracleModel(dm, w, Mode("fp32")), B, wl.carry_window)
     o16 = OracleDFlow(OracleModel(dm, w, Mode("bf16")), B, wl.carry_window)
     del w
-    s32, s16 = o32.prefill(prompt), o16.prefill(prompt)
+    s32 = o32.prefill(prompt)
+    print(f"[fullsize] fp32 oracle prefill done", flush=True)
+    s16 = o16.prefill(prompt)
+    print(f"[fullsize] bf16 oracle prefill done", flush=True)
     sess = Session(rt, 1)
     sess.prefill([prompt])
     torch.cuda.synchronize()
     assert rt.status() == 0
+    excused = 0
+    # the first anchor: the device must match the fp32 oracle unless the prompt's
+    # last row is a near tie; from here on both oracles continue from the device's
+    dev_anchor = int(sess.anchor.cpu()[0])
+    b_first, n_first = bound_from_noise(dm.dtype, s16.last_logits[None], s32.last_logits[None])
+    m_first = float(margin_rel(s32.last_logits[None])[0])
+    print(f"[fullsize] first anchor: device {dev_anchor} fp32 oracle {s32.anchor} bf16 oracle {s16.anchor}, "
+          f"fp32 margin {m_first:.3e}, bound {b_first:.3e} (bf16 noise {n_first:.3e})", flush=True)
+    if dev_anchor != s32.anchor:
+        assert m_first <= b_first, f"first anchor differs at a clear margin {m_first:.3e}"
+        excused += 1
+        s32.tokens[-1] = dev_anchor
+    s16.tokens[-1] = dev_anchor
     rng = np.random.default_rng(20260602)
     traj = np.zeros((1, 1), np.int32)
     traj_d = torch.from_numpy(traj).cuda()
     capd = dm.m * dm.d
-    excused = 0
     for r in range(ROUNDS):
         mode = np.zeros((1, B), np.int8)
         tok = rng.integers(0, V, (1, B)).astype(np.int32)
@@ -93,9 +118,8 @@ def test_round_parity_full_width(name):
         def follow(tag):
             def decide(a, bonus, logits):
                 seen[tag] = np.asarray(logits)
-                if (a, bonus) == (g_a, g_bonus):
-                    return a, bonus
-                seen[tag + "_excused"] = (a, bonus)
+                if (a, bonus) != (g_a, g_bonus):
+                    seen[tag + "_differs"] = (a, bonus)
                 return g_a, g_bonus
             return decide
 
@@ -106,21 +130,21 @@ def test_round_parity_full_width(name):
              "captured states": (dev_values(hc, dm.dtype).reshape(B, capd), r32.hcap, r16.hcap),
              "projected features": (dev_values(ft, dm.dtype).reshape(B, dm.d), r32.f, r16.f)}
         bound = {}
-        for name, (dev, ref, ref16) in g.items():
-            noise = rel_rows(ref16, ref).max()
-            bound[name] = min(NOISE_CAP, max(TOL[dm.dtype], NOISE_FACTOR * noise))
+        for qname, (dev, ref, ref16) in g.items():
+            bound[qname], noise = bound_from_noise(dm.dtype, ref16, ref)
             e = rel_rows(dev, ref).max()
-            print(f"[fullsize] r{r} {name}: device vs fp32 oracle {e:.3e}, bf16 oracle vs fp32 oracle {noise:.3e}",
-                  flush=True)
-            assert e <= bound[name], f"r{r} {name}: {e:.3e} > {bound[name]:.3e}"
+            print(f"[fullsize] r{r} {qname}: device vs fp32 oracle {e:.3e}, bf16 oracle vs fp32 oracle "
+                  f"{noise:.3e}, bound {bound[qname]:.3e}", flush=True)
+            assert e <= bound[qname], f"r{r} {qname}: {e:.3e} > {bound[qname]:.3e}"
         np.testing.assert_array_equal(sess.block.cpu().numpy()[0], r32.block, err_msg=f"r{r} block")
-        for name, idx in (("draft logits", sess.draft_tok.cpu().numpy()[0]), ("verify logits", sess.tgt.cpu().numpy()[0])):
-            ref = g[name][1]
-            need = margin_rel(ref) > bound[name]
+        for qname, idx in (("draft logits", sess.draft_tok.cpu().numpy()[0]),
+                           ("verify logits", sess.tgt.cpu().numpy()[0])):
+            ref = g[qname][1]
+            need = margin_rel(ref) > bound[qname]
             bad = need & (idx != np.argmax(ref, axis=-1))
-            assert not bad.any(), f"r{r} {name}: argmax differs at rows {np.where(bad)[0]} with clear margins"
-        if "32_excused" in seen:   # the device's acceptance differs from the fp32 oracle's: only at a near tie
-            a32 = seen["32_excused"][0]
+            assert not bad.any(), f"r{r} {qname}: argmax differs at rows {np.where(bad)[0]} with clear margins"
+        if "32_differs" in seen:   # the device's acceptance differs from the fp32 oracle's: only at a near tie
+            a32 = seen["32_differs"][0]
             crit = margin_rel(seen["32"])[:min(max(a32, g_a), K) + 1]
             assert (crit <= bound["verify logits"]).any(), f"r{r}: acceptance differs at clear margins {crit}"
             excused += 1
@@ -131,5 +155,5 @@ def test_round_parity_full_width(name):
         assert int(sess.seq_len.cpu()[0]) == s32.t
         print(f"[fullsize] round {r}: a={g_a} bonus={g_bonus} n_carry={r32.n_carry}", flush=True)
     assert rt.status() == 0
-    print(f"[fullsize] excused rounds {excused}", flush=True)
+    print(f"[fullsize] excused decisions (near ties) {excused}", flush=True)
     rt.close()

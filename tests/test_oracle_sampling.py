@@ -9,6 +9,8 @@
 * The implemented block rule, run over many independent streams: the first
   emitted token follows p_0, the second (after an acceptance) p_1,
   chi-square at a fixed seed; the Gumbel-max sampler follows softmax(z / T).
+* The first token after a prompt (sample_first): its law softmax(z / T) over
+  many streams, and its counter address, which no round reuses.
 * Special cases: drafter = target accepts every draft; a draft the target
   gives probability 0 is always rejected and never emitted; a tiny
   temperature reduces sampling to the argmax.
@@ -186,6 +188,64 @@ def test_temperature_must_be_positive():
     for bad in (0.0, -1.0, float("inf"), float("nan")):
         with pytest.raises(ValueError):
             sp.inv_temperature(bad)
+
+
+# ------------------------------------------------------------ the first token after a prompt
+def _first_and_round(seed, stream, z, t_last):
+    """The prompt's first token (sample_first at position t_last) and the first
+    draft of the round that follows (anchor at t_last + 1), both drawn from
+    the same logits row."""
+    inv_t = sp.inv_temperature(1.0)
+    first = sp.sample_first(z, inv_t, seed, stream, t_last)
+    d, _, _ = sp.sample_drafts(z[None], inv_t, seed, stream, t_last + 1)
+    return first, int(d[0])
+
+
+@pytest.mark.parametrize("T", [1.0, 0.7])
+def test_sample_first_law(T):
+    """The first token after a prompt follows softmax(z / T) over independent
+    streams (chi-square), and a vanishing temperature makes it the argmax."""
+    z = _rows(31, 1)[0]
+    inv_t = sp.inv_temperature(T)
+    s = np.array([sp.sample_first(z, inv_t, 13, st, 77) for st in range(N_TRIALS)])
+    assert _chi2_p(s, _softmax64(z / T)) > 1e-3
+    assert all(sp.sample_first(z, sp.inv_temperature(1e-4), 13, st, 77) == int(np.argmax(z)) for st in range(20))
+
+
+def test_sample_first_counter_is_disjoint_from_the_rounds(monkeypatch):
+    """The first token's random numbers are addressed at (t_last, 0, correction),
+    which no round addresses: rounds start at t_last + 1 and draw corrections
+    at block indices >= 1.  Recorded over a sampled round, no counter repeats,
+    and over many streams the first token and the following round's first
+    draft (same logits row) agree at the rate of independent draws, sum p^2,
+    not always as shared numbers would make them."""
+    seen = []
+    real = sp.uniforms
+    monkeypatch.setattr(sp, "uniforms", lambda seed, stream, pos, row, purpose, n:
+                        seen.append((pos, row, purpose)) or real(seed, stream, pos, row, purpose, n))
+    z = _rows(32, 1)[0]
+    sp.sample_first(z, np.float32(1), 3, 0, 40)
+    first_addr = set(seen)
+    seen.clear()
+    tgt = _rows(33, 4)
+    d, _, _ = sp.sample_drafts(tgt[:3], np.float32(1), 3, 0, 41)
+    sp.accept_sampled([1] + list(d), tgt, tgt[:3], np.float32(1), 3, 0, 41)
+    assert first_addr == {(40, 0, sp.RESAMPLE)} and not first_addr & set(seen)
+    monkeypatch.setattr(sp, "uniforms", real)
+    p = _softmax64(z)
+    same = np.mean([a == b for a, b in (_first_and_round(5, st, z, 40) for st in range(N_TRIALS))])
+    assert abs(same - (p * p).sum()) < 0.03, (same, (p * p).sum())
+
+
+def test_mutation_first_token_reuses_the_rounds_numbers(monkeypatch):
+    """Planted mistake: the first token addressed like the next round's first
+    draft.  The agreement-rate pin catches it."""
+    monkeypatch.setattr(sp, "sample_first", lambda z, inv_t, seed, stream, t_last: int(
+        sp.sample_drafts(np.asarray(z)[None], inv_t, seed, stream, t_last + 1)[0][0]))
+    z = _rows(32, 1)[0]
+    p = _softmax64(z)
+    same = np.mean([a == b for a, b in (_first_and_round(5, st, z, 40) for st in range(500))])
+    assert abs(same - (p * p).sum()) > 0.3
 
 
 # ------------------------------------------------------------ planted mistakes

@@ -169,6 +169,31 @@ def make_prompts(wl: Workload) -> List[np.ndarray]:
     return out
 
 
+def balanced_capped_geometric(rng: np.random.Generator, R: int, q: float, cap: int) -> np.ndarray:
+    """R draws of a = min(G, cap), P(G = k) = (1-q) q^k, arranged so that every
+    prefix of the rounds realises close to the distribution's mean.
+
+    The values are the distribution's quantiles at the stratified points
+    u_i = (i + 1/2) / R (through the inverse CDF G = floor(log(1-u) / log q));
+    they are then ordered greedily, each round taking the remaining value that
+    keeps the running sum closest to n times their mean (ties broken by a
+    seeded shuffle).  The multiset follows the law; the order bounds the
+    prefix error by cap / n, so a short timed run measures the configured
+    acceptance instead of whatever a few pseudo-random draws happened to be.
+    """
+    u = (np.arange(R) + 0.5) / R
+    vals = np.minimum(np.floor(np.log1p(-u) / np.log(q)), cap).astype(np.int64)
+    target = vals.mean()
+    pool = [int(v) for v in rng.permutation(vals)]
+    out = np.empty(R, np.int64)
+    s = 0
+    for n in range(R):
+        i = min(range(len(pool)), key=lambda j: abs(s + pool[j] - (n + 1) * target))
+        out[n] = pool.pop(i)
+        s += int(out[n])
+    return out
+
+
 # forcing modes for draft position j of round r, sequence s
 FORCE_RANDOM, FORCE_TRAJ, FORCE_MISMATCH = 0, 1, 2
 
@@ -193,8 +218,7 @@ def make_schedule(wl: Workload, rounds: int | None = None) -> Dict[str, np.ndarr
         mode[:] = np.where(coin < wl.sched_param, FORCE_TRAJ, FORCE_RANDOM)
     elif wl.schedule == "geometric":
         q = wl.sched_param / (1.0 + wl.sched_param)
-        G = r.geometric(1.0 - q, size=(R, b)) - 1          # P(G=k) = (1-q) q^k, k >= 0
-        a = np.minimum(G, K).astype(np.int32)
+        a = np.stack([balanced_capped_geometric(r, R, q, K) for _ in range(b)], axis=1).astype(np.int32)
         accept[:] = a
         j = np.arange(B)[None, None, :]
         mode[:] = np.where(j <= a[..., None], FORCE_TRAJ,
