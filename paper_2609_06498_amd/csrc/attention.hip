@@ -227,8 +227,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     const gu4* vg = (const gu4*)(reinterpret_cast<const T*>(p.vpool) + off);
 #pragma unroll
     for (int it = 0; it < PER; ++it) {
-      kr[i][it] = kg[threadIdx.x + it * NT];
-      vr[i][it] = vg[threadIdx.x + it * NT];
+      kr[i][it] = __builtin_nontemporal_load(&kg[threadIdx.x + it * NT]);   // each page is read once per launch
+      vr[i][it] = __builtin_nontemporal_load(&vg[threadIdx.x + it * NT]);
     }
     __builtin_amdgcn_sched_barrier(0);        // issue order = page order = consumption order
   }
