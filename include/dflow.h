@@ -304,6 +304,24 @@ int dflow_sample_draft(dflow_ctx* ctx, hipStream_t stream, int nseq, const float
                        const int32_t* anchor_tok, const int32_t* anchor_pos, const dflow_sampler* smp,
                        int32_t* draft_tok, int32_t* block_out);
 
+/* Allocation-free variant of dflow_sample_draft, for callers that cannot
+ * allocate or provide device memory for a call's scratch (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments, outputs and random-number addressing as dflow_sample_draft, and
+ * bit-identical drafts; the per-chunk draw keys (nseq * (block - 1) *
+ * ceil(vocab / 1024) 8-byte keys) go to a fixed device array of the library,
+ * DFLOW_SAMPLE_SCRATCH_BYTES on every GPU it runs on, held until the process
+ * ends, instead of the context's workspace.  A request needing more returns
+ * DFLOW_ECAPACITY before any launch (at the Qwen3 vocabulary: up to 879 drawn
+ * rows, 58 sequences at block 16).  The call allocates nothing.  Every call on
+ * one GPU shares that GPU's array, which keeps the last call's keys: calls
+ * that overlap on one GPU (streams not ordered against each other) race on it
+ * and must not be issued. */
+#define DFLOW_SAMPLE_SCRATCH_BYTES (1u << 20)
+int dflow_sample_draft_noalloc(dflow_ctx* ctx, hipStream_t stream, int nseq, const float* draft_logits,
+                               const int32_t* anchor_tok, const int32_t* anchor_pos, const dflow_sampler* smp,
+                               int32_t* draft_tok, int32_t* block_out);
+
 /* Prompt processing for sampling decoding: dflow_prefill, except that the
  * first token is drawn from softmax(z / T) of the prompt's last row with the
  * Philox counter (len - 1, 0, 2, column / 4) and key (seed, smp->stream[0]):

@@ -89,6 +89,7 @@ static constexpr int CLS_ATTN = 7;
 static constexpr int MAX_ROWS = 1024;
 
 static constexpr int PROF_MAX = 16384;
+static_assert(DFLOW_SAMPLE_SCRATCH_BYTES == SAMPLE_SCRATCH_BYTES, "the header states the scratch size");
 
 extern "C" const char* dflow_last_error(void) { return g_err.c_str(); }
 
@@ -325,6 +326,14 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
     for (size_t p = 0; p < npos; ++p) {
       const double a = (double)p * inv;
       tab[p * half + i] = make_float2((float)std::cos(a), (float)std::sin(a));
+    }
+  }
+  {   // the device address of the allocation-free sampling call's scratch, resolved on this device now
+    void* sp = nullptr;
+    const hipError_t es = sample_scratch(&sp);
+    if (es != hipSuccess) {
+      delete c;
+      return fail(DFLOW_EHIP, "create: scratch symbol: %s", hipGetErrorString(es));
     }
   }
   // set-up on the caller's stream: clear the workspace and the status word,
@@ -768,6 +777,25 @@ extern "C" int dflow_sample_draft(dflow_ctx* c, hipStream_t st, int nseq, const 
   SampleArgs a;
   if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
   HIPCHK(launch_sample_draft(draft_logits, a, nseq, c->dm.block, anchor_tok, draft_tok, block_out, c->samp, st));
+  return DFLOW_OK;
+}
+
+extern "C" int dflow_sample_draft_noalloc(dflow_ctx* c, hipStream_t st, int nseq, const float* draft_logits,
+                                          const int32_t* anchor_tok, const int32_t* anchor_pos,
+                                          const dflow_sampler* smp, int32_t* draft_tok, int32_t* block_out) {
+  int rc = check_nseq(c, nseq);
+  if (rc) return rc;
+  if (!draft_logits || !anchor_tok || !draft_tok) return fail(DFLOW_EINVAL, "sample_draft_noalloc: null argument");
+  SampleArgs a;
+  if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
+  const size_t need = (size_t)nseq * (c->dm.block - 1) * samp_chunks(c->dm.vocab) * sizeof(uint64_t);
+  if (need > SAMPLE_SCRATCH_BYTES)
+    return fail(DFLOW_ECAPACITY, "sample_draft_noalloc: %zu bytes of draw keys (%d sequences x %d rows x %d chunks) "
+                                 "exceed the fixed scratch of %zu bytes", need, nseq, c->dm.block - 1,
+                samp_chunks(c->dm.vocab), SAMPLE_SCRATCH_BYTES);
+  void* ws = nullptr;
+  HIPCHK(sample_scratch(&ws));
+  HIPCHK(launch_sample_draft(draft_logits, a, nseq, c->dm.block, anchor_tok, draft_tok, block_out, ws, st));
   return DFLOW_OK;
 }
 

@@ -110,6 +110,12 @@ size_t samp_workspace_bytes(int V, int rows, int nseq);
 // drafts d_i ~ softmax(z_i) of drafter logits rows s*B + i (i = 1..K)
 hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq, int B, const int* anchor,
                                int* draft_tok, int* block_out, void* ws, hipStream_t st);
+// Fixed scratch of the allocation-free draft sampling call: the draw keys in a
+// file-scope device array (one copy per GPU).  sample_scratch resolves the
+// array's device address on the current device (once per device, cached) and
+// returns it with its size in bytes.
+constexpr size_t SAMPLE_SCRATCH_BYTES = (size_t)1 << 20;
+hipError_t sample_scratch(void** ptr);
 // first token after a prompt: out[0] ~ softmax(row / T), counter (pos[0], 0, 2, column / 4)
 hipError_t launch_sample_first(const float* row, const SampleArgs& a, int* out, void* ws, hipStream_t st);
 // rollout: trajectory tokens as acceptance targets, and the decayed drafter loss

@@ -25,6 +25,8 @@
 // (1024-column chunk, row); a lane handles one group of four columns (one
 // Philox block and one 16-byte load), so a Qwen3 vocabulary row spreads over
 // 149 workgroups.  Chunk partials are folded by one wave per row or sequence.
+#include <mutex>
+
 #include "common.h"
 #include "kernels.h"
 #include "round_state.h"
@@ -483,6 +485,34 @@ hipError_t launch_sample_draft(const float* dlog, const SampleArgs& a, int nseq,
   hipLaunchKernelGGL(draw_finish_kernel, dim3((rows + 3) / 4), dim3(256), 0, st, part, rows, p.chunks, B,
                      anchor, draft_tok, block_out);
   return hipGetLastError();
+}
+
+// The allocation-free draft sampling call keeps its draw keys here instead of
+// in a context workspace.  The name is a host-side stand-in for the device
+// array: host code only ever passes the address hipGetSymbolAddress returns.
+static __device__ __align__(256) uint64_t scratch[SAMPLE_SCRATCH_BYTES / sizeof(uint64_t)];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[SCRATCH_MAX_DEVICES] = {};
+}  // namespace
+
+hipError_t sample_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {   // first use on this device: resolve the device's own copy
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_sample_first(const float* row, const SampleArgs& a, int* out, void* ws, hipStream_t st) {

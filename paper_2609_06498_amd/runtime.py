@@ -90,6 +90,9 @@ EXPORTS = {
     "dflow_sample_draft": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Sampler),
                                           ctypes.c_void_p, ctypes.c_void_p]),
+    "dflow_sample_draft_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Sampler),
+                                                  ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_accept_sampled": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.POINTER(Sampler), ctypes.c_void_p, ctypes.c_void_p,
@@ -316,6 +319,13 @@ class Runtime:
         self._check(self.lib.dflow_sample_draft(self.ctx, _stream(), nseq, _ptr(draft_logits), _ptr(anchor_tok),
                                                 _ptr(anchor_pos), ctypes.byref(sampler), _ptr(draft_tok),
                                                 _ptr(block_out)), "dflow_sample_draft")
+
+    def sample_draft_noalloc(self, nseq, draft_logits, anchor_tok, anchor_pos, sampler, draft_tok, block_out=None):
+        """dflow_sample_draft with the draw keys in the library's fixed device scratch (no workspace)."""
+        self._check(self.lib.dflow_sample_draft_noalloc(self.ctx, _stream(), nseq, _ptr(draft_logits),
+                                                        _ptr(anchor_tok), _ptr(anchor_pos), ctypes.byref(sampler),
+                                                        _ptr(draft_tok), _ptr(block_out)),
+                    "dflow_sample_draft_noalloc")
 
     def accept_sampled(self, nseq, block_tok, anchor_pos, logits, draft_logits, sampler, accept_len, bonus,
                        committed, n_carry, feat=None):
