@@ -73,6 +73,15 @@ struct dflow_ctx {
   void* samp;            // sampling decoding partials
   float* samp_row;       // [vocab] logits of the last prompt row (dflow_prefill_sampled)
   float* kpart;          // K-part partial sums of the split residual and gate/up GEMMs
+  // Matrix-core-order copies of the skinny projections' A operands (FRAG_MAX_ROWS
+  // rows each): x (QKV, gate/up, LM heads), attention output (O), SwiGLU /
+  // relay hidden (down, relay W2), captured states (W_c), relay input (W1),
+  // projected features (drafter context K/V).  Used by the round's calls when
+  // nseq * block <= FRAG_MAX_ROWS (frag); a copy is read only by the call
+  // that wrote it, or -- captured states, features -- by the next call of the
+  // round (accept after verify, commit after accept).
+  void *xf, *attnf, *actf, *hcapf, *uf, *ff;
+  bool frag = false;
 
   // kernel timing record (dflow_profile)
   bool prof = false;
@@ -144,7 +153,7 @@ int validate(const dflow_dims* d) {
 }
 
 struct Layout {
-  size_t off[32];
+  size_t off[40];
   size_t total;
 };
 
@@ -212,6 +221,15 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
       if (r > need) need = r;
     }
     add(need);
+  }
+  {   // 27..32 matrix-core-order operand copies of FRAG_MAX_ROWS rows
+    const size_t fr = (size_t)FRAG_MAX_ROWS * elt;
+    add(fr * d->d);                                       // 27 x
+    add(fr * qd);                                         // 28 attention output
+    add(fr * (d->ffn > d->relay_hidden ? d->ffn : d->relay_hidden));   // 29 SwiGLU / relay hidden
+    add(fr * d->n_capture * d->d);                        // 30 captured states
+    add(fr * 3 * d->d);                                   // 31 relay input
+    add(fr * d->d);                                       // 32 projected features
   }
   L.total = o;
   if (nsplit_out) *nsplit_out = nsplit;
@@ -314,6 +332,12 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->samp = b + L.off[24];
   c->samp_row = (float*)(b + L.off[25]);
   c->kpart = (float*)(b + L.off[26]);
+  c->xf = b + L.off[27];
+  c->attnf = b + L.off[28];
+  c->actf = b + L.off[29];
+  c->hcapf = b + L.off[30];
+  c->uf = b + L.off[31];
+  c->ff = b + L.off[32];
   c->u = c->xn;
   c->hid = c->act;
 
@@ -371,11 +395,24 @@ struct NormIn {            // RMSNorm of the A rows: per-strip sums of squares; 
   const float* ssq = nullptr;
 };
 
+struct Frag {              // matrix-core-order A operand and output copies (skinny launches only)
+  const void* a = nullptr;
+  FragOut y{}, y2{};
+};
+
+// copy of `cols` columns at c0 of a K-wide consumer operand, when the call uses them
+FragOut fout(const dflow_ctx* c, void* buf, int K, int c0 = 0) {
+  return c->frag ? FragOut{buf, K / c->KT, c0} : FragOut{nullptr, 0, 0};
+}
+
 hipError_t gemm(dflow_ctx* c, hipStream_t st, int epi, const void* A, int lda, const void* W, int M, int N, int K,
                 void* Y, int ldy, const void* R = nullptr, int ldr = 0, void* Y2 = nullptr, int ldy2 = 0,
                 const void* bias = nullptr, float* logits = nullptr, int ldl = 0, NormIn nin = NormIn(),
-                float* ssq_out = nullptr, int ksplit = 1) {
+                float* ssq_out = nullptr, int ksplit = 1, Frag fr = Frag()) {
   GemmParams p{};
+  p.Af = fr.a;
+  p.yf = fr.y;
+  p.y2f = fr.y2;
   p.ksplit = ksplit;
   p.y_part = (size_t)M * ldy;
   if (nin.ssq) {
@@ -462,6 +499,7 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
   a.part_o = c->part_o;
   a.part_ml = c->part_ml;
   a.out = c->attn;
+  a.outf = fout(c, c->attnf, c->q_dim);
   const bool rec = c->prof && c->n_ev < PROF_MAX;
   hipError_t e;
   if (rec && (e = hipEventRecord(c->ev0[c->n_ev], st)) != hipSuccess) return e;
@@ -501,7 +539,8 @@ RopeParams rope_params(dflow_ctx* c, const dflow_layer& L, int nseq, int Bq, int
 
 // One Qwen3-style decoder layer over x (M = nseq*Bq rows) in place.
 hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nseq, int Bq, const int* start_pos,
-                         const int* page_table, void* kpool, void* vpool, int causal, void* capture) {
+                         const int* page_table, void* kpool, void* vpool, int causal, void* capture,
+                         FragOut capf = FragOut{nullptr, 0, 0}) {
   const dflow_dims& d = c->dm;
   const int M = nseq * Bq;
   hipError_t e;
@@ -514,8 +553,21 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   ffn_n.ssq = c->ssq;
   // QKV projection as fp32 partial sums over qkv_ks K parts (spreads the
   // weight stream evenly over the compute units); its consumers add them
+  // matrix-core-order operands (skinny rounds): x from its producer, the
+  // attention output from the combine kernel, the SwiGLU output from gate/up
+  Frag fq, fo, fgu, fdn;
+  if (c->frag) {
+    fq.a = c->xf;
+    fo.a = c->attnf;
+    fo.y = fout(c, c->xf, d.d);
+    fgu.a = c->xf;
+    fgu.y = fout(c, c->actf, d.ffn);
+    fdn.a = c->actf;
+    fdn.y = fout(c, c->xf, d.d);
+    fdn.y2 = capf;
+  }
   if ((e = gemm(c, st, EPI_STORE_F32, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
-                nullptr, nullptr, 0, attn_n, nullptr, c->qkv_ks)))
+                nullptr, nullptr, 0, attn_n, nullptr, c->qkv_ks, fq)))
     return e;
   const bool fused = attention_fuses_rope(c->bf, Bq, c->G, d.head_dim);
   if (!fused) {
@@ -527,14 +579,14 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   }
   if ((e = attention(c, st, L, nseq, Bq, start_pos, page_table, kpool, vpool, causal, fused))) return e;
   if ((e = gemm(c, st, EPI_RESID, c->attn, c->q_dim, L.wo, M, d.d, c->q_dim, c->x, d.d, c->x, d.d, nullptr, 0,
-                nullptr, nullptr, 0, NormIn(), c->ssq)))
+                nullptr, nullptr, 0, NormIn(), c->ssq, 1, fo)))
     return e;
   if ((e = gemm(c, st, EPI_SWIGLU, c->x, d.d, L.wgu, M, 2 * d.ffn, d.d, c->act, d.ffn, nullptr, 0, nullptr, 0,
-                nullptr, nullptr, 0, ffn_n)))
+                nullptr, nullptr, 0, ffn_n, nullptr, 1, fgu)))
     return e;
   const int capld = d.n_capture * d.d;
   if ((e = gemm(c, st, EPI_RESID, c->act, d.ffn, L.wdown, M, d.d, d.ffn, c->x, d.d, c->x, d.d, capture, capld,
-                nullptr, nullptr, 0, NormIn(), c->ssq)))
+                nullptr, nullptr, 0, NormIn(), c->ssq, 1, fdn)))
     return e;
   return hipSuccess;
 }
@@ -548,9 +600,13 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
   int ci = 0;
   for (int l = 0; l < d.n_layers; ++l) {
     void* cap = nullptr;
-    if (ci < d.n_capture && d.capture_layers[ci] == l) cap = (char*)c->hcap + (size_t)ci++ * d.d * c->elt;
+    FragOut capf{nullptr, 0, 0};
+    if (ci < d.n_capture && d.capture_layers[ci] == l) {
+      capf = fout(c, c->hcapf, d.n_capture * d.d, ci * d.d);
+      cap = (char*)c->hcap + (size_t)ci++ * d.d * c->elt;
+    }
     if ((e = decoder_layer(c, st, c->layers[l], nseq, Bq, start_pos, page_table, pool_layer(c, c->c.k_pool, l),
-                           pool_layer(c, c->c.v_pool, l), 1, cap)))
+                           pool_layer(c, c->c.v_pool, l), 1, cap, capf)))
       return e;
   }
   if (!argmax_out && !logits) return hipSuccess;
@@ -559,20 +615,27 @@ hipError_t target_forward(dflow_ctx* c, hipStream_t st, int nseq, int Bq, const 
   const size_t off = (size_t)lm_row0 * d.d * c->elt;
   NormIn fin;
   fin.ssq = c->ssq + (size_t)lm_row0 * SSQ_LD;
+  Frag flm;
+  if (c->frag && lm_row0 == 0) flm.a = c->xf;
   if ((e = gemm(c, st, EPI_ARGMAX, (char*)c->x + off, d.d, c->w.lm_head, lm_rows, d.vocab, d.d, nullptr, 0, nullptr,
-                0, nullptr, 0, nullptr, logits, d.vocab, fin)))
+                0, nullptr, 0, nullptr, logits, d.vocab, fin, nullptr, 1, flm)))
     return e;
   if (!argmax_out) return hipSuccess;
   return launch_argmax_reduce(c->amax, c->lm_groups, lm_rows, c->amax_part, c->counters, argmax_out, nullptr, st);
 }
 
 // F = RMSNorm(W_c [captured states]) for M rows -> fout (storage type)
-hipError_t project(dflow_ctx* c, hipStream_t st, int M, void* fout) {
+hipError_t project(dflow_ctx* c, hipStream_t st, int M, void* out) {
   const dflow_dims& d = c->dm;
   hipError_t e;
   const int K = d.n_capture * d.d;
-  if ((e = gemm(c, st, EPI_STORE_F32, c->hcap, K, c->w.w_c, M, d.d, K, c->fproj, d.d))) return e;
-  return launch_rmsnorm(c->bf, true, c->fproj, d.d, M, d.d, c->w.g_c, d.rms_eps, fout, d.d, st);
+  Frag fr;
+  if (c->frag) fr.a = c->hcapf;
+  if ((e = gemm(c, st, EPI_STORE_F32, c->hcap, K, c->w.w_c, M, d.d, K, c->fproj, d.d, nullptr, 0, nullptr, 0,
+                nullptr, nullptr, 0, NormIn(), nullptr, 1, fr)))
+    return e;
+  return launch_rmsnorm(c->bf, true, c->fproj, d.d, M, d.d, c->w.g_c, d.rms_eps, out, d.d, fout(c, c->ff, d.d),
+                        st);
 }
 
 // Drafter context K/V of feature rows (nseq x Bq) at start_pos + j for rows j <= row_limit[s].
@@ -585,7 +648,11 @@ hipError_t ctx_append(dflow_ctx* c, hipStream_t st, const void* feat, int nseq, 
   const int M = nseq * Bq;
   const int ncols = d.n_draft_layers * 2 * c->kv_dim;
   hipError_t e;
-  if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, c->w.draft_wkv_ctx, M, ncols, d.d, c->ctxkv, ncols))) return e;
+  Frag fr;
+  if (c->frag) fr.a = c->ff;
+  if ((e = gemm(c, st, EPI_STORE_T, feat, d.d, c->w.draft_wkv_ctx, M, ncols, d.d, c->ctxkv, ncols, nullptr, 0,
+                nullptr, 0, nullptr, nullptr, 0, NormIn(), nullptr, 1, fr)))
+    return e;
   RopeParams r{};
   r.qkv = c->ctxkv;
   r.ld = ncols;
@@ -632,6 +699,7 @@ int prefill_impl(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int 
   if ((long long)len + c->dm.block > (long long)c->dm.max_pages * PAGE)
     return fail(DFLOW_ECAPACITY, "prefill: %d tokens exceed the page table (%d)", len, c->dm.max_pages * PAGE);
   c->phase = DFLOW_PHASE_PREFILL;
+  c->frag = false;
   SampleArgs sa;
   if (smp) {
     // counter word 0 of the first draw: the prompt's last position (held in tmp_pos[1])
@@ -644,7 +712,8 @@ int prefill_impl(dflow_ctx* c, hipStream_t st, int seq, const int32_t* tok, int 
     const int n = (len - p0) < d.max_rows ? (len - p0) : d.max_rows;
     const bool last = p0 + n >= len;
     HIPCHK(launch_set_int(c->tmp_pos, p0, st));
-    HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
+    HIPCHK(launch_embed(c->bf, tok + p0, n, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD,
+                        FragOut{nullptr, 0, 0}, st));
     int* amax = last && !smp ? c->tmp_argmax : nullptr;
     float* lrow = last && smp ? c->samp_row : nullptr;
     HIPCHK(target_forward(c, st, 1, n, c->tmp_pos, pt, amax, lrow, n - 1, 1));
@@ -699,23 +768,33 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   c->phase = DFLOW_PHASE_DRAFT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
+  c->frag = M <= FRAG_MAX_ROWS;
   if (carry_on) {
-    HIPCHK(launch_relay_gather(c->bf, 1, c->carry_rec, c->w.embed, c->f, nseq, B, d.d, d.vocab, c->u, st));
+    Frag f1, f2;
+    if (c->frag) {
+      f1.a = c->uf;
+      f1.y = fout(c, c->actf, d.relay_hidden);
+      f2.a = c->actf;
+    }
+    HIPCHK(launch_relay_gather(c->bf, 1, c->carry_rec, c->w.embed, c->f, nseq, B, d.d, d.vocab, c->u,
+                               fout(c, c->uf, 3 * d.d), st));
     HIPCHK(gemm(c, st, EPI_BIAS_SILU, c->u, 3 * d.d, c->w.relay_w1, M, d.relay_hidden, 3 * d.d, c->hid,
-                d.relay_hidden, nullptr, 0, nullptr, 0, c->w.relay_c1));
+                d.relay_hidden, nullptr, 0, nullptr, 0, c->w.relay_c1, nullptr, 0, NormIn(), nullptr, 1, f1));
     HIPCHK(gemm(c, st, EPI_BIAS_F32, c->hid, d.relay_hidden, c->w.relay_w2, M, 2 * d.d, d.relay_hidden, c->bg,
-                2 * d.d, nullptr, 0, nullptr, 0, c->w.relay_c2));
+                2 * d.d, nullptr, 0, nullptr, 0, c->w.relay_c2, nullptr, 0, NormIn(), nullptr, 1, f2));
   }
   HIPCHK(launch_relay_input(c->bf, carry_on ? 1 : 0, c->carry_rec, anchor_tok, c->w.embed, c->w.e_mask, c->f, c->bg,
                             c->w.relay_ln_g, c->w.relay_ln_b, d.ln_eps, nseq, B, d.d, d.vocab, c->x, c->status,
-                            c->ssq, SSQ_LD, st));
+                            c->ssq, SSQ_LD, fout(c, c->xf, d.d), st));
   for (int l = 0; l < d.n_draft_layers; ++l)
     HIPCHK(decoder_layer(c, st, c->dlayers[l], nseq, B, anchor_pos, c->c.page_table, pool_layer(c, c->c.ck_pool, l),
                          pool_layer(c, c->c.cv_pool, l), 0, nullptr));
   NormIn fin;
   fin.ssq = c->ssq;
+  Frag flm;
+  if (c->frag) flm.a = c->xf;
   HIPCHK(gemm(c, st, EPI_ARGMAX, c->x, d.d, c->w.draft_lm_head, M, d.vocab, d.d, nullptr, 0, nullptr, 0, nullptr, 0,
-              nullptr, draft_logits, d.vocab, fin));
+              nullptr, draft_logits, d.vocab, fin, nullptr, 1, flm));
   if (!draft_tok && !block_out) return DFLOW_OK;
   const DraftOut dr{anchor_tok, B, draft_tok, block_out};
   HIPCHK(launch_argmax_reduce(c->amax, c->lm_groups, M, c->amax_part, c->counters, nullptr, &dr, st));
@@ -730,7 +809,9 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
   c->phase = DFLOW_PHASE_VERIFY;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD, st));
+  c->frag = M <= FRAG_MAX_ROWS;
+  HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD,
+                      fout(c, c->xf, d.d), st));
   HIPCHK(target_forward(c, st, nseq, B, start_pos, c->c.page_table, tgt_argmax, logits));
   if (hcap)
     HIPCHK(hipMemcpyAsync(hcap, c->hcap, (size_t)M * d.n_capture * d.d * c->elt, hipMemcpyDeviceToDevice, st));
@@ -747,6 +828,7 @@ extern "C" int dflow_accept_and_carry(dflow_ctx* c, hipStream_t st, int nseq, co
   c->phase = DFLOW_PHASE_ACCEPT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
+  c->frag = M <= FRAG_MAX_ROWS;
   HIPCHK(launch_accept(block_tok, tgt_argmax, nseq, B, d.carry_window, accept_len, bonus, committed, n_carry,
                        c->carry_rec, st));
   HIPCHK(project(c, st, M, c->f));
@@ -812,6 +894,7 @@ extern "C" int dflow_accept_sampled(dflow_ctx* c, hipStream_t st, int nseq, cons
   if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
+  c->frag = M <= FRAG_MAX_ROWS;
   HIPCHK(launch_accept_sampled(logits, draft_logits, block_tok, a, nseq, B, d.carry_window, accept_len, bonus,
                                committed, n_carry, c->carry_rec, c->status, c->samp, st));
   HIPCHK(project(c, st, M, c->f));
@@ -849,6 +932,7 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
   if (rc) return rc;
   if (!accept_len || !seq_len) return fail(DFLOW_EINVAL, "kv_commit: null argument");
   c->phase = DFLOW_PHASE_COMMIT;
+  c->frag = nseq * c->dm.block <= FRAG_MAX_ROWS;
   HIPCHK(ctx_append(c, st, c->f, nseq, c->dm.block, seq_len, accept_len, c->c.page_table));
   HIPCHK(launch_commit(accept_len, nseq, seq_len, st));
   return DFLOW_OK;

@@ -490,6 +490,7 @@ __global__ void __launch_bounds__(DH) attn_combine_kernel(AttnParams p) {
   }
   const float v = lsum > 0.f ? acc / lsum : 0.f;
   TT<T>::st(reinterpret_cast<T*>(p.out), (size_t)row * p.Hq * DH + hq * DH + d, v);
+  frag_st<T>(p.outf, row, hq * DH + d, v);
 }
 
 // Dynamic LDS of the attention kernel: the split's K and V pages, plus the

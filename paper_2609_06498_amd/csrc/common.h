@@ -2,6 +2,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include "gemm.h"
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
@@ -59,6 +60,24 @@ template <> struct TT<float> {
   __device__ static inline void st(float* p, size_t i, float v) { p[i] = v; }
   __device__ static inline float rnd(float v) { return v; }
 };
+
+// Matrix-core operand order of an activation block [rows][K] (the A operand
+// of a skinny projection): 16-row tiles of KT columns, 1 KB per (row tile, k
+// tile), lane l holding KL consecutive k values of row l%16 at k chunk l/16 --
+// one contiguous 16-byte load per lane, the k tiles of a row tile adjacent.
+// A producer that feeds a projection of at most FRAG_MAX_ROWS rows writes this
+// copy besides its row-major output; ktiles = K/KT of the consumer and c0 the
+// producer's first column within the consumer's K (the capture layers write
+// their slices of the W_c input).
+template <typename T>
+__device__ inline size_t afrag_off(int m, int c, int ktiles) {
+  constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
+  return ((((size_t)(m >> 4) * ktiles + c / KT) * 64 + ((c % KT) / KL) * 16 + (m & 15)) * KL) + (c % KL);
+}
+template <typename T>
+__device__ inline void frag_st(const FragOut& f, int m, int c, float v) {
+  if (f.p) TT<T>::st(reinterpret_cast<T*>(f.p), afrag_off<T>(m, f.c0 + c, f.ktiles), v);
+}
 
 // 16 consecutive elements (16-byte aligned) <-> fp32, stores rounded to the storage type
 template <typename T> struct Row16;

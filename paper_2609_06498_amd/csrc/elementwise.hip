@@ -12,7 +12,8 @@ namespace dflow {
 // Also writes the per-16-column-strip sums of squares of the row (the
 // RMSNorm row scale of the next projection), ssq[row * ssq_ld + c].
 template <typename T>
-__global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, int* status, float* ssq, int ssq_ld) {
+__global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, int* status, float* ssq, int ssq_ld,
+                             FragOut of) {
   const int row = blockIdx.x;
   int t = tok[row];
   const bool ok = t >= 0 && t < V;
@@ -24,6 +25,7 @@ __global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, i
       const size_t i = (size_t)c * 16 + e;
       const float v = ok ? TT<T>::ld(E, (size_t)t * d + i) : 0.f;
       TT<T>::st(out, (size_t)row * d + i, v);
+      frag_st<T>(of, row, (int)i, v);
       sq += v * v;
     }
     if (ssq) ssq[(size_t)row * ssq_ld + c] = sq;
@@ -31,15 +33,15 @@ __global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, i
 }
 
 hipError_t launch_embed(bool isbf, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
-                        float* ssq, int ssq_ld, hipStream_t s) {
+                        float* ssq, int ssq_ld, FragOut of, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (d % 16) return hipErrorInvalidValue;
   if (isbf)
     hipLaunchKernelGGL(embed_kernel<bf16>, dim3(M), dim3(256), 0, s, tok, (const bf16*)E, V, d, (bf16*)out, status,
-                       ssq, ssq_ld);
+                       ssq, ssq_ld, of);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, tok, (const float*)E, V, d, (float*)out,
-                       status, ssq, ssq_ld);
+                       status, ssq, ssq_ld, of);
   return hipGetLastError();
 }
 
@@ -66,7 +68,7 @@ template <> struct Vec16<float> {
 
 template <typename T, typename TI>
 __global__ void __launch_bounds__(256) rmsnorm_kernel(const TI* x, int ldx, int d, const T* g, float eps, T* out,
-                                                      int ldo) {
+                                                      int ldo, FragOut of) {
   constexpr int VN = Vec16<TI>::N;
   constexpr int RV = 4;                       // vectors held per thread (d <= 256*RV*VN)
   __shared__ float sh[32];
@@ -98,29 +100,37 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const TI* x, int ldx, int 
     const int i = threadIdx.x + r * blockDim.x;
     if (i < nv)
 #pragma unroll
-      for (int e = 0; e < VN; ++e) TT<T>::st(o, (size_t)i * VN + e, v[r][e] * rs * TT<T>::ld(g, (size_t)i * VN + e));
+      for (int e = 0; e < VN; ++e) {
+        const float y = v[r][e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
+        TT<T>::st(o, (size_t)i * VN + e, y);
+        frag_st<T>(of, row, i * VN + e, y);
+      }
   }
   for (int i = threadIdx.x + RV * blockDim.x; i < nv; i += blockDim.x) {
     float t[VN];
     Vec16<TI>::load(xr + (size_t)i * VN, t);
 #pragma unroll
-    for (int e = 0; e < VN; ++e) TT<T>::st(o, (size_t)i * VN + e, t[e] * rs * TT<T>::ld(g, (size_t)i * VN + e));
+    for (int e = 0; e < VN; ++e) {
+      const float y = t[e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
+      TT<T>::st(o, (size_t)i * VN + e, y);
+      frag_st<T>(of, row, i * VN + e, y);
+    }
   }
 }
 
 hipError_t launch_rmsnorm(bool isbf, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
-                          void* out, int ldo, hipStream_t s) {
+                          void* out, int ldo, FragOut of, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if ((d & 7) || (ldx & 7)) return hipErrorInvalidValue;   // 16-byte row vectors
   if (isbf && in_f32)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, float>), dim3(M), dim3(256), 0, s, (const float*)x, ldx, d,
-                       (const bf16*)g, eps, (bf16*)out, ldo);
+                       (const bf16*)g, eps, (bf16*)out, ldo, of);
   else if (isbf)
     hipLaunchKernelGGL((rmsnorm_kernel<bf16, bf16>), dim3(M), dim3(256), 0, s, (const bf16*)x, ldx, d,
-                       (const bf16*)g, eps, (bf16*)out, ldo);
+                       (const bf16*)g, eps, (bf16*)out, ldo, of);
   else
     hipLaunchKernelGGL((rmsnorm_kernel<float, float>), dim3(M), dim3(256), 0, s, (const float*)x, ldx, d,
-                       (const float*)g, eps, (float*)out, ldo);
+                       (const float*)g, eps, (float*)out, ldo, of);
   return hipGetLastError();
 }
 
@@ -316,7 +326,8 @@ hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int ca
 // u[s*B + i] = [E(b); E(y_rej); f[s*B + rec[1] + i - 1]] for relayed block indices rec[4]..rec[0], else 0.
 // One workgroup per (row, segment), 16-byte copies (d * sizeof(T) is a multiple of 16).
 template <typename T>
-__global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, const T* f, int B, int d, int V, T* u) {
+__global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, const T* f, int B, int d, int V, T* u,
+                                    FragOut of) {
   const int row = blockIdx.x, seg = blockIdx.y;
   const int s = row / B, i = row - s * B;
   const int* r = rec + (size_t)s * CARRY_REC;
@@ -324,25 +335,38 @@ __global__ void relay_gather_kernel(int carry_on, const int* rec, const T* E, co
                      r[1] + r[0] <= B && r[2] >= 0 && r[2] < V && r[3] >= 0 && r[3] < V;
   uint4* dst = reinterpret_cast<uint4*>(u + ((size_t)row * 3 + seg) * d);
   const int nvec = d * (int)sizeof(T) / 16;
+  constexpr int EV = 16 / (int)sizeof(T);   // elements per 16-byte vector
+  static_assert(EV == TT<T>::KL, "a 16-byte vector is one lane fragment");
+  // one vector is one lane fragment of the matrix-core-order copy
+  auto fdst = [&](int v) {
+    return reinterpret_cast<uint4*>(reinterpret_cast<T*>(of.p) + afrag_off<T>(row, of.c0 + seg * d + v * EV, of.ktiles));
+  };
   if (!valid) {
-    for (int v = threadIdx.x; v < nvec; v += blockDim.x) dst[v] = make_uint4(0u, 0u, 0u, 0u);
+    for (int v = threadIdx.x; v < nvec; v += blockDim.x) {
+      dst[v] = make_uint4(0u, 0u, 0u, 0u);
+      if (of.p) *fdst(v) = make_uint4(0u, 0u, 0u, 0u);
+    }
     return;
   }
   const T* src = seg == 0 ? E + (size_t)r[2] * d : seg == 1 ? E + (size_t)r[3] * d
                                                             : f + ((size_t)s * B + r[1] + i - 1) * d;
   const uint4* sv = reinterpret_cast<const uint4*>(src);
-  for (int v = threadIdx.x; v < nvec; v += blockDim.x) dst[v] = sv[v];
+  for (int v = threadIdx.x; v < nvec; v += blockDim.x) {
+    const uint4 x = sv[v];
+    dst[v] = x;
+    if (of.p) *fdst(v) = x;
+  }
 }
 
 hipError_t launch_relay_gather(bool isbf, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
-                               int B, int d, int V, void* u, hipStream_t s) {
+                               int B, int d, int V, void* u, FragOut of, hipStream_t s) {
   if (d % 16) return hipErrorInvalidValue;
   if (isbf)
     hipLaunchKernelGGL(relay_gather_kernel<bf16>, dim3(nseq * B, 3), dim3(256), 0, s, carry_on, carry_rec,
-                       (const bf16*)E, (const bf16*)f, B, d, V, (bf16*)u);
+                       (const bf16*)E, (const bf16*)f, B, d, V, (bf16*)u, of);
   else
     hipLaunchKernelGGL(relay_gather_kernel<float>, dim3(nseq * B, 3), dim3(256), 0, s, carry_on, carry_rec,
-                       (const float*)E, (const float*)f, B, d, V, (float*)u);
+                       (const float*)E, (const float*)f, B, d, V, (float*)u, of);
   return hipGetLastError();
 }
 
@@ -355,7 +379,7 @@ __global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const in
                                                           const T* e_mask, const T* f,
                                                           const float* bg, const T* ln_g, const T* ln_b, float ln_eps,
                                                           int B, int d, int V, T* x, int* status, float* ssq,
-                                                          int ssq_ld) {
+                                                          int ssq_ld, FragOut of) {
   constexpr int RC = 2;
   __shared__ float sh[32];
   const int row = blockIdx.x;
@@ -435,6 +459,9 @@ __global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const in
       }
     }
     Row16<T>::store(xr + (size_t)c * 16, v);
+    if (of.p)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) frag_st<T>(of, row, c * 16 + e, v[e]);
     float sq = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) sq += v[e] * v[e];
@@ -445,16 +472,16 @@ __global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const in
 hipError_t launch_relay_input(bool isbf, int carry_on, const int* carry_rec, const int* anchor, const void* E,
                               const void* e_mask, const void* f, const float* bg, const void* ln_g,
                               const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
-                              float* ssq, int ssq_ld, hipStream_t s) {
+                              float* ssq, int ssq_ld, FragOut of, hipStream_t s) {
   if (d % 16 || d > 16 * 256 * 2) return hipErrorInvalidValue;
   if (isbf)
     hipLaunchKernelGGL(relay_input_kernel<bf16>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
                        (const bf16*)E, (const bf16*)e_mask, (const bf16*)f, bg, (const bf16*)ln_g,
-                       (const bf16*)ln_b, ln_eps, B, d, V, (bf16*)x, status, ssq, ssq_ld);
+                       (const bf16*)ln_b, ln_eps, B, d, V, (bf16*)x, status, ssq, ssq_ld, of);
   else
     hipLaunchKernelGGL(relay_input_kernel<float>, dim3(nseq * B), dim3(256), 0, s, carry_on, carry_rec, anchor,
                        (const float*)E, (const float*)e_mask, (const float*)f, bg, (const float*)ln_g,
-                       (const float*)ln_b, ln_eps, B, d, V, (float*)x, status, ssq, ssq_ld);
+                       (const float*)ln_b, ln_eps, B, d, V, (float*)x, status, ssq, ssq_ld, of);
   return hipGetLastError();
 }
 

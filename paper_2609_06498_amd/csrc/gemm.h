@@ -5,6 +5,17 @@
 
 namespace dflow {
 
+// Matrix-core-order copy of an activation block (afrag_off): written by the
+// producer of the A operand of a projection of at most FRAG_MAX_ROWS rows (a
+// multiple of 16: the weight-streaming kernel reads whole 16-row tiles).
+// p null: no copy.
+constexpr int FRAG_MAX_ROWS = 48;
+struct FragOut {
+  void* p;
+  int ktiles;   // K / KT of the consuming projection
+  int c0;       // first column of the producer's output within that K
+};
+
 enum Epi : int {
   EPI_STORE_T = 0,   // Y = acc                       (storage type)
   EPI_STORE_F32,     // Y = acc                       (fp32)
@@ -46,6 +57,11 @@ struct GemmParams {
   // split)
   float* part_ws;
   int cus;                          // compute units (0: unknown, no balance-driven split)
+  // Skinny launches (weight-streaming kernel, at most FRAG_MAX_ROWS rows): A
+  // read from its matrix-core-order copy (afrag_off), and copies of the
+  // outputs Y / Y2 written in that order for the next projection.
+  const void* Af;
+  FragOut yf, y2f;
 };
 
 constexpr int SPLIT_MIN_ROWS = 48, SWIGLU_SPLIT_MAX_ROWS = 256;

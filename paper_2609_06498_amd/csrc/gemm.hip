@@ -61,19 +61,25 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
 #pragma unroll
   for (int j = 0; j < NG; ++j) wrow[j] = Wp + (size_t)min(nt0 + j, p.ntiles - 1) * p.ktiles * 64 + lane;
   const gu4* arow[MT];
+  // one k tile of A: 16 bytes per lane, 4 apart along a row-major row (16 row
+  // pieces per load), or 64 apart in the matrix-core-order copy (1 KB contiguous)
+  const int ast = p.Af ? 64 : KT * (int)sizeof(T) / 16;
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    const int m = min(i * 16 + (lane & 15), M - 1);
-    arow[i] = (const gu4*)(Ap + (size_t)m * p.lda + (lane >> 4) * KL);
+    if (p.Af) {   // rows past M in the last row tile are read and never stored
+      arow[i] = (const gu4*)(p.Af) + (size_t)min(i, mtiles - 1) * p.ktiles * 64 + lane;
+    } else {
+      const int m = min(i * 16 + (lane & 15), M - 1);
+      arow[i] = (const gu4*)(Ap + (size_t)m * p.lda + (lane >> 4) * KL);
+    }
   }
-  constexpr int AST = KT * (int)sizeof(T) / 16;   // uint4 stride of one k tile along an A row
 
   u32x4_t bq[2][U][NG];
   u32x4_t aq[2][U][MT];
 #define DFLOW_LOAD(st, kt)                                                             \
   _Pragma("unroll") for (int u = 0; u < U; ++u) {                                       \
     _Pragma("unroll") for (int j = 0; j < NG; ++j) bq[st][u][j] = __builtin_nontemporal_load(&wrow[j][(size_t)((kt) + u) * 64]); \
-    _Pragma("unroll") for (int i = 0; i < MT; ++i) aq[st][u][i] = arow[i][(size_t)((kt) + u) * AST]; \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i) aq[st][u][i] = arow[i][(size_t)((kt) + u) * ast]; \
   }                                                                                     \
   __builtin_amdgcn_sched_barrier(0);
 #define DFLOW_COMPUTE(st)                                                              \
@@ -138,7 +144,7 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NG; ++j) b1[j] = __builtin_nontemporal_load(&wrow[j][(size_t)kt * 64]);
 #pragma unroll
-    for (int i = 0; i < MT; ++i) a1[i] = arow[i][(size_t)kt * AST];
+    for (int i = 0; i < MT; ++i) a1[i] = arow[i][(size_t)kt * ast];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -246,7 +252,9 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
         gt *= s_rs[m];
         up *= s_rs[m];
       }
-      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + obase + c, silu(gt) * up);
+      const float y = silu(gt) * up;
+      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + obase + c, y);
+      frag_st<T>(p.yf, m, obase + c, y);
     }
   } else {
     for (int e = threadIdx.x; e < M * ncols; e += blockDim.x) {
@@ -262,10 +270,13 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
         v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col));
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
         if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), (size_t)m * p.ldy2 + col, v);
+        frag_st<T>(p.yf, m, col, v);
+        frag_st<T>(p.y2f, m, col, v);
         ct[m * CW + n] = v;
       } else if constexpr (EPI == EPI_BIAS_SILU) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, silu(v));
+        frag_st<T>(p.yf, m, col, silu(v));
       } else if constexpr (EPI == EPI_BIAS_F32) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
@@ -904,6 +915,9 @@ static bool swiglu_split_pays(const GemmParams& p) {
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   const int ks = p.ksplit > 1 ? p.ksplit : 1;
+  // matrix-core-order operands and copies only on the weight-streaming kernel,
+  // which every launch of at most FRAG_MAX_ROWS rows takes
+  if ((p.Af || p.yf.p || p.y2f.p) && p.M > FRAG_MAX_ROWS) return hipErrorInvalidValue;
   if (epi == EPI_RESID && p.M > SPLIT_MIN_ROWS && p.part_ws && !p.norm && p.col0 == 0)
     return launch_resid_split<T>(p, st);
   if (epi == EPI_SWIGLU && p.M > SPLIT_MIN_ROWS && p.M <= SWIGLU_SPLIT_MAX_ROWS && p.part_ws && p.col0 == 0 &&

@@ -39,6 +39,7 @@ struct AttnParams {
   float* part_o;             // [nseq][Hkv][rg][nsplit][16][Dh]
   float* part_ml;            // [nseq][Hkv][rg][nsplit][16][2]
   void* out;                 // [nseq*Bq, Hq*Dh] storage type
+  FragOut outf;              // matrix-core-order copy of out for the O projection (skinny launches)
 };
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
 // Whether the fused variant fits (block rows per wave, LDS) for this shape.
@@ -71,9 +72,9 @@ struct RopeParams {
 };
 
 hipError_t launch_embed(bool bf16, const int* tok, int M, const void* E, int V, int d, void* out, int* status,
-                        float* ssq, int ssq_ld, hipStream_t s);
+                        float* ssq, int ssq_ld, FragOut of, hipStream_t s);
 hipError_t launch_rmsnorm(bool bf16, bool in_f32, const void* x, int ldx, int M, int d, const void* g, float eps,
-                          void* out, int ldo, hipStream_t s);
+                          void* out, int ldo, FragOut of, hipStream_t s);
 hipError_t launch_qk_rope_write(bool bf16, const RopeParams& p, hipStream_t s);
 constexpr int ARGMAX_SPLITS = 32;   // workgroups of the argmax reduction
 // Optional drafter layout of the row argmaxes (rows s*B + j): block_out[s][j] =
@@ -84,11 +85,11 @@ hipError_t launch_argmax_reduce(const uint64_t* amax, int groups, int M, uint64_
 hipError_t launch_accept(const int* block, const int* g, int nseq, int B, int carry_window, int* accept_len,
                          int* bonus, int* committed, int* n_carry, int* carry_rec, hipStream_t s);
 hipError_t launch_relay_gather(bool bf16, int carry_on, const int* carry_rec, const void* E, const void* f, int nseq,
-                               int B, int d, int V, void* u, hipStream_t s);
+                               int B, int d, int V, void* u, FragOut of, hipStream_t s);
 hipError_t launch_relay_input(bool bf16, int carry_on, const int* carry_rec, const int* anchor, const void* E,
                               const void* e_mask, const void* f, const float* bg, const void* ln_g,
                               const void* ln_b, float ln_eps, int nseq, int B, int d, int V, void* x, int* status,
-                              float* ssq, int ssq_ld, hipStream_t s);
+                              float* ssq, int ssq_ld, FragOut of, hipStream_t s);
 hipError_t launch_commit(const int* accept_len, int nseq, int* seq_len, hipStream_t s);
 hipError_t launch_force(const int* traj, int traj_stride, int traj_len, const signed char* mode, const int* tok,
                         const int* anchor, const int* start_pos, int nseq, int B, int V, int* block_tok,
