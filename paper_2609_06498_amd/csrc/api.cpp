@@ -47,6 +47,7 @@ struct dflow_ctx {
   int q_dim, kv_dim, qkv_n;
   int mmax, rows_round;
   int G, nsplit, part_items;
+  int split_keys;            // keys per attention split (split_keys_for)
   int lm_groups;
   int qkv_ks;                // K parts of the QKV projection (fp32 partial sums, added by the consumers)
   int cus;                   // compute units of the device (launch balance decisions)
@@ -165,7 +166,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   const int rows_round = d->max_batch * d->block;
   const int mmax = rows_round > d->max_rows ? rows_round : d->max_rows;
   const int G = d->n_heads / d->n_kv_heads;
-  const int split_keys = d->dtype == DFLOW_BF16 ? SplitKeys<bf16>::value : SplitKeys<float>::value;
+  const int split_keys = split_keys_for(d->dtype == DFLOW_BF16, d->n_kv_heads, d->max_pages * PAGE);
   const int nsplit = (d->max_pages * PAGE + split_keys - 1) / split_keys;
   const int rg_round = (d->block * G + 15) / 16, rg_pre = (d->max_rows * G + 15) / 16;
   int items = d->max_batch * rg_round;
@@ -302,6 +303,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->pool_layer_elems = (size_t)dims->num_pages * dims->n_kv_heads * PAGE * dims->head_dim;
 
   Layout L = plan(dims, &c->nsplit, &c->part_items, &c->lm_groups);
+  c->split_keys = split_keys_for(c->bf, dims->n_kv_heads, dims->max_pages * PAGE);
   c->ws = workspace;
   c->ws_bytes = L.total;
   char* b = (char*)c->ws;
@@ -493,6 +495,7 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
   a.Hkv = c->dm.n_kv_heads;
   a.Dh = c->dm.head_dim;
   a.causal = causal;
+  a.split_keys = c->split_keys;
   a.nsplit = c->nsplit;
   a.num_pages = c->dm.num_pages;
   a.rg = (Bq * c->G + 15) / 16;
@@ -569,7 +572,7 @@ hipError_t decoder_layer(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int
   if ((e = gemm(c, st, EPI_STORE_F32, c->x, d.d, L.wqkv, M, c->qkv_n, d.d, c->qkv, c->qkv_n, nullptr, 0, nullptr, 0,
                 nullptr, nullptr, 0, attn_n, nullptr, c->qkv_ks, fq)))
     return e;
-  const bool fused = attention_fuses_rope(c->bf, Bq, c->G, d.head_dim);
+  const bool fused = attention_fuses_rope(c->bf, Bq, c->G, d.head_dim, c->split_keys);
   if (!fused) {
     RopeParams r = rope_params(c, L, nseq, Bq, d.n_heads, start_pos, nullptr, page_table, kpool, vpool);
     r.qkv32 = reinterpret_cast<const float*>(c->qkv);

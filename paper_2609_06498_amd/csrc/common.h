@@ -17,10 +17,18 @@ namespace dflow {
 constexpr int WAVE = 64;
 constexpr int PAGE = 64;          // KV page size in tokens (also the attention sub-chunk)
 constexpr int SSQ_LD = 512;       // row stride of the RMSNorm partial sums [row][strip] (d <= 16 * SSQ_LD)
-// keys per attention split (fixed absolute positions): 4 pages bf16, 2 pages fp32,
-// so the staged K+V pages of a split fit the 160 KB LDS of a CU
-template <typename T> struct SplitKeys;
-template <> struct SplitKeys<float> { static constexpr int value = 128; };
+// Keys per attention split (fixed absolute positions): at most 4 pages bf16, 2
+// pages fp32, so the staged K+V pages of a split fit the 160 KB LDS of a CU.
+// Split size of a context, from its dimensions only (never from a batch): the
+// largest split (fewest partials to merge, every split re-reads the query
+// rows) unless the kv heads x splits of a full-capacity sequence would leave
+// most compute units idle, then 128 keys (Qwen3-1.7B shape at context 1024:
+// attention 16.5 -> 13.8 us per layer; at context 4096 256-key splits win,
+// 18.7 vs 25.8 us).
+inline int split_keys_for(bool bf16, int n_kv_heads, int max_keys) {
+  if (!bf16) return 128;
+  return (long long)n_kv_heads * ((max_keys + 255) / 256) >= 128 ? 256 : 128;
+}
 
 // ------------------------------------------------------------------ bf16 storage
 struct bf16 { uint16_t u; };
@@ -41,7 +49,6 @@ __device__ inline uint32_t f2bf2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_hw_t));
 }
 
-template <> struct SplitKeys<bf16> { static constexpr int value = 256; };
 
 // Storage-type traits.  A "lane fragment" is the 16 bytes one lane feeds to
 // the matrix core per tile: 8 bf16 or 4 fp32 consecutive k values.

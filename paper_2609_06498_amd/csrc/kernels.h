@@ -33,6 +33,7 @@ struct AttnParams {
   const int* start_pos;      // [nseq] absolute position of block row 0
   int nseq, Bq, Hq, Hkv, Dh;
   int causal;                // 1: row j sees keys <= start+j; 0: all keys < start+Bq
+  int split_keys;            // keys per split (split_keys_for), a multiple of PAGE
   int nsplit;                // split slots per sequence (upper bound)
   int num_pages;             // pages per layer pool (page ids are checked)
   int rg;                    // 16-row groups per (seq, kv head)
@@ -43,7 +44,7 @@ struct AttnParams {
 };
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
 // Whether the fused variant fits (block rows per wave, LDS) for this shape.
-bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh);
+bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh, int split_keys);
 
 }  // namespace dflow
 

@@ -5,9 +5,10 @@ benchmark's seeded weights:
 * qwen3-8b  -- the benchmarked shape (36 + 5 layers, d 4096, 32/8 heads,
   FFN 12288, vocab 151936) at a 640-token context: the prefill runs a
   512-row chunk (tiled GEMMs, the unfused attention) and a 128-row chunk, and
-  every round's attention spans three 256-key splits plus the block, merged
-  by the split combine, with the QKV projection in two K parts and QK-norm,
-  RoPE and the block's KV write fused into the attention;
+  every round's attention spans five or six 128-key splits (the split size
+  at this capacity) with the block, merged by the split combine, with
+  the QKV projection in two K parts and QK-norm, RoPE and the block's KV
+  write fused into the attention;
 * qwen3-1.7b -- 28 + 5 layers, d 2048, 16/8 heads, FFN 6144;
 * qwen3-32b-d5 -- the Qwen3-32B widths (d 5120, 64/8 heads: GQA group 8,
   which takes the attention path without the fused QK-norm/RoPE, FFN 25600)
