@@ -118,6 +118,23 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   const int nst = (ke - kb) / U;
   int kt = kb;
   if (nst > 0) { DFLOW_LOAD(0, kt); }
+  // The epilogue's own operand -- the residual rows (written by the previous
+  // launch, so an L2 miss) or the bias -- for this thread's first PF outputs,
+  // loaded behind the first weight stage instead of after the main loop.
+  constexpr bool EPF = EPI == EPI_RESID || EPI == EPI_BIAS_SILU || EPI == EPI_BIAS_F32;
+  constexpr int PF = EPF ? 4 : 1;
+  const int ncols = nvalid * 16;
+  const int colbase = p.col0 + nt0 * 16;
+  float pre[PF];
+  if constexpr (EPF) {
+#pragma unroll
+    for (int it = 0; it < PF; ++it) {
+      const int e = threadIdx.x + it * (int)blockDim.x;
+      const int m = min(e / ncols, M - 1), col = colbase + e % ncols;   // clamped: never used past M
+      pre[it] = EPI == EPI_RESID ? TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col)
+                                 : TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+    }
+  }
   if (nst > 0) {
     int left = nst;
     while (left > 2) {
@@ -220,8 +237,6 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   }
 
   // ---- epilogue
-  const int ncols = nvalid * 16;
-  const int colbase = p.col0 + nt0 * 16;
   if constexpr (EPI == EPI_ARGMAX) {
     for (int e = threadIdx.x; e < M * ncols; e += blockDim.x) {
       const int m = e / ncols, n = e - m * ncols;
@@ -257,7 +272,8 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
       frag_st<T>(p.yf, m, obase + c, y);
     }
   } else {
-    for (int e = threadIdx.x; e < M * ncols; e += blockDim.x) {
+    // output e of this thread; x = the residual or bias value of its column
+    auto out1 = [&](int e, float x) {
       const int m = e / ncols, n = e - m * ncols;
       const int col = colbase + n;
       float v = ct[m * CW + n];
@@ -267,20 +283,35 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
       } else if constexpr (EPI == EPI_STORE_F32) {
         reinterpret_cast<float*>(p.Y)[(size_t)h * p.y_part + (size_t)m * p.ldy + col] = v;
       } else if constexpr (EPI == EPI_RESID) {
-        v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col));
+        v = TT<T>::rnd(v + x);
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, v);
         if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), (size_t)m * p.ldy2 + col, v);
         frag_st<T>(p.yf, m, col, v);
         frag_st<T>(p.y2f, m, col, v);
         ct[m * CW + n] = v;
       } else if constexpr (EPI == EPI_BIAS_SILU) {
-        v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+        v += x;
         TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, silu(v));
         frag_st<T>(p.yf, m, col, silu(v));
       } else if constexpr (EPI == EPI_BIAS_F32) {
-        v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+        v += x;
         reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
       }
+    };
+    const int nout = M * ncols;
+#pragma unroll
+    for (int it = 0; it < PF; ++it) {
+      const int e = threadIdx.x + it * (int)blockDim.x;
+      if (e < nout) out1(e, pre[it]);
+    }
+    for (int e = threadIdx.x + PF * (int)blockDim.x; e < nout; e += blockDim.x) {
+      const int col = colbase + e % ncols;
+      float x = 0.f;
+      if constexpr (EPI == EPI_RESID)
+        x = TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)(e / ncols) * p.ldr + col);
+      else if constexpr (EPI == EPI_BIAS_SILU || EPI == EPI_BIAS_F32)
+        x = TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+      out1(e, x);
     }
     if constexpr (EPI == EPI_RESID) {
       if (p.ssq_out) {   // sum of squares of the stored values, per row and 16-column strip
