@@ -94,49 +94,63 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   // c = q (mod 16) in increasing c, then a fixed butterfly over the group --
   // the same order for every row, batch and launch shape.  Group g owns rows
   // g + k * ngrp; the partials of strips c < 256 for its first two rows are
-  // loaded here, ahead of the weights, and consumed after the main loop, so
-  // the reduction costs no latency on the critical path.
+  // loaded early (see below) and consumed after the main loop, so the
+  // reduction costs no latency on the critical path.
   constexpr int EL = 16;                  // early partials per lane and row
   const int q16 = threadIdx.x & 15, grp = threadIdx.x >> 4, ngrp = blockDim.x >> 4;
   float ea[NORM ? EL : 1], eb[NORM ? EL : 1];
-  if constexpr (NORM) {
-    // rows of a group are clamped to valid rows and strips read the padded
-    // row (ssq_ld >= 256 entries), so every load is unconditional
-    gf32* ra = (gf32*)(p.ssq) + (size_t)min(grp, M - 1) * p.ssq_ld + q16;
-    gf32* rb = (gf32*)(p.ssq) + (size_t)min(grp + ngrp, M - 1) * p.ssq_ld + q16;
+  // The epilogue's own operand -- the residual rows (written by the previous
+  // launch, so an L2 miss) or the bias -- for this thread's first PF outputs,
+  // loaded early instead of after the main loop.
+  constexpr bool EPF = EPI == EPI_RESID || EPI == EPI_BIAS_SILU || EPI == EPI_BIAS_F32;
+  constexpr int PF = EPF ? 4 : 1;
+  const int ncols = nvalid * 16;
+  const int colbase = p.col0 + nt0 * 16;
+  float pre[PF];
+  // Early operand loads (row-scale partials, epilogue operand).  Loads
+  // complete in order, so they are issued after the first matrix-core ops:
+  // ahead of them they would hold up the pipeline start (the 8B QKV launch's
+  // first stage landed 3.7 instead of 1.6 us after its start).
+  auto prefetch = [&]() {
+    if constexpr (NORM) {
+      // rows of a group are clamped to valid rows and strips read the padded
+      // row (ssq_ld >= 256 entries), so every load is unconditional
+      gf32* ra = (gf32*)(p.ssq) + (size_t)min(grp, M - 1) * p.ssq_ld + q16;
+      gf32* rb = (gf32*)(p.ssq) + (size_t)min(grp + ngrp, M - 1) * p.ssq_ld + q16;
 #pragma unroll
-    for (int it = 0; it < EL; ++it) {
-      ea[it] = ra[16 * it];
-      eb[it] = rb[16 * it];
+      for (int it = 0; it < EL; ++it) {
+        ea[it] = ra[16 * it];
+        eb[it] = rb[16 * it];
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-  }
+
+    if constexpr (EPF) {
+#pragma unroll
+      for (int it = 0; it < PF; ++it) {
+        const int e = threadIdx.x + it * (int)blockDim.x;
+        const int m = min(e / ncols, M - 1), col = colbase + e % ncols;   // clamped: never used past M
+        pre[it] = EPI == EPI_RESID ? TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col)
+                                   : TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
+      }
+    }
+  };
 
   // Full stages of U tiles, double-buffered.  Inside the steady-state loop
   // every load is unconditional, so the compiler's wait before each compute
   // covers only the stage being consumed, never the prefetch just issued.
   const int nst = (ke - kb) / U;
   int kt = kb;
-  if (nst > 0) { DFLOW_LOAD(0, kt); }
-  // The epilogue's own operand -- the residual rows (written by the previous
-  // launch, so an L2 miss) or the bias -- for this thread's first PF outputs,
-  // loaded behind the first weight stage instead of after the main loop.
-  constexpr bool EPF = EPI == EPI_RESID || EPI == EPI_BIAS_SILU || EPI == EPI_BIAS_F32;
-  constexpr int PF = EPF ? 4 : 1;
-  const int ncols = nvalid * 16;
-  const int colbase = p.col0 + nt0 * 16;
-  float pre[PF];
-  if constexpr (EPF) {
-#pragma unroll
-    for (int it = 0; it < PF; ++it) {
-      const int e = threadIdx.x + it * (int)blockDim.x;
-      const int m = min(e / ncols, M - 1), col = colbase + e % ncols;   // clamped: never used past M
-      pre[it] = EPI == EPI_RESID ? TT<T>::ld(reinterpret_cast<const T*>(p.R), (size_t)m * p.ldr + col)
-                                 : TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
-    }
-  }
-  if (nst > 0) {
-    int left = nst;
+  if (nst > 2) {
+    // first iteration peeled: the early loads go out after its first stage
+    DFLOW_LOAD(0, kt);
+    DFLOW_LOAD(1, kt + U);
+    DFLOW_COMPUTE(0);
+    prefetch();
+    DFLOW_LOAD(0, kt + 2 * U);
+    DFLOW_COMPUTE(1);
+    kt += 2 * U;
+    int left = nst - 2;
     while (left > 2) {
       DFLOW_LOAD(1, kt + U);
       DFLOW_COMPUTE(0);
@@ -153,6 +167,20 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
     } else {
       DFLOW_COMPUTE(0);
       kt += U;
+    }
+  } else {   // short range (a few stages)
+    prefetch();
+    if (nst > 0) {
+      DFLOW_LOAD(0, kt);
+      if (nst == 2) {
+        DFLOW_LOAD(1, kt + U);
+        DFLOW_COMPUTE(0);
+        DFLOW_COMPUTE(1);
+        kt += 2 * U;
+      } else {
+        DFLOW_COMPUTE(0);
+        kt += U;
+      }
     }
   }
   // ragged tail (fewer than U tiles)
