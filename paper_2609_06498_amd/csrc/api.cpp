@@ -74,13 +74,13 @@ struct dflow_ctx {
   void* samp;            // sampling decoding partials
   float* samp_row;       // [vocab] logits of the last prompt row (dflow_prefill_sampled)
   float* kpart;          // K-part partial sums of the split residual and gate/up GEMMs
-  // Matrix-core-order copies of the skinny projections' A operands (FRAG_MAX_ROWS
-  // rows each): x (QKV, gate/up, LM heads), attention output (O), SwiGLU /
-  // relay hidden (down, relay W2), captured states (W_c), relay input (W1),
-  // projected features (drafter context K/V).  Used by the round's calls when
-  // nseq * block <= FRAG_MAX_ROWS (frag); a copy is read only by the call
-  // that wrote it, or -- captured states, features -- by the next call of the
-  // round (accept after verify, commit after accept).
+  // Matrix-core-order copies of the projections' A operands (the round's
+  // max_batch * block rows, rounded up to 16): x (QKV, gate/up, LM heads),
+  // attention output (O), SwiGLU / relay hidden (down, relay W2), captured
+  // states (W_c), relay input (W1), projected features (drafter context K/V).
+  // Used by the round's calls (frag; prefill reads row-major A); a copy is read
+  // only by the call that wrote it, or -- captured states, features -- by the
+  // next call of the round (accept after verify, commit after accept).
   void *xf, *attnf, *actf, *hcapf, *uf, *ff;
   bool frag = false;
 
@@ -223,8 +223,8 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
     }
     add(need);
   }
-  {   // 27..32 matrix-core-order operand copies of FRAG_MAX_ROWS rows
-    const size_t fr = (size_t)FRAG_MAX_ROWS * elt;
+  {   // 27..32 matrix-core-order operand copies of the round's rows
+    const size_t fr = (size_t)((rows_round + 15) / 16 * 16) * elt;
     add(fr * d->d);                                       // 27 x
     add(fr * qd);                                         // 28 attention output
     add(fr * (d->ffn > d->relay_hidden ? d->ffn : d->relay_hidden));   // 29 SwiGLU / relay hidden
@@ -771,7 +771,7 @@ extern "C" int dflow_draft_block(dflow_ctx* c, hipStream_t st, int nseq, const i
   c->phase = DFLOW_PHASE_DRAFT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  c->frag = M <= FRAG_MAX_ROWS;
+  c->frag = true;
   if (carry_on) {
     Frag f1, f2;
     if (c->frag) {
@@ -812,7 +812,7 @@ extern "C" int dflow_verify_block(dflow_ctx* c, hipStream_t st, int nseq, const 
   c->phase = DFLOW_PHASE_VERIFY;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  c->frag = M <= FRAG_MAX_ROWS;
+  c->frag = true;
   HIPCHK(launch_embed(c->bf, block_tok, M, c->w.embed, d.vocab, d.d, c->x, c->status, c->ssq, SSQ_LD,
                       fout(c, c->xf, d.d), st));
   HIPCHK(target_forward(c, st, nseq, B, start_pos, c->c.page_table, tgt_argmax, logits));
@@ -831,7 +831,7 @@ extern "C" int dflow_accept_and_carry(dflow_ctx* c, hipStream_t st, int nseq, co
   c->phase = DFLOW_PHASE_ACCEPT;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  c->frag = M <= FRAG_MAX_ROWS;
+  c->frag = true;
   HIPCHK(launch_accept(block_tok, tgt_argmax, nseq, B, d.carry_window, accept_len, bonus, committed, n_carry,
                        c->carry_rec, st));
   HIPCHK(project(c, st, M, c->f));
@@ -897,7 +897,7 @@ extern "C" int dflow_accept_sampled(dflow_ctx* c, hipStream_t st, int nseq, cons
   if ((rc = sampler_args(c, smp, anchor_pos, &a))) return rc;
   const dflow_dims& d = c->dm;
   const int B = d.block, M = nseq * B;
-  c->frag = M <= FRAG_MAX_ROWS;
+  c->frag = true;
   HIPCHK(launch_accept_sampled(logits, draft_logits, block_tok, a, nseq, B, d.carry_window, accept_len, bonus,
                                committed, n_carry, c->carry_rec, c->status, c->samp, st));
   HIPCHK(project(c, st, M, c->f));
@@ -935,7 +935,7 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
   if (rc) return rc;
   if (!accept_len || !seq_len) return fail(DFLOW_EINVAL, "kv_commit: null argument");
   c->phase = DFLOW_PHASE_COMMIT;
-  c->frag = nseq * c->dm.block <= FRAG_MAX_ROWS;
+  c->frag = true;
   HIPCHK(ctx_append(c, st, c->f, nseq, c->dm.block, seq_len, accept_len, c->c.page_table));
   HIPCHK(launch_commit(accept_len, nseq, seq_len, st));
   return DFLOW_OK;

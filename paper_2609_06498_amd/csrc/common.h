@@ -72,8 +72,8 @@ template <> struct TT<float> {
 // of a skinny projection): 16-row tiles of KT columns, 1 KB per (row tile, k
 // tile), lane l holding KL consecutive k values of row l%16 at k chunk l/16 --
 // one contiguous 16-byte load per lane, the k tiles of a row tile adjacent.
-// A producer that feeds a projection of at most FRAG_MAX_ROWS rows writes this
-// copy besides its row-major output; ktiles = K/KT of the consumer and c0 the
+// A producer that feeds a projection writes this copy besides its row-major
+// output; ktiles = K/KT of the consumer and c0 the
 // producer's first column within the consumer's K (the capture layers write
 // their slices of the W_c input).
 template <typename T>
@@ -87,6 +87,25 @@ __device__ inline void frag_st(const FragOut& f, int m, int c, float v) {
 }
 
 // 16 consecutive elements (16-byte aligned) <-> fp32, stores rounded to the storage type
+// n consecutive values of row m from column c (c and n multiples of KL, the
+// producer's c0 too) as whole 16-byte lane fragments of the copy
+template <typename T>
+__device__ inline void frag_st_run(const FragOut& f, int m, int c, const float* v, int n) {
+  if (!f.p) return;
+  constexpr int KL = TT<T>::KL;
+  for (int q = 0; q < n; q += KL) {
+    uint4 u;
+    if constexpr (sizeof(T) == 2) {
+      u = make_uint4(f2bf2(v[q], v[q + 1]), f2bf2(v[q + 2], v[q + 3]), f2bf2(v[q + 4], v[q + 5]),
+                     f2bf2(v[q + 6], v[q + 7]));
+    } else {
+      u = make_uint4(__float_as_uint(v[q]), __float_as_uint(v[q + 1]), __float_as_uint(v[q + 2]),
+                     __float_as_uint(v[q + 3]));
+    }
+    *reinterpret_cast<uint4*>(reinterpret_cast<T*>(f.p) + afrag_off<T>(m, f.c0 + c + q, f.ktiles)) = u;
+  }
+}
+
 template <typename T> struct Row16;
 template <> struct Row16<bf16> {
   __device__ static inline void load(const bf16* p, float* v) {

@@ -19,15 +19,16 @@ __global__ void embed_kernel(const int* tok, const T* E, int V, int d, T* out, i
   const bool ok = t >= 0 && t < V;
   if (!ok && threadIdx.x == 0) set_status(status, ST_BAD_TOKEN);
   for (int c = threadIdx.x; c < d / 16; c += blockDim.x) {
-    float sq = 0.f;
+    float sq = 0.f, vs[16];
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
       const size_t i = (size_t)c * 16 + e;
       const float v = ok ? TT<T>::ld(E, (size_t)t * d + i) : 0.f;
       TT<T>::st(out, (size_t)row * d + i, v);
-      frag_st<T>(of, row, (int)i, v);
+      vs[e] = v;
       sq += v * v;
     }
+    frag_st_run<T>(of, row, c * 16, vs, 16);
     if (ssq) ssq[(size_t)row * ssq_ld + c] = sq;
   }
 }
@@ -98,23 +99,26 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const TI* x, int ldx, int 
 #pragma unroll
   for (int r = 0; r < RV; ++r) {
     const int i = threadIdx.x + r * blockDim.x;
-    if (i < nv)
+    if (i < nv) {
+      float y[VN];
 #pragma unroll
       for (int e = 0; e < VN; ++e) {
-        const float y = v[r][e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
-        TT<T>::st(o, (size_t)i * VN + e, y);
-        frag_st<T>(of, row, i * VN + e, y);
+        y[e] = v[r][e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
+        TT<T>::st(o, (size_t)i * VN + e, y[e]);
       }
+      frag_st_run<T>(of, row, i * VN, y, VN);
+    }
   }
   for (int i = threadIdx.x + RV * blockDim.x; i < nv; i += blockDim.x) {
     float t[VN];
     Vec16<TI>::load(xr + (size_t)i * VN, t);
+    float y[VN];
 #pragma unroll
     for (int e = 0; e < VN; ++e) {
-      const float y = t[e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
-      TT<T>::st(o, (size_t)i * VN + e, y);
-      frag_st<T>(of, row, i * VN + e, y);
+      y[e] = t[e] * rs * TT<T>::ld(g, (size_t)i * VN + e);
+      TT<T>::st(o, (size_t)i * VN + e, y[e]);
     }
+    frag_st_run<T>(of, row, i * VN, y, VN);
   }
 }
 
@@ -459,9 +463,7 @@ __global__ void __launch_bounds__(256) relay_input_kernel(int carry_on, const in
       }
     }
     Row16<T>::store(xr + (size_t)c * 16, v);
-    if (of.p)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) frag_st<T>(of, row, c * 16 + e, v[e]);
+    frag_st_run<T>(of, row, c * 16, v, 16);
     float sq = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; ++e) sq += v[e] * v[e];

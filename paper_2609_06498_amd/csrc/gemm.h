@@ -6,10 +6,9 @@
 namespace dflow {
 
 // Matrix-core-order copy of an activation block (afrag_off): written by the
-// producer of the A operand of a projection of at most FRAG_MAX_ROWS rows (a
-// multiple of 16: the weight-streaming kernel reads whole 16-row tiles).
-// p null: no copy.
-constexpr int FRAG_MAX_ROWS = 48;
+// producer of a projection's A operand besides its row-major output, read by
+// the projection in whole 16-row tiles (buffers hold the launch's rows rounded
+// up to 16).  p null: no copy.
 struct FragOut {
   void* p;
   int ktiles;   // K / KT of the consuming projection
@@ -57,9 +56,9 @@ struct GemmParams {
   // split)
   float* part_ws;
   int cus;                          // compute units (0: unknown, no balance-driven split)
-  // Skinny launches (weight-streaming kernel, at most FRAG_MAX_ROWS rows): A
-  // read from its matrix-core-order copy (afrag_off), and copies of the
-  // outputs Y / Y2 written in that order for the next projection.
+  // A read from its matrix-core-order copy (afrag_off; null: from A), and
+  // copies of the outputs Y / Y2 written in that order for the next
+  // projection (every path and epilogue that writes Y / Y2 honours them).
   const void* Af;
   FragOut yf, y2f;
 };

@@ -444,15 +444,25 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   // swizzle.  W chunk c is lane c%64 of strip c/64.
   u32x4_t* sa = reinterpret_cast<u32x4_t*>(lds);             // [buffer][8 m tiles][64]
   u32x4_t* sw = sa + 2 * 512;                                 // [buffer][BS strips][64]
+  // From the matrix-core-order copy (p.Af) chunk c is lane c%64 of the 1 KB
+  // tile of m tile c/64: contiguous loads and LDS slots, no swizzle needed
+  // (rows past M in the last 16-row tile are loaded and never stored).
+  const bool af = p.Af != nullptr;
   const gu4* asrc[2];
   const gu4* wsrc[NWC];
   int adst[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = threadIdx.x + 256 * i;
-    const int r = c >> 2, q = c & 3;
-    asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
-    adst[i] = (r >> 4) * 64 + q * 16 + ((r & 15) ^ (2 * q));
+    if (af) {
+      const int mtg = min(m0 / 16 + (c >> 6), (p.M + 15) / 16 - 1);
+      asrc[i] = (const gu4*)(p.Af) + (size_t)mtg * p.ktiles * 64 + (c & 63);
+      adst[i] = c;
+    } else {
+      const int r = c >> 2, q = c & 3;
+      asrc[i] = (const gu4*)(Ap + (size_t)(m0 + min(r, rows - 1)) * p.lda + q * KL);   // clamped rows are not stored
+      adst[i] = (r >> 4) * 64 + q * 16 + ((r & 15) ^ (2 * q));
+    }
   }
 #pragma unroll
   for (int i = 0; i < NWC; ++i) {
@@ -460,11 +470,12 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
     wsrc[i] = Wp + (size_t)min(nt0 + (c >> 6), p.ntiles - 1) * p.ktiles * 64 + (c & 63);   // clamped strips: not stored
   }
   constexpr int AST = KT * (int)sizeof(T) / 16;              // 16-byte chunks per k tile along an A row
+  const int ast = af ? 64 : AST;
   u32x4_t ra[D][2], rw[D][NWC];                               // register slots
   auto load = [&](int slot, int kt) {                         // clamped: a load past the end is never used
     kt = min(kt, k1 - 1);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) ra[slot][i] = asrc[i][(size_t)kt * AST];
+    for (int i = 0; i < 2; ++i) ra[slot][i] = asrc[i][(size_t)kt * ast];
 #pragma unroll
     for (int i = 0; i < NWC; ++i)
       rw[slot][i] = NTW ? __builtin_nontemporal_load(&wsrc[i][(size_t)kt * 64]) : wsrc[i][(size_t)kt * 64];
@@ -495,7 +506,7 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
   };
   auto compute = [&](int buf) {
     u32x4_t a[4], b[WS];
-    const int aslot = (lane & 48) | ((lane & 15) ^ (2 * (lane >> 4)));   // fragment lane -> swizzled slot
+    const int aslot = af ? lane : (lane & 48) | ((lane & 15) ^ (2 * (lane >> 4)));   // fragment lane -> slot
 #pragma unroll
     for (int i = 0; i < 4; ++i) a[i] = sa[buf * 512 + (wm * 4 + i) * 64 + aslot];
 #pragma unroll
@@ -577,7 +588,9 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
         gt *= s_rs[m];
         up *= s_rs[m];
       }
-      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)(m0 + m) * p.ldy + obase + c, silu(gt) * up);
+      const float y = silu(gt) * up;
+      TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)(m0 + m) * p.ldy + obase + c, y);
+      frag_st<T>(p.yf, m0 + m, obase + c, y);
     }
   } else {
     for (int e = threadIdx.x; e < rows * ncols; e += blockDim.x) {
@@ -594,10 +607,13 @@ __global__ void __launch_bounds__(256, 2) gemm_tile_kernel(GemmParams p, int nw,
         v = TT<T>::rnd(v + TT<T>::ld(reinterpret_cast<const T*>(p.R), gm * p.ldr + col));
         TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, v);
         if (p.Y2) TT<T>::st(reinterpret_cast<T*>(p.Y2), gm * p.ldy2 + col, v);
+        frag_st<T>(p.yf, (int)gm, col, v);
+        frag_st<T>(p.y2f, (int)gm, col, v);
         ct[m * CW + n] = v;
       } else if constexpr (EPI == EPI_BIAS_SILU) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         TT<T>::st(reinterpret_cast<T*>(p.Y), gm * p.ldy + col, silu(v));
+        frag_st<T>(p.yf, (int)gm, col, silu(v));
       } else if constexpr (EPI == EPI_BIAS_F32) {
         v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
         reinterpret_cast<float*>(p.Y)[gm * p.ldy + col] = v;
@@ -733,7 +749,8 @@ static hipError_t launch_ng(const GemmParams& p, const GemmShape& sh, hipStream_
 template <typename T>
 __global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, size_t part_stride, int ks, int M,
                                                            int N, const T* R, int ldr, T* Y, int ldy, T* Y2, int ldy2,
-                                                           float* ssq_out, int ssq_ld, int strip0) {
+                                                           float* ssq_out, int ssq_ld, int strip0, FragOut yf,
+                                                           FragOut y2f) {
   const int nstrips = N / 16;
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= M * nstrips) return;
@@ -759,8 +776,11 @@ __global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, si
     const float v = TT<T>::rnd(s[c] + TT<T>::ld(R, (size_t)m * ldr + col));
     TT<T>::st(Y, (size_t)m * ldy + col, v);
     if (Y2) TT<T>::st(Y2, (size_t)m * ldy2 + col, v);
+    s[c] = v;
     sq += v * v;
   }
+  frag_st_run<T>(yf, m, j * 16, s, 16);
+  frag_st_run<T>(y2f, m, j * 16, s, 16);
   if (ssq_out) ssq_out[(size_t)m * ssq_ld + strip0 + j] = sq;
 }
 
@@ -793,6 +813,7 @@ __global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const 
       s[4 * q + 3] += v.w;
     }
   }
+  float y[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
     float gt = s[c], up = s[8 + c];
@@ -800,8 +821,10 @@ __global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const 
       gt *= rs;
       up *= rs;
     }
-    TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + j * 8 + c, silu(gt) * up);
+    y[c] = silu(gt) * up;
+    TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + j * 8 + c, y[c]);
   }
+  frag_st_run<T>(p.yf, m, j * 8, y, 8);
 }
 
 // The gate/up projection between SPLIT_MIN_ROWS and SWIGLU_SPLIT_MAX_ROWS
@@ -813,7 +836,8 @@ __global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const 
 template <typename T>
 static hipError_t launch_swiglu_split(const GemmParams& p, hipStream_t st) {
   const int ks = split_parts(EPI_SWIGLU, p.ntiles, p.ktiles);
-  GemmParams q = p;
+  GemmParams q = p;   // the parts read A (or its matrix-core-order copy); the reduce writes the copies
+  q.yf = q.y2f = FragOut{nullptr, 0, 0};
   q.ksplit = ks;
   q.norm = 0;
   q.Y = p.part_ws;
@@ -840,7 +864,8 @@ static hipError_t launch_swiglu_split(const GemmParams& p, hipStream_t st) {
 template <typename T>
 static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
   const int ks = split_parts(EPI_RESID, p.ntiles, p.ktiles);
-  GemmParams q = p;
+  GemmParams q = p;   // the parts read A (or its matrix-core-order copy); the reduce writes the copies
+  q.yf = q.y2f = FragOut{nullptr, 0, 0};
   q.ksplit = ks;
   q.Y = p.part_ws;
   q.ldy = p.ntiles * 16;
@@ -856,7 +881,7 @@ static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
   const int items = p.M * p.ntiles;
   hipLaunchKernelGGL(resid_reduce_kernel<T>, dim3((items + 255) / 256), dim3(256), 0, st, p.part_ws, q.y_part, ks,
                      p.M, q.ldy, reinterpret_cast<const T*>(p.R), p.ldr, reinterpret_cast<T*>(p.Y), p.ldy,
-                     reinterpret_cast<T*>(p.Y2), p.ldy2, p.ssq_out, p.ssq_out_ld, 0);
+                     reinterpret_cast<T*>(p.Y2), p.ldy2, p.ssq_out, p.ssq_out_ld, 0, p.yf, p.y2f);
   return hipGetLastError();
 }
 
@@ -897,6 +922,7 @@ __global__ void __launch_bounds__(256) range_reduce_kernel(GemmParams p, const f
     } else if constexpr (EPI == EPI_BIAS_SILU) {
       v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
       TT<T>::st(reinterpret_cast<T*>(p.Y), (size_t)m * p.ldy + col, silu(v));
+      frag_st<T>(p.yf, m, col, silu(v));
     } else if constexpr (EPI == EPI_BIAS_F32) {
       v += TT<T>::ld(reinterpret_cast<const T*>(p.bias), col);
       reinterpret_cast<float*>(p.Y)[(size_t)m * p.ldy + col] = v;
@@ -919,7 +945,8 @@ static hipError_t launch_range_reduce(const GemmParams& p, size_t part_stride, i
 template <typename T>
 static hipError_t launch_range_split(int epi, const GemmParams& p, hipStream_t st) {
   const int nw = split_parts(epi, p.ntiles, p.ktiles);
-  GemmParams q = p;
+  GemmParams q = p;   // the parts read A (or its matrix-core-order copy); the reduce writes the copies
+  q.yf = q.y2f = FragOut{nullptr, 0, 0};
   q.ksplit = nw;
   q.norm = 0;
   q.Y = p.part_ws;
@@ -974,9 +1001,6 @@ static bool swiglu_split_pays(const GemmParams& p) {
 template <typename T>
 static hipError_t launch_t(int epi, const GemmParams& p, hipStream_t st) {
   const int ks = p.ksplit > 1 ? p.ksplit : 1;
-  // matrix-core-order operands and copies only on the weight-streaming kernel,
-  // which every launch of at most FRAG_MAX_ROWS rows takes
-  if ((p.Af || p.yf.p || p.y2f.p) && p.M > FRAG_MAX_ROWS) return hipErrorInvalidValue;
   if (epi == EPI_RESID && p.M > SPLIT_MIN_ROWS && p.part_ws && !p.norm && p.col0 == 0)
     return launch_resid_split<T>(p, st);
   if (epi == EPI_SWIGLU && p.M > SPLIT_MIN_ROWS && p.M <= SWIGLU_SPLIT_MAX_ROWS && p.part_ws && p.col0 == 0 &&
