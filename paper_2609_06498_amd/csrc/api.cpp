@@ -47,7 +47,8 @@ struct dflow_ctx {
   int q_dim, kv_dim, qkv_n;
   int mmax, rows_round;
   int G, nsplit, part_items;
-  int split_keys;            // keys per attention split (split_keys_for)
+  int split_keys;            // keys per attention chunk (split_keys_for)
+  int round_chunks;          // attention chunks per split in the round calls (prefill: 1)
   int lm_groups;
   int qkv_ks;                // K parts of the QKV projection (fp32 partial sums, added by the consumers)
   int cus;                   // compute units of the device (launch balance decisions)
@@ -304,6 +305,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
 
   Layout L = plan(dims, &c->nsplit, &c->part_items, &c->lm_groups);
   c->split_keys = split_keys_for(c->bf, dims->n_kv_heads, dims->max_pages * PAGE);
+  c->round_chunks = round_chunks_for(dims->max_batch, dims->n_kv_heads, dims->max_pages * PAGE, c->split_keys, c->cus);
   c->ws = workspace;
   c->ws_bytes = L.total;
   char* b = (char*)c->ws;
@@ -495,8 +497,12 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
   a.Hkv = c->dm.n_kv_heads;
   a.Dh = c->dm.head_dim;
   a.causal = causal;
-  a.split_keys = c->split_keys;
-  a.nsplit = c->nsplit;
+  {
+    const int nw = attention_waves(fused, Bq, c->G), nrg = (Bq * c->G + 15) / 16;
+    a.chunks = (c->phase != DFLOW_PHASE_PREFILL && nrg <= nw) ? c->round_chunks : 1;
+    a.split_keys = c->split_keys * a.chunks;
+    a.nsplit = (c->dm.max_pages * PAGE + a.split_keys - 1) / a.split_keys;   // <= c->nsplit
+  }
   a.num_pages = c->dm.num_pages;
   a.rg = (Bq * c->G + 15) / 16;
   a.part_o = c->part_o;

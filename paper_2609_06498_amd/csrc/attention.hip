@@ -79,33 +79,41 @@ __device__ inline int vfrag_off(int slot, int e) {
   return (((slot / VG) * DT + e / 16) * 64 + ((slot % 16) / 4) * 16 + e % 16) * KL + ((slot % VG) / 16) * 4 + slot % 4;
 }
 
-// One workgroup of NW waves per (sequence, kv head, split of NPG pages at
-// fixed absolute positions); wave w owns the 16-row groups w, w + NW, ...
-// Attention rows of a group are (block row j, query head g) pairs, R = Bq * G.
+// One workgroup of NW waves per (sequence, kv head, split at fixed absolute
+// positions); a split is one or more chunks of NPG pages, the pages resident
+// in LDS at once.  Wave w owns the 16-row groups w, w + NW, ...  Attention
+// rows of a group are (block row j, query head g) pairs, R = Bq * G.
 //  1. Loads are issued in the order their consumers need them and all stay in
-//     flight together: the query rows and the block's own key/value rows of
-//     this split (fused variant) first, then the split's K/V pages, page by
-//     page, into registers.  Vector loads complete in issue order, so the
-//     query math below waits only for the query loads.
+//     flight together: the split's page ids (one vector load), the query rows
+//     and the block's own key/value rows of this split (fused variant), then
+//     the first chunk's K/V pages, page by page, into registers.  Vector loads
+//     complete in issue order, so the query math below waits only for the
+//     query loads.
 //  2. Fused variant: QK-norm + RoPE of the R query rows into an LDS query
 //     tile; QK-norm + RoPE of the block rows' keys, written to the paged
 //     cache and to an LDS row tile together with their values.
-//  3. Page by page in key order: the staged page goes to LDS, the block rows
-//     replace their (stale) slots, and every wave computes the masked scores
-//     of its first row group against the page (S^T = K Q^T on the matrix
-//     cores), so early pages are consumed while later ones still arrive.
-//  4. One softmax over the split's scores (row maximum, exp2, sum), P V on
-//     the matrix cores, and the split partial (m, l, O) of the row group.  A
-//     wave's further row groups then run over the resident pages.  The
-//     combine kernel merges the splits in split order.
+//  3. Chunk by chunk, page by page in key order: the staged page goes to LDS
+//     (its registers then take the next chunk's page), the block rows replace
+//     their (stale) slots, and every wave computes the masked scores of its
+//     first row group against the page (S^T = K Q^T on the matrix cores), so
+//     early pages are consumed while later ones still arrive.
+//  4. Per chunk one softmax step over the chunk's scores: the running row
+//     maximum, the rescale of the running sum and output by 2^(m_old - m_new)
+//     (skipped for the first chunk), exp2 of the scores, P V on the matrix
+//     cores; after the last chunk the split partial (m, l, O) of the row
+//     group.  A wave's further row groups (single-chunk splits only) then run
+//     over the resident pages.  The combine kernel merges the splits in split
+//     order.
 // A row's arithmetic depends only on its own visible keys and the fixed split
-// boundaries, never on the batch it is part of.
-template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG>
+// and chunk boundaries, never on the batch it is part of.  A single-chunk
+// split computes exactly what a one-step softmax over the split does; MC = 0
+// instantiates single-chunk splits only (no chunk loop, no rescale code).
+template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG, bool MC>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
   constexpr int KS = DH / KT;                 // k steps of S^T
   constexpr int DT = DH / 16;                 // output channel tiles
-  constexpr int SK = NPG * PAGE;              // keys per split
+  constexpr int SK = NPG * PAGE;              // keys per chunk
   constexpr int PG = PAGE * DH;               // elements of one K (or V) page block
   constexpr int NT = NW * 64;
   constexpr int HALF = DH / 2;
@@ -135,21 +143,24 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   const int R = p.Bq * G;
   const int nrg = (R + 15) / 16;
   const float sl2 = rsqrtf((float)DH) * 1.4426950408889634f;   // softmax scale x log2(e)
-  const int key0 = split * SK;
+  const int SPK = p.split_keys;               // keys per split: p.chunks chunks of SK keys
+  const int key0 = split * SPK;
   const int t0 = p.start_pos[s];
   const int kv_len = t0 + p.Bq;
   const int cap = p.max_pages * PAGE;
   if (threadIdx.x == 0 && split == 0 && kv_len > cap) set_status(p.status, ST_CAPACITY);
   if (key0 >= kv_len) return;                 // uniform over the workgroup
+  const int nch = MC ? min(p.chunks, (kv_len - key0 + SK - 1) / SK) : 1;   // chunks holding keys of the sequence
   T* lq = lv + (size_t)NPG * PG;              // [R][QLD] queries after QK-norm + RoPE (fused)
   T* ln = lq + (size_t)(FUSED ? R : 0) * QLD; // [rows][2][DH] block rows' keys and values (fused)
 
   // ---- 1. loads, in this order: page ids; query rows and the block rows of
   // the split as raw storage values (clamped rows are loaded and never
-  // stored); then, once the page ids are in, the K/V pages.  Nothing between
-  // the first load and the last K/V load waits on memory.
-  // (one vector load: lane i < NPG reads page i; broadcast once it is needed)
-  const int pvl = p.page_table[(size_t)s * p.max_pages + min(key0 / PAGE + (lane < NPG ? lane : 0), p.max_pages - 1)];
+  // stored); then, once the page ids are in, the first chunk's K/V pages.
+  // Nothing between the first load and the last K/V load waits on memory.
+  // (one vector load: lane i reads page i of the split, i < p.chunks * NPG <= 64)
+  const int npl = p.chunks * NPG;
+  const int pvl = p.page_table[(size_t)s * p.max_pages + min(key0 / PAGE + (lane < npl ? lane : 0), p.max_pages - 1)];
   // Head rows (queries, block keys/values) are handled as 16-byte chunks: LPR
   // lanes per row, lane chunk cl holds channels [cl*CE, cl*CE + CE); its
   // rotate-half partner chunk sits LPR/2 lanes away and shares its RoPE angles.
@@ -174,7 +185,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       for (int c = 0; c < RC; ++c) qrope[it][c] = rp[c];
     }
   }
-  const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SK - t0);   // block rows in this split
+  const int jlo = max(0, key0 - t0), jhi = min(p.Bq, key0 + SPK - t0);   // block rows in this split
   u32x4_t kraw[NPART][NQ], vraw[NPART][NQ], krope[RC];
   auto load_rows = [&](int it) {
     const int j = max(0, min(jlo + (w + NW * it) * RPI + rl, jhi - 1));   // clamped rows are not stored
@@ -202,26 +213,43 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
         x[4 * c + e] = TT<T>::rnd(v);
       }
   };
+  // query fragments of row group rg from the query rows after QK-norm + RoPE (unfused variant)
+  auto load_q_global = [&](int rg, u32x4_t (&qf)[KS]) {
+    const int qr = min(rg * 16 + (lane & 15), R - 1);
+    const int j = qr / G, g = qr - j * G;
+    const T* qrow = reinterpret_cast<const T*>(p.q) + ((size_t)(s * p.Bq + j) * p.Hq + kvh * G + g) * DH;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) qf[k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
+  };
   u32x4_t gq, gk;                             // QK-norm gains of the lane's chunk
   if constexpr (FUSED) {
-    load_rows(0);
+    if (jlo < jhi) load_rows(0);              // uniform: only splits holding block rows
     gq = *(const gu4*)(reinterpret_cast<const T*>(p.q_norm) + cl * CE);
     gk = *(const gu4*)(reinterpret_cast<const T*>(p.k_norm) + cl * CE);
   }
   __builtin_amdgcn_sched_barrier(0);
-  int pgid[NPG];
-  unsigned present = 0;                       // pages holding keys of the sequence, with valid ids
-#pragma unroll
-  for (int i = 0; i < NPG; ++i) {
-    const int pv = __builtin_amdgcn_readlane(pvl, i);
-    const bool ok = key0 + i * PAGE < kv_len && pv >= 0 && pv < p.num_pages;
-    pgid[i] = ok ? pv : 0;                    // absent pages read page 0 of the pool, never used
-    present |= ok ? (1u << i) : 0u;
+  // a page of the split holding keys of the sequence with an invalid id sets
+  // the status (once, here: the chunk loop below issues no conditional stores)
+  {
+    const bool bad = lane < npl && key0 + lane * PAGE < kv_len && (pvl < 0 || pvl >= p.num_pages);
+    if (__builtin_amdgcn_ballot_w64(bad) != 0 && threadIdx.x == 0) set_status(p.status, ST_BAD_PAGE);
   }
-  u32x4_t kr[NPG][PER], vr[NPG][PER];
+  // page ids of chunk c: absent pages (past the sequence or invalid ids) read
+  // page 0 of the pool and are never used
+  auto chunk_pages = [&](int c, int (&pg)[NPG]) {
+    unsigned pres = 0;
 #pragma unroll
-  for (int i = 0; i < NPG; ++i) {
-    const size_t off = ((size_t)pgid[i] * p.Hkv + kvh) * PG;
+    for (int i = 0; i < NPG; ++i) {
+      const int pv = __builtin_amdgcn_readlane(pvl, c * NPG + i);
+      const bool ok = key0 + (c * NPG + i) * PAGE < kv_len && pv >= 0 && pv < p.num_pages;
+      pg[i] = ok ? pv : 0;
+      pres |= ok ? (1u << i) : 0u;
+    }
+    return pres;
+  };
+  u32x4_t kr[NPG][PER], vr[NPG][PER];
+  auto issue_page = [&](int i, int pgid) {
+    const size_t off = ((size_t)pgid * p.Hkv + kvh) * PG;
     const gu4* kg = (const gu4*)(reinterpret_cast<const T*>(p.kpool) + off);
     const gu4* vg = (const gu4*)(reinterpret_cast<const T*>(p.vpool) + off);
 #pragma unroll
@@ -229,12 +257,18 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       kr[i][it] = __builtin_nontemporal_load(&kg[threadIdx.x + it * NT]);   // each page is read once per launch
       vr[i][it] = __builtin_nontemporal_load(&vg[threadIdx.x + it * NT]);
     }
-    __builtin_amdgcn_sched_barrier(0);        // issue order = page order = consumption order
+  };
+  u32x4_t qf[KS];                             // the wave's first row group's query fragments
+  const bool own = w < nrg;                    // uniform: the wave has a row group
+  if constexpr (!FUSED) {
+    if (own) load_q_global(w, qf);
   }
-  if (threadIdx.x == 0) {
+  int pgid[NPG];
+  unsigned present = chunk_pages(0, pgid);    // pages holding keys of the sequence, with valid ids
 #pragma unroll
-    for (int i = 0; i < NPG; ++i)
-      if (key0 + i * PAGE < kv_len && !((present >> i) & 1u)) set_status(p.status, ST_BAD_PAGE);
+  for (int i = 0; i < NPG; ++i) {
+    issue_page(i, pgid[i]);
+    __builtin_amdgcn_sched_barrier(0);        // issue order = page order = consumption order
   }
 
   // ---- 2. query tile; block rows to the cache and the row tile
@@ -282,16 +316,15 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       vchunk = Chunk<T>::pack(x);
       const int j = jlo + (w + NW * it) * RPI + rl;
       const int pos = t0 + j;
+      // the cache page of the row (page index within the split, a lane of pvl)
+      const int gp = __shfl(pvl, min(max((pos - key0) / PAGE, 0), 63), 64);
       if (j >= jhi) continue;
       T* row = ln + (size_t)(j - jlo) * 2 * DH;
       *reinterpret_cast<u32x4_t*>(row + cl * CE) = y;
       *reinterpret_cast<u32x4_t*>(row + DH + cl * CE) = vchunk;
       if (pos >= cap) continue;                // status set above
-      const int pi = (pos - key0) / PAGE, slot = pos % PAGE;
-      if (!((present >> pi) & 1u)) continue;   // status set above
-      int gp = 0;
-#pragma unroll
-      for (int i = 0; i < NPG; ++i) gp = i == pi ? pgid[i] : gp;
+      if (gp < 0 || gp >= p.num_pages) continue;   // status set when the page's chunk is staged
+      const int slot = pos % PAGE;
       T* kt_g = reinterpret_cast<T*>(p.kpool) + ((size_t)gp * p.Hkv + kvh) * PG;
       T* vt_g = reinterpret_cast<T*>(p.vpool) + ((size_t)gp * p.Hkv + kvh) * PG;
       *reinterpret_cast<u32x4_t*>(kt_g + kfrag_off<T, DH>(slot, cl * CE)) = y;   // CE = KL consecutive channels
@@ -300,16 +333,16 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     }
   }
 
-  // ---- 3. page by page: scores as pages land, then one softmax over the split
+  // ---- 3. page by page: scores as pages land, then one softmax step per chunk
   // The softmax runs in log2 units (scale folded with log2 e) with exp2; the
-  // split partial is (M, sum 2^(s - M), sum 2^(s - M) v) with
-  // M the row's maximum over the split's visible keys, so no running rescale.
+  // split partial is (M, sum 2^(s - M), sum 2^(s - M) v) with M the row's
+  // maximum over the split's visible keys, reached chunk by chunk.
   typedef float score_t[4][4];               // [key tile][key within the lane's group of 4]
-  auto scores = [&](int rg, int pi, const u32x4_t (&qf)[KS], score_t& sc) {
+  auto scores = [&](int rg, int pi, int kc0, const u32x4_t (&qf)[KS], score_t& sc) {
     const int ar = rg * 16 + (lane & 15);
     const bool row_ok = ar < R;
     const int pos_row = t0 + (row_ok ? ar / G : 0);
-    const int kp0 = key0 + pi * PAGE;
+    const int kp0 = kc0 + pi * PAGE;
     const u32x4_t* kb = reinterpret_cast<const u32x4_t*>(lk + (size_t)pi * PG);
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
@@ -332,12 +365,14 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
         }
     }
   };
-  // softmax over the present pages, P V, and the split partial of row group rg
-  auto finish = [&](int rg, score_t (&sc)[NPG]) {
+  // one softmax step over the chunk's present pages: running maximum m (log2
+  // units) and sum l of row lane&15, running output o (row 4*(lane>>4)+r of
+  // o[dt][r]); the first step starts from m = -inf, l = 0, o = 0 unscaled
+  auto step = [&](score_t (&sc)[NPG], unsigned pres, bool first, float& m, float& l, f32x4_t (&o)[DT]) {
     float mx = -INFINITY;
 #pragma unroll
     for (int pi = 0; pi < NPG; ++pi)
-      if ((present >> pi) & 1u)                // uniform
+      if ((pres >> pi) & 1u)                   // uniform
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -345,15 +380,27 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     // scores are raw dot products; in log2 units a score is s * sl2 and the
-    // row maximum m = mx * sl2 (sl2 > 0).  A row with no visible key keeps
+    // row maximum is mx * sl2 (sl2 > 0).  A row with no visible key keeps
     // m = -inf, l = 0 and a zero output: its scores are all -inf and
     // exponentiate to 0 against a finite reference.
     mx *= sl2;
-    const float mref = mx == -INFINITY ? 0.f : mx;
+    const float mn = first ? mx : fmaxf(m, mx);
+    const float mref = mn == -INFINITY ? 0.f : mn;
+    if (!first) {                              // uniform: rescale the running sum and output
+      const float f = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mref);
+      l *= f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float fr = __shfl(f, 4 * (lane >> 4) + r, 64);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt][r] *= fr;
+      }
+    }
+    m = mn;
     float ls = 0.f;
 #pragma unroll
     for (int pi = 0; pi < NPG; ++pi) {
-      if (!((present >> pi) & 1u)) continue;   // uniform
+      if (!((pres >> pi) & 1u)) continue;      // uniform
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
@@ -366,12 +413,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     }
     ls += __shfl_xor(ls, 16, 64);
     ls += __shfl_xor(ls, 32, 64);
-    f32x4_t o[DT];
-#pragma unroll
-    for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    l = first ? ls : l + ls;
 #pragma unroll
     for (int pi = 0; pi < NPG; ++pi) {
-      if (!((present >> pi) & 1u)) continue;   // uniform
+      if (!((pres >> pi) & 1u)) continue;      // uniform
       if constexpr (KL == 8) {
         // P V with 32 keys per matrix-core op: lane group g supplies keys
         // 4g..4g+3 of key tiles 2c and 2c+1, and V holds the same keys in
@@ -393,6 +438,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
           for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[pi][kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
       }
     }
+  };
+  auto write_partial = [&](int rg, float m, float l, const f32x4_t (&o)[DT]) {
     const size_t pidx = (((size_t)s * p.Hkv + kvh) * p.rg + rg) * p.nsplit + split;
     float* po = p.part_o + pidx * 16 * DH;
 #pragma unroll
@@ -400,61 +447,95 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) po[(4 * (lane >> 4) + r) * DH + dt * 16 + (lane & 15)] = o[dt][r];
     if (lane < 16) {
-      p.part_ml[pidx * 32 + 2 * lane] = mx;
-      p.part_ml[pidx * 32 + 2 * lane + 1] = ls;
+      p.part_ml[pidx * 32 + 2 * lane] = m;
+      p.part_ml[pidx * 32 + 2 * lane + 1] = l;
     }
   };
   auto load_q = [&](int rg, u32x4_t (&qf)[KS]) {
-    const int qr = min(rg * 16 + (lane & 15), R - 1);
     if constexpr (FUSED) {
+      const int qr = min(rg * 16 + (lane & 15), R - 1);
 #pragma unroll
       for (int k = 0; k < KS; ++k)
         qf[k] = *reinterpret_cast<const u32x4_t*>(lq + (size_t)qr * QLD + k * KT + (lane >> 4) * KL);
     } else {
-      const int j = qr / G, g = qr - j * G;
-      const T* qrow = reinterpret_cast<const T*>(p.q) + ((size_t)(s * p.Bq + j) * p.Hq + kvh * G + g) * DH;
-#pragma unroll
-      for (int k = 0; k < KS; ++k) qf[k] = *(const gu4*)(qrow + k * KT + (lane >> 4) * KL);
+      load_q_global(rg, qf);
     }
   };
 
-  u32x4_t qf[KS];
   score_t sc[NPG];
-  const bool own = w < nrg;                    // uniform: the wave has a row group
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t o_run[DT];
 #pragma unroll
-  for (int pi = 0; pi < NPG; ++pi) {
+  for (int i = 0; i < DT; ++i) o_run[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // the staged pages of chunk c: to LDS page by page (each page's registers
+  // then take the same page of the next chunk when `next`), block-row patch,
+  // scores of the wave's first row group.  The vector-memory operations of a
+  // chunk are exactly its prefetch loads, so the waits stay exact per page.
+  auto chunk = [&](int c, bool next, const int (&pg_next)[NPG]) {
+    const int kc0 = key0 + c * SK;
 #pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      reinterpret_cast<u32x4_t*>(lk + (size_t)pi * PG)[threadIdx.x + it * NT] = kr[pi][it];
-      reinterpret_cast<u32x4_t*>(lv + (size_t)pi * PG)[threadIdx.x + it * NT] = vr[pi][it];
-    }
-    __syncthreads();
-    if constexpr (FUSED) {
-      // block rows of this page replace the slots staged from the cache
-      const int jp0 = max(jlo, key0 + pi * PAGE - t0), jp1 = min(jhi, key0 + (pi + 1) * PAGE - t0);
-      if (jp0 < jp1) {                         // uniform
-        T* kt_l = lk + (size_t)pi * PG;
-        T* vt_l = lv + (size_t)pi * PG;
-        for (int e = threadIdx.x; e < (jp1 - jp0) * DH; e += NT) {
-          const int j = jp0 + e / DH, d = e % DH;
-          const int slot = (t0 + j) % PAGE;
-          const T* row = ln + (size_t)(j - jlo) * 2 * DH;
-          kt_l[kfrag_off<T, DH>(slot, d)] = row[d];
-          vt_l[vfrag_off<T, DH>(slot, d)] = row[DH + d];
-        }
-        __syncthreads();
+    for (int pi = 0; pi < NPG; ++pi) {
+#pragma unroll
+      for (int it = 0; it < PER; ++it) {
+        reinterpret_cast<u32x4_t*>(lk + (size_t)pi * PG)[threadIdx.x + it * NT] = kr[pi][it];
+        reinterpret_cast<u32x4_t*>(lv + (size_t)pi * PG)[threadIdx.x + it * NT] = vr[pi][it];
       }
+      if (next) issue_page(pi, pg_next[pi]);   // the next chunk's page streams in meanwhile
+      __syncthreads();
+      if constexpr (FUSED) {
+        // block rows of this page replace the slots staged from the cache
+        const int jp0 = max(jlo, kc0 + pi * PAGE - t0), jp1 = min(jhi, kc0 + (pi + 1) * PAGE - t0);
+        if (jp0 < jp1) {                       // uniform
+          T* kt_l = lk + (size_t)pi * PG;
+          T* vt_l = lv + (size_t)pi * PG;
+          for (int e = threadIdx.x; e < (jp1 - jp0) * DH; e += NT) {
+            const int j = jp0 + e / DH, d = e % DH;
+            const int slot = (t0 + j) % PAGE;
+            const T* row = ln + (size_t)(j - jlo) * 2 * DH;
+            kt_l[kfrag_off<T, DH>(slot, d)] = row[d];
+            vt_l[vfrag_off<T, DH>(slot, d)] = row[DH + d];
+          }
+          __syncthreads();
+        }
+        if (c == 0 && pi == 0 && own) load_q(w, qf);   // LDS reads only
+      }
+      if (own && ((present >> pi) & 1u)) scores(w, pi, kc0, qf, sc[pi]);
     }
-    if (pi == 0 && own) load_q(w, qf);
-    if (own && ((present >> pi) & 1u)) scores(w, pi, qf, sc[pi]);
+  };
+  // chunks 0 .. nch-2 prefetch the next one unconditionally; the last chunk is peeled
+  if constexpr (MC) {
+    for (int c = 0; c + 1 < nch; ++c) {        // uniform
+      int pg_next[NPG];
+      const unsigned pres_next = chunk_pages(c + 1, pg_next);
+      if (c > 0) __syncthreads();              // every wave is done with the previous chunk's pages
+      chunk(c, true, pg_next);
+      if (own) step(sc, present, c == 0, m_run, l_run, o_run);
+      present = pres_next;
+    }
+    if (nch > 1) __syncthreads();
   }
-  if (own) finish(w, sc);
-  for (int rg = w + NW; rg < nrg; rg += NW) {  // uniform per wave; pages resident, no barrier
+  chunk(nch - 1, false, pgid);
+  if (own) step(sc, present, nch == 1, m_run, l_run, o_run);
+  if (own) write_partial(w, m_run, l_run, o_run);
+  // further row groups: single-chunk splits only (the host launches no others
+  // with more row groups than waves); pages resident, no barrier
+  for (int rg = w + NW; rg < nrg; rg += NW) {  // uniform per wave
+    float m = -INFINITY, l = 0.f;
+    f32x4_t o[DT];
+#pragma unroll
+    for (int i = 0; i < DT; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     load_q(rg, qf);
+    unsigned pres0 = 0;
+#pragma unroll
+    for (int i = 0; i < NPG; ++i) {
+      const int pv = __builtin_amdgcn_readlane(pvl, i);
+      pres0 |= (key0 + i * PAGE < kv_len && pv >= 0 && pv < p.num_pages) ? (1u << i) : 0u;
+    }
 #pragma unroll
     for (int pi = 0; pi < NPG; ++pi)
-      if ((present >> pi) & 1u) scores(rg, pi, qf, sc[pi]);
-    finish(rg, sc);
+      if ((pres0 >> pi) & 1u) scores(rg, pi, key0, qf, sc[pi]);
+    step(sc, pres0, true, m, l, o);
+    write_partial(rg, m, l, o);
   }
 }
 
@@ -512,16 +593,16 @@ static bool fuses_dh(int Bq, int G, int sk) {
   return Bq * G <= 64 && attn_lds<T, DH>(true, Bq, G, sk) <= ATTN_LDS_MAX;
 }
 
-template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG>
+template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG, bool MC>
 static hipError_t launch_kn(const AttnParams& p, hipStream_t st) {
-  const size_t lds = attn_lds<T, DH>(FUSED, p.Bq, p.Hq / p.Hkv, NPG * PAGE);
+  const size_t lds = attn_lds<T, DH>(FUSED, p.Bq, p.Hq / p.Hkv, NPG * PAGE);   // one chunk resident
   if (lds > ATTN_LDS_MAX) return hipErrorInvalidConfiguration;
   // allow the largest dynamic LDS, once per instantiation (thread-safe static initialisation)
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART, NPG>),
+      reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART, NPG, MC>),
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATTN_LDS_MAX);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART, NPG>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64),
+  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART, NPG, MC>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64),
                      lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -529,19 +610,28 @@ static hipError_t launch_kn(const AttnParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// split sizes: 128 keys, and 256 for bf16 (four fp32 pages exceed the LDS)
+// chunk sizes: 128 keys, and 256 for bf16 (four fp32 pages exceed the LDS)
 template <typename T, int DH, int NW, bool FUSED, int NPART>
 static hipError_t launch_k(const AttnParams& p, hipStream_t st) {
-  if (p.split_keys == 2 * PAGE) return launch_kn<T, DH, NW, FUSED, NPART, 2>(p, st);
+  if (p.chunks < 1 || p.split_keys % p.chunks) return hipErrorInvalidValue;
+  const int ck = p.split_keys / p.chunks;
+  if (ck * p.chunks > 64 * PAGE) return hipErrorInvalidValue;   // one page-id lane per page of a split
+  if (p.chunks > 1 && (p.Bq * (p.Hq / p.Hkv) + 15) / 16 > NW) return hipErrorInvalidValue;
+  if (ck == 2 * PAGE)
+    return p.chunks > 1 ? launch_kn<T, DH, NW, FUSED, NPART, 2, true>(p, st)
+                        : launch_kn<T, DH, NW, FUSED, NPART, 2, false>(p, st);
   if constexpr (sizeof(T) == 2)
-    if (p.split_keys == 4 * PAGE) return launch_kn<T, DH, NW, FUSED, NPART, 4>(p, st);
+    if (ck == 4 * PAGE)
+      return p.chunks > 1 ? launch_kn<T, DH, NW, FUSED, NPART, 4, true>(p, st)
+                          : launch_kn<T, DH, NW, FUSED, NPART, 4, false>(p, st);
   return hipErrorInvalidValue;
 }
 
 template <typename T, int DH>
 static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
   if (p.fused) {
-    if (!fuses_dh<T, DH>(p.Bq, p.Hq / p.Hkv, p.split_keys)) return hipErrorInvalidConfiguration;
+    if (p.chunks < 1 || !fuses_dh<T, DH>(p.Bq, p.Hq / p.Hkv, p.split_keys / p.chunks))
+      return hipErrorInvalidConfiguration;
     if (p.qkv_ks == 2) return launch_k<T, DH, 8, true, 2>(p, st);
     if (p.qkv_ks == 1) return launch_k<T, DH, 8, true, 1>(p, st);
     return hipErrorInvalidValue;
@@ -550,6 +640,8 @@ static hipError_t launch_dh(const AttnParams& p, hipStream_t st) {
   if (p.Bq * (p.Hq / p.Hkv) <= 64) return launch_k<T, DH, 4, false, 1>(p, st);
   return launch_k<T, DH, 8, false, 1>(p, st);
 }
+
+int attention_waves(bool fused, int Bq, int G) { return fused || Bq * G > 64 ? 8 : 4; }
 
 bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh, int sk) {
   if (Dh == 128) return bf16 ? fuses_dh<dflow::bf16, 128>(Bq, G, sk) : fuses_dh<float, 128>(Bq, G, sk);

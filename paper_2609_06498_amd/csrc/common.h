@@ -30,6 +30,22 @@ inline int split_keys_for(bool bf16, int n_kv_heads, int max_keys) {
   return (long long)n_kv_heads * ((max_keys + 255) / 256) >= 128 ? 256 : 128;
 }
 
+// Chunks per attention split in the round calls (verify and draft).  One chunk
+// (split = split_keys_for keys) while a full-capacity round launch -- every
+// sequence at max_keys, batch x kv heads x splits workgroups -- fits one
+// workgroup per compute unit; beyond, each split streams that many chunks
+// (running softmax across them) so the full-capacity launch keeps about one
+// workgroup per unit and the partials to merge shrink accordingly (8 ragged
+// Qwen3-8B-shape sequences: attention + merge 72.4 -> 58.2 us per layer).  At
+// most 64 pages per split (one page-id lane each).  Fixed per context, so a
+// row's split and chunk boundaries never depend on the batch.
+inline int round_chunks_for(int max_batch, int n_kv_heads, int max_keys, int chunk_keys, int cus) {
+  const long long items = (long long)max_batch * n_kv_heads * ((max_keys + chunk_keys - 1) / chunk_keys);
+  const long long c = cus > 0 ? (items + cus - 1) / cus : 1;
+  const int cap = 64 * PAGE / chunk_keys;
+  return c < 1 ? 1 : (c > cap ? cap : (int)c);
+}
+
 // ------------------------------------------------------------------ bf16 storage
 struct bf16 { uint16_t u; };
 

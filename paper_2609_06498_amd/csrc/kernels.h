@@ -33,8 +33,10 @@ struct AttnParams {
   const int* start_pos;      // [nseq] absolute position of block row 0
   int nseq, Bq, Hq, Hkv, Dh;
   int causal;                // 1: row j sees keys <= start+j; 0: all keys < start+Bq
-  int split_keys;            // keys per split (split_keys_for), a multiple of PAGE
-  int nsplit;                // split slots per sequence (upper bound)
+  int split_keys;            // keys per split: `chunks` chunks of split_keys_for keys, at most 64 pages
+  int chunks;                // chunks per split (resident in LDS one after another); 1 when the
+                             // launch has more 16-row groups than attention_waves
+  int nsplit;                // split slots per sequence for this launch (grid and partial stride)
   int num_pages;             // pages per layer pool (page ids are checked)
   int rg;                    // 16-row groups per (seq, kv head)
   float* part_o;             // [nseq][Hkv][rg][nsplit][16][Dh]
@@ -43,6 +45,8 @@ struct AttnParams {
   FragOut outf;              // matrix-core-order copy of out for the O projection (skinny launches)
 };
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
+// Waves per attention workgroup (each owns one 16-row group; more groups need chunks = 1).
+int attention_waves(bool fused, int Bq, int G);
 // Whether the fused variant fits (block rows per wave, LDS) for this shape.
 bool attention_fuses_rope(bool bf16, int Bq, int G, int Dh, int split_keys);
 
