@@ -95,19 +95,18 @@ __device__ inline int vfrag_off(int slot, int e) {
 //  3. Chunk by chunk, page by page in key order: the staged page goes to LDS
 //     (its registers then take the next chunk's page), the block rows replace
 //     their (stale) slots, and every wave computes the masked scores of its
-//     first row group against the page (S^T = K Q^T on the matrix cores), so
-//     early pages are consumed while later ones still arrive.
-//  4. Per chunk one softmax step over the chunk's scores: the running row
-//     maximum, the rescale of the running sum and output by 2^(m_old - m_new)
-//     (skipped for the first chunk), exp2 of the scores, P V on the matrix
-//     cores; after the last chunk the split partial (m, l, O) of the row
-//     group.  A wave's further row groups (single-chunk splits only) then run
-//     over the resident pages.  The combine kernel merges the splits in split
+//     first row group against the page (S^T = K Q^T on the matrix cores) and
+//     takes one running-softmax step over them: the row maximum so far, the
+//     rescale of the running sum and output by 2^(m_old - m_new), exp2 of the
+//     scores and P V on the matrix cores.  Early pages are consumed while
+//     later ones still arrive; after the last page the split partial (m, l,
+//     O) of the row group is written.
+//  4. A wave's further row groups (single-chunk splits only) then run over
+//     the resident pages.  The combine kernel merges the splits in split
 //     order.
 // A row's arithmetic depends only on its own visible keys and the fixed split
-// and chunk boundaries, never on the batch it is part of.  A single-chunk
-// split computes exactly what a one-step softmax over the split does; MC = 0
-// instantiates single-chunk splits only (no chunk loop, no rescale code).
+// boundaries (and page order within them), never on the batch it is part of.
+// MC = 0 instantiates single-chunk splits only (no chunk loop).
 template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG, bool MC>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
@@ -365,78 +364,64 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
         }
     }
   };
-  // one softmax step over the chunk's present pages: running maximum m (log2
-  // units) and sum l of row lane&15, running output o (row 4*(lane>>4)+r of
-  // o[dt][r]); the first step starts from m = -inf, l = 0, o = 0 unscaled
-  auto step = [&](score_t (&sc)[NPG], unsigned pres, bool first, float& m, float& l, f32x4_t (&o)[DT]) {
+  // one softmax step over page pi's scores: running maximum m (log2 units)
+  // and sum l of row lane&15, running output o (row 4*(lane>>4)+r of
+  // o[dt][r]); the state starts at m = -inf, l = 0, o = 0, and a step rescales
+  // it by 2^(m_old - m_new) before adding the page's terms
+  auto step = [&](score_t& sc, int pi, float& m, float& l, f32x4_t (&o)[DT]) {
     float mx = -INFINITY;
 #pragma unroll
-    for (int pi = 0; pi < NPG; ++pi)
-      if ((pres >> pi) & 1u)                   // uniform
+    for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[pi][kt][r]);
+      for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sc[kt][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     // scores are raw dot products; in log2 units a score is s * sl2 and the
-    // row maximum is mx * sl2 (sl2 > 0).  A row with no visible key keeps
-    // m = -inf, l = 0 and a zero output: its scores are all -inf and
+    // row maximum is mx * sl2 (sl2 > 0).  A row with no visible key so far
+    // keeps m = -inf, l = 0 and a zero output: its scores are all -inf and
     // exponentiate to 0 against a finite reference.
-    mx *= sl2;
-    const float mn = first ? mx : fmaxf(m, mx);
+    const float mn = fmaxf(m, mx * sl2);
     const float mref = mn == -INFINITY ? 0.f : mn;
-    if (!first) {                              // uniform: rescale the running sum and output
-      const float f = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mref);
-      l *= f;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float fr = __shfl(f, 4 * (lane >> 4) + r, 64);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt][r] *= fr;
-      }
-    }
+    const float f = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mref);
     m = mn;
     float ls = 0.f;
 #pragma unroll
-    for (int pi = 0; pi < NPG; ++pi) {
-      if (!((pres >> pi) & 1u)) continue;      // uniform
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // hardware 2^x: arguments are <= 0; results below 2^-126 flush to 0
+        const float e = __builtin_amdgcn_exp2f(fmaf(sc[kt][r], sl2, -mref));
+        sc[kt][r] = e;
+        ls += e;
+      }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    l = fmaf(l, f, ls);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float fr = __shfl(f, 4 * (lane >> 4) + r, 64);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt][r] *= fr;
+    }
+    if constexpr (KL == 8) {
+      // P V with 32 keys per matrix-core op: lane group g supplies keys
+      // 4g..4g+3 of key tiles 2c and 2c+1, and V holds the same keys in
+      // one 16-byte fragment
+      const u32x4_t* vb = reinterpret_cast<const u32x4_t*>(lv + (size_t)pi * PG);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const float (&a)[4] = sc[2 * c];
+        const float (&b)[4] = sc[2 * c + 1];
+        const u32x4_t pa = {f2bf2(a[0], a[1]), f2bf2(a[2], a[3]), f2bf2(b[0], b[1]), f2bf2(b[2], b[3])};
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] = mma_frag(T(), pa, vb[(c * DT + dt) * 64 + lane], o[dt]);
+      }
+    } else {
+      const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          // hardware 2^x: arguments are <= 0; results below 2^-126 flush to 0
-          const float e = __builtin_amdgcn_exp2f(fmaf(sc[pi][kt][r], sl2, -mref));
-          sc[pi][kt][r] = e;
-          ls += e;
-        }
-    }
-    ls += __shfl_xor(ls, 16, 64);
-    ls += __shfl_xor(ls, 32, 64);
-    l = first ? ls : l + ls;
-#pragma unroll
-    for (int pi = 0; pi < NPG; ++pi) {
-      if (!((pres >> pi) & 1u)) continue;      // uniform
-      if constexpr (KL == 8) {
-        // P V with 32 keys per matrix-core op: lane group g supplies keys
-        // 4g..4g+3 of key tiles 2c and 2c+1, and V holds the same keys in
-        // one 16-byte fragment
-        const u32x4_t* vb = reinterpret_cast<const u32x4_t*>(lv + (size_t)pi * PG);
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const float (&a)[4] = sc[pi][2 * c];
-          const float (&b)[4] = sc[pi][2 * c + 1];
-          const u32x4_t pa = {f2bf2(a[0], a[1]), f2bf2(a[2], a[3]), f2bf2(b[0], b[1]), f2bf2(b[2], b[3])};
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_frag(T(), pa, vb[(c * DT + dt) * 64 + lane], o[dt]);
-        }
-      } else {
-        const vfrag_t* vb = reinterpret_cast<const vfrag_t*>(lv + (size_t)pi * PG);
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[pi][kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
-      }
+        for (int dt = 0; dt < DT; ++dt) o[dt] = mma_pv_frag<T>(sc[kt], vb[(kt * DT + dt) * 64 + lane], o[dt]);
     }
   };
   auto write_partial = [&](int rg, float m, float l, const f32x4_t (&o)[DT]) {
@@ -462,7 +447,7 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     }
   };
 
-  score_t sc[NPG];
+  score_t sc;
   float m_run = -INFINITY, l_run = 0.f;
   f32x4_t o_run[DT];
 #pragma unroll
@@ -499,7 +484,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
         }
         if (c == 0 && pi == 0 && own) load_q(w, qf);   // LDS reads only
       }
-      if (own && ((present >> pi) & 1u)) scores(w, pi, kc0, qf, sc[pi]);
+      if (own && ((present >> pi) & 1u)) {   // uniform
+        scores(w, pi, kc0, qf, sc);
+        step(sc, pi, m_run, l_run, o_run);
+      }
     }
   };
   // chunks 0 .. nch-2 prefetch the next one unconditionally; the last chunk is peeled
@@ -509,13 +497,11 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       const unsigned pres_next = chunk_pages(c + 1, pg_next);
       if (c > 0) __syncthreads();              // every wave is done with the previous chunk's pages
       chunk(c, true, pg_next);
-      if (own) step(sc, present, c == 0, m_run, l_run, o_run);
       present = pres_next;
     }
     if (nch > 1) __syncthreads();
   }
   chunk(nch - 1, false, pgid);
-  if (own) step(sc, present, nch == 1, m_run, l_run, o_run);
   if (own) write_partial(w, m_run, l_run, o_run);
   // further row groups: single-chunk splits only (the host launches no others
   // with more row groups than waves); pages resident, no barrier
@@ -533,8 +519,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     }
 #pragma unroll
     for (int pi = 0; pi < NPG; ++pi)
-      if ((pres0 >> pi) & 1u) scores(rg, pi, key0, qf, sc[pi]);
-    step(sc, pres0, true, m, l, o);
+      if ((pres0 >> pi) & 1u) {
+        scores(rg, pi, key0, qf, sc);
+        step(sc, pi, m, l, o);
+      }
     write_partial(rg, m, l, o);
   }
 }
