@@ -61,10 +61,21 @@ def parse():
                     help="issue the greedy round's launches one by one instead of replaying its recorded HIP graph")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this size first (calibrates HBM counters)")
+    ap.add_argument("--counter-pass", action="store_true",
+                    help="the program of an HBM counter pass (run under rocprofv3 --pmc): set-up prefill, the "
+                         "calibration copy, then --steps eager rounds with the drafter's own drafts; no timing, "
+                         "no JSON line")
+    ap.add_argument("--traffic-record", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the dominant kernel's HBM counter record from the counter_collection.csv files of "
+                         "a FETCH_SIZE and a WRITE_SIZE counter pass (host only, no GPU)")
     return ap.parse_args()
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# the dominant kernel at the Qwen3-8B shape: the gate|up SwiGLU projection of a round (M = 16 rows)
+TRAFFIC_KERNEL = ("gemm.swiglu N=24576 K=4096 M=16", "_ZN5dflow11gemm_kernelINS_4bf16ELi2ELi1ELi3ELb1EEEvNS_10GemmParamsE",
+                  "gemm_kernel<dflow::bf16, 2, 1, 3, true>", 24576 * 4096 * 2 + 16 * 4096 * 2 + 16 * 12288 * 2)
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
 NSEG = 4   # timed segments (median and min per-step time besides the whole-run value)
 
 
@@ -87,6 +98,47 @@ def measured_traffic(kernel_name):
     except (OSError, ValueError, KeyError):
         return None
     return int(rec["fetch_bytes"] + rec["write_bytes"])
+
+
+def write_traffic_record(fetch_csv, write_csv, copy_mib=256):
+    """HBM bytes per launch of the dominant kernel from two rocprofv3 counter
+    passes of `bench.py --counter-pass --calib-copy-mib 256`: each counter's
+    mean per dispatch of that kernel, divided by the same counter's reading
+    per byte of the calibration copy (copy_mib MiB read and written).  The
+    record is keyed to the kernel's machine code in the library built here."""
+    import csv
+    from paper_2609_06498_amd import library_path
+    from paper_2609_06498_amd.codeobj import kernel_code_digest
+    name, symbol, pretty, alg = TRAFFIC_KERNEL
+    copy_bytes = copy_mib << 20
+
+    def read(path, counter):
+        per, copies = [], []
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                v = float(r["Counter_Value"])
+                if pretty in r["Kernel_Name"]:
+                    per.append(v)
+                elif COPY_KERNEL in r["Kernel_Name"]:
+                    copies.append(v)
+        if not per or not copies:
+            raise SystemExit(f"{path}: no {counter} records for {pretty} or the calibration copy")
+        return sum(per) / len(per), max(copies), len(per)
+
+    f_kib, f_copy, nd = read(fetch_csv, "FETCH_SIZE")
+    w_kib, w_copy, _ = read(write_csv, "WRITE_SIZE")
+    ff, wf = f_copy * 1024 / copy_bytes, w_copy * 1024 / copy_bytes
+    rec = {"kernel": name, "symbol": symbol, "code_sha256": kernel_code_digest(library_path(), symbol),
+           "fetch_bytes": int(round(f_kib * 1024 / ff)), "write_bytes": int(round(w_kib * 1024 / wf)),
+           "fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1), "dispatches": nd,
+           "calibration_copy_bytes": copy_bytes, "copy_fetch_kib": f_copy, "copy_write_kib": w_copy,
+           "fetch_factor": round(ff, 5), "write_factor": round(wf, 5), "algorithmic_bytes": alg}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
 
 
 def log(*a):
@@ -208,6 +260,9 @@ def build_trajectory(rt, sess, prompts, need, sched, B, b):
 
 def main():
     args = parse()
+    if args.traffic_record:
+        write_traffic_record(*args.traffic_record, copy_mib=args.calib_copy_mib or 256)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the DFlow round is a single-GPU "
               f"data-parallel step (sequences shard across GPUs with no exchange); it runs on one GPU only.", file=sys.stderr)
@@ -262,6 +317,13 @@ def main():
         del src, dst
 
     carry_on = args.carry == "on"
+    if args.counter_pass:   # the rounds' kernels with the drafter's own drafts, nothing timed
+        sess.prefill(prompts)
+        for _ in range(K):
+            sess.round(carry_on)
+        torch.cuda.synchronize()
+        log(f"counter pass: {K} rounds, status {rt.status()}")
+        return
     if kr > 0:
         traj, L, _, _ = build_trajectory(rt, sess, prompts, need, sched, B, b)
 

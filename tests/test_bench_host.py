@@ -53,3 +53,29 @@ def test_gemm_byte_model_at_the_8b_shape():
         + (3 * d * 4096 + 4096 * 2 * d) * 2 + Ld * 2 * 1024 * d * 2
     assert weights <= gb <= weights * 1.01, (gb, weights)
     assert nl == (L + Ld) * 4 + 2 + 1 + 2 + 1
+
+
+def test_traffic_record_arithmetic(tmp_path, monkeypatch):
+    """The record writer scales each counter's mean per dispatch of the
+    dominant kernel by the same counter's reading for the calibration copy
+    (synthetic counter files; the digest lookup is stubbed)."""
+    import paper_2609_06498_amd.codeobj as co
+    name, symbol, pretty, _ = bench.TRAFFIC_KERNEL
+    hdr = "Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value\n"
+
+    def csv_file(path, counter, copy_kib, vals):
+        rows = [f'1,"{bench.COPY_KERNEL}",{counter},1.5', f'2,"{bench.COPY_KERNEL}",{counter},{copy_kib}']
+        rows += [f'{3 + i},"void dflow::{pretty}(dflow::GemmParams)",{counter},{v}' for i, v in enumerate(vals)]
+        rows.append(f'99,"void dflow::other_kernel()",{counter},12345')
+        path.write_text(hdr + "\n".join(rows) + "\n")
+        return str(path)
+
+    f = csv_file(tmp_path / "f.csv", "FETCH_SIZE", 131072.0, [1000.0, 1002.0])
+    w = csv_file(tmp_path / "w.csv", "WRITE_SIZE", 262144.0, [768.0, 768.0])
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic.json"))
+    monkeypatch.setattr(co, "kernel_code_digest", lambda lib, sym: "d" * 64)
+    bench.write_traffic_record(f, w, copy_mib=256)
+    rec = json.loads((tmp_path / "traffic.json").read_text())
+    assert rec["kernel"] == name and rec["symbol"] == symbol and rec["code_sha256"] == "d" * 64
+    assert rec["fetch_factor"] == 0.5 and rec["write_factor"] == 1.0 and rec["dispatches"] == 2
+    assert rec["fetch_bytes"] == 1001 * 1024 * 2 and rec["write_bytes"] == 768 * 1024
