@@ -20,7 +20,7 @@ __global__ void __launch_bounds__(512) gemm_kernel(GemmParams p) {
   constexpr int KL = TT<T>::KL;
   constexpr int KT = TT<T>::KT;
   // k tiles per pipeline stage: 4 fragments of weights per stage and buffer
-  constexpr int U = (MT * NG >= 4) ? 1 : 4 / (MT * NG);
+  constexpr int U = (MT * NG >= 8) ? 1 : 8 / (MT * NG);
   extern __shared__ float lds[];
   const int lane = threadIdx.x & 63;
   // wave index as a scalar: keeps the k-range bounds and the pipeline control uniform
