@@ -9,8 +9,11 @@
   kernel: the launch configuration bench.py times at b = 1.
 * qwen3-8b-b8-d5 -- the ragged eight-sequence workload (its prompts, 2251 to
   6183 tokens; 128 rows per round: tiled GEMMs, the K-split residual and
-  gate/up paths, the range-split drafter projections, attention over up to
-  25 splits per sequence) at five target layers.  Sequences never interact in
+  gate/up paths, the range-split drafter projections; at this context's
+  capacity the round attention runs multi-chunk splits -- seven 256-key
+  chunks streamed per split with the running softmax carried across them --
+  so the longest sequence's rows cross four splits and 25 chunks) at five
+  target layers.  Sequences never interact in
   the method, so the oracle follows the shortest and the longest sequence and
   their rows of the batched rounds are compared.
 
