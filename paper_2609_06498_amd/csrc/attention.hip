@@ -490,6 +490,89 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
       }
     }
   };
+  // Fused multi-chunk splits: a chunk's pages are staged first, then the two
+  // halves of the workgroup (waves w and w + 4, same row group) take the
+  // even and the odd pages, each with a running softmax of its own, and the
+  // two states are merged at the end -- twice the waves on the matrix cores
+  // and the exponentials while the next chunk streams in.
+  if constexpr (MC && FUSED) {
+    static_assert(NW == 8, "fused launches have eight waves");
+    const int rgw = w & 3, par = w >> 2;
+    const bool own2 = rgw < nrg;              // uniform (R <= 64: at most four row groups)
+    auto chunk2 = [&](int c, bool next, const int (&pg_next)[NPG]) {
+      const int kc0 = key0 + c * SK;
+#pragma unroll
+      for (int pi = 0; pi < NPG; ++pi) {
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+          reinterpret_cast<u32x4_t*>(lk + (size_t)pi * PG)[threadIdx.x + it * NT] = kr[pi][it];
+          reinterpret_cast<u32x4_t*>(lv + (size_t)pi * PG)[threadIdx.x + it * NT] = vr[pi][it];
+        }
+        if (next) issue_page(pi, pg_next[pi]);   // the next chunk's page streams in meanwhile
+      }
+      __syncthreads();
+      // block rows of this chunk replace the slots staged from the cache
+      const int jc0 = max(jlo, kc0 - t0), jc1 = min(jhi, kc0 + SK - t0);
+      if (jc0 < jc1) {                         // uniform
+        for (int e = threadIdx.x; e < (jc1 - jc0) * DH; e += NT) {
+          const int j = jc0 + e / DH, d = e % DH;
+          const int pos = t0 + j, pi = (pos - kc0) / PAGE, slot = pos % PAGE;
+          const T* row = ln + (size_t)(j - jlo) * 2 * DH;
+          lk[(size_t)pi * PG + kfrag_off<T, DH>(slot, d)] = row[d];
+          lv[(size_t)pi * PG + vfrag_off<T, DH>(slot, d)] = row[DH + d];
+        }
+        __syncthreads();
+      }
+      if (c == 0 && own2) load_q(rgw, qf);     // LDS reads only
+#pragma unroll
+      for (int pi = 0; pi < NPG; ++pi)
+        if ((pi & 1) == par && own2 && ((present >> pi) & 1u)) {   // uniform
+          scores(rgw, pi, kc0, qf, sc);
+          step(sc, pi, m_run, l_run, o_run);
+        }
+    };
+    for (int c = 0; c + 1 < nch; ++c) {        // uniform
+      int pg_next[NPG];
+      const unsigned pres_next = chunk_pages(c + 1, pg_next);
+      if (c > 0) __syncthreads();              // every wave is done with the previous chunk's pages
+      chunk2(c, true, pg_next);
+      present = pres_next;
+    }
+    if (nch > 1) __syncthreads();
+    chunk2(nch - 1, false, pgid);
+    // merge: the odd-page state of each row group through LDS into the even-page one
+    __syncthreads();                           // the pages are no longer read
+    float* scr = reinterpret_cast<float*>(lk);     // [4][DT][4][64] outputs, then [4][16][2] (m, l)
+    float* sml = scr + 4 * DT * 4 * 64;
+    if (own2 && par == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) scr[((rgw * DT + dt) * 4 + r) * 64 + lane] = o_run[dt][r];
+      if (lane < 16) {
+        sml[(rgw * 16 + lane) * 2] = m_run;
+        sml[(rgw * 16 + lane) * 2 + 1] = l_run;
+      }
+    }
+    __syncthreads();
+    if (own2 && par == 0) {
+      const float m1 = sml[(rgw * 16 + (lane & 15)) * 2], l1 = sml[(rgw * 16 + (lane & 15)) * 2 + 1];
+      const float M = fmaxf(m_run, m1);
+      const float Mref = M == -INFINITY ? 0.f : M;
+      const float f0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - Mref);
+      const float f1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - Mref);
+      const float l = fmaf(l_run, f0, l1 * f1);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float g0 = __shfl(f0, 4 * (lane >> 4) + r, 64), g1 = __shfl(f1, 4 * (lane >> 4) + r, 64);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          o_run[dt][r] = fmaf(o_run[dt][r], g0, scr[((rgw * DT + dt) * 4 + r) * 64 + lane] * g1);
+      }
+      write_partial(rgw, M, l, o_run);
+    }
+    return;
+  }
   // chunks 0 .. nch-2 prefetch the next one unconditionally; the last chunk is peeled
   if constexpr (MC) {
     for (int c = 0; c + 1 < nch; ++c) {        // uniform

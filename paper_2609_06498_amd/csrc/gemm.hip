@@ -746,7 +746,31 @@ static hipError_t launch_ng(const GemmParams& p, const GemmShape& sh, hipStream_
 // weight-streaming kernel adds its waves' ranges, so each row is bit-identical
 // to that kernel's -- then applies its EPI_RESID epilogue: rnd(sum + R) to Y
 // (and Y2) and the strip's sum of squares of the stored values.
-template <typename T>
+// The KS parts (KS > 0: all loads in flight at once; KS = 0: a loop over ks)
+// of a thread's 16 columns, summed in part order from +0.
+template <int KS>
+__device__ inline void sum_parts16(const float* part, size_t part_stride, int ks, size_t off, float (&s)[16]) {
+#pragma unroll
+  for (int c = 0; c < 16; ++c) s[c] = 0.f;
+  if constexpr (KS > 0) {
+    float v[KS][16];
+#pragma unroll
+    for (int h = 0; h < KS; ++h) Row16<float>::load(part + h * part_stride + off, v[h]);
+#pragma unroll
+    for (int h = 0; h < KS; ++h)
+#pragma unroll
+      for (int c = 0; c < 16; ++c) s[c] += v[h][c];
+  } else {
+    for (int h = 0; h < ks; ++h) {
+      float v[16];
+      Row16<float>::load(part + h * part_stride + off, v);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) s[c] += v[c];
+    }
+  }
+}
+
+template <typename T, int KS>
 __global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, size_t part_stride, int ks, int M,
                                                            int N, const T* R, int ldr, T* Y, int ldy, T* Y2, int ldy2,
                                                            float* ssq_out, int ssq_ld, int strip0, FragOut yf,
@@ -755,30 +779,17 @@ __global__ void __launch_bounds__(256) resid_reduce_kernel(const float* part, si
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= M * nstrips) return;
   const int m = e / nstrips, j = e - m * nstrips;
-  float s[16];
-#pragma unroll
-  for (int c = 0; c < 16; ++c) s[c] = 0.f;
-  for (int h = 0; h < ks; ++h) {
-    const float4* src = reinterpret_cast<const float4*>(part + h * part_stride + (size_t)m * N + j * 16);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 v = src[q];
-      s[4 * q] += v.x;
-      s[4 * q + 1] += v.y;
-      s[4 * q + 2] += v.z;
-      s[4 * q + 3] += v.w;
-    }
-  }
+  float r[16], s[16];
+  Row16<T>::load(R + (size_t)m * ldr + j * 16, r);
+  sum_parts16<KS>(part, part_stride, ks, (size_t)m * N + j * 16, s);
   float sq = 0.f;
 #pragma unroll
   for (int c = 0; c < 16; ++c) {
-    const int col = j * 16 + c;
-    const float v = TT<T>::rnd(s[c] + TT<T>::ld(R, (size_t)m * ldr + col));
-    TT<T>::st(Y, (size_t)m * ldy + col, v);
-    if (Y2) TT<T>::st(Y2, (size_t)m * ldy2 + col, v);
-    s[c] = v;
-    sq += v * v;
+    s[c] = TT<T>::rnd(s[c] + r[c]);
+    sq += s[c] * s[c];
   }
+  Row16<T>::store(Y + (size_t)m * ldy + j * 16, s);
+  if (Y2) Row16<T>::store(Y2 + (size_t)m * ldy2 + j * 16, s);
   frag_st_run<T>(yf, m, j * 16, s, 16);
   frag_st_run<T>(y2f, m, j * 16, s, 16);
   if (ssq_out) ssq_out[(size_t)m * ssq_ld + strip0 + j] = sq;
@@ -791,7 +802,7 @@ int split_parts(int epi, int ntiles, int ktiles) { return gemm_shape(ntiles, kti
 // weight-streaming kernel's epilogue (row scale, silu(gate) * up, rounding).
 // Every 16-lane group computes the row scale (the same value) before any lane
 // leaves.
-template <typename T, bool NORM>
+template <typename T, bool NORM, int KS>
 __global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const float* part, size_t part_stride,
                                                             int ks, int N) {
   const int m = blockIdx.y;
@@ -800,19 +811,7 @@ __global__ void __launch_bounds__(256) swiglu_reduce_kernel(GemmParams p, const 
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= N / 16) return;
   float s[16];
-#pragma unroll
-  for (int c = 0; c < 16; ++c) s[c] = 0.f;
-  for (int h = 0; h < ks; ++h) {
-    const float4* src = reinterpret_cast<const float4*>(part + h * part_stride + (size_t)m * N + j * 16);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float4 v = src[q];
-      s[4 * q] += v.x;
-      s[4 * q + 1] += v.y;
-      s[4 * q + 2] += v.z;
-      s[4 * q + 3] += v.w;
-    }
-  }
+  sum_parts16<KS>(part, part_stride, ks, (size_t)m * N + j * 16, s);
   float y[8];
 #pragma unroll
   for (int c = 0; c < 8; ++c) {
@@ -849,11 +848,21 @@ static hipError_t launch_swiglu_split(const GemmParams& p, hipStream_t st) {
   hipError_t e = launch_tile<T, EPI_STORE_F32, false>(q, sh, ks, st);
   if (e != hipSuccess) return e;
   const dim3 grid((p.ntiles + 255) / 256, p.M);
-  if (p.norm)
-    hipLaunchKernelGGL((swiglu_reduce_kernel<T, true>), grid, dim3(256), 0, st, p, p.part_ws, q.y_part, ks, q.ldy);
-  else
-    hipLaunchKernelGGL((swiglu_reduce_kernel<T, false>), grid, dim3(256), 0, st, p, p.part_ws, q.y_part, ks, q.ldy);
-  return hipGetLastError();
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, p, p.part_ws, q.y_part, ks, q.ldy);
+    return hipGetLastError();
+  };
+  // the part count as a template argument where it is one of the wave counts, so all loads are in flight at once
+  if (p.norm) {
+    if (ks == 2) return go(swiglu_reduce_kernel<T, true, 2>);
+    if (ks == 4) return go(swiglu_reduce_kernel<T, true, 4>);
+    if (ks == 8) return go(swiglu_reduce_kernel<T, true, 8>);
+    return go(swiglu_reduce_kernel<T, true, 0>);
+  }
+  if (ks == 2) return go(swiglu_reduce_kernel<T, false, 2>);
+  if (ks == 4) return go(swiglu_reduce_kernel<T, false, 4>);
+  if (ks == 8) return go(swiglu_reduce_kernel<T, false, 8>);
+  return go(swiglu_reduce_kernel<T, false, 0>);
 }
 
 // A narrow weight (O, down) at more than SPLIT_MIN_ROWS rows: the weight-
@@ -879,10 +888,16 @@ static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
   hipError_t e = launch_tile<T, EPI_STORE_F32, false>(q, sh, ks, st);
   if (e != hipSuccess) return e;
   const int items = p.M * p.ntiles;
-  hipLaunchKernelGGL(resid_reduce_kernel<T>, dim3((items + 255) / 256), dim3(256), 0, st, p.part_ws, q.y_part, ks,
-                     p.M, q.ldy, reinterpret_cast<const T*>(p.R), p.ldr, reinterpret_cast<T*>(p.Y), p.ldy,
-                     reinterpret_cast<T*>(p.Y2), p.ldy2, p.ssq_out, p.ssq_out_ld, 0, p.yf, p.y2f);
-  return hipGetLastError();
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3((items + 255) / 256), dim3(256), 0, st, p.part_ws, q.y_part, ks, p.M, q.ldy,
+                       reinterpret_cast<const T*>(p.R), p.ldr, reinterpret_cast<T*>(p.Y), p.ldy,
+                       reinterpret_cast<T*>(p.Y2), p.ldy2, p.ssq_out, p.ssq_out_ld, 0, p.yf, p.y2f);
+    return hipGetLastError();
+  };
+  if (ks == 2) return go(resid_reduce_kernel<T, 2>);
+  if (ks == 4) return go(resid_reduce_kernel<T, 4>);
+  if (ks == 8) return go(resid_reduce_kernel<T, 8>);
+  return go(resid_reduce_kernel<T, 0>);
 }
 
 // Range split of the narrow drafter-side projections (W_c, relay MLP,
@@ -894,7 +909,7 @@ static hipError_t launch_resid_split(const GemmParams& p, hipStream_t st) {
 // folds the parts in range order from +0 -- that kernel's wave fold -- and
 // applies its epilogue.  One workgroup row per output row (every 16-lane group
 // computes the row scale); four columns per thread.
-template <typename T, int EPI, bool NORM>
+template <typename T, int EPI, bool NORM, int KS>
 __global__ void __launch_bounds__(256) range_reduce_kernel(GemmParams p, const float* part, size_t part_stride,
                                                            int nw, int N) {
   const int m = blockIdx.y;
@@ -903,12 +918,26 @@ __global__ void __launch_bounds__(256) range_reduce_kernel(GemmParams p, const f
   const int c4 = blockIdx.x * 256 + threadIdx.x;
   if (c4 >= N / 4) return;
   float s[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int w = 0; w < nw; ++w) {
-    const float4 v = *reinterpret_cast<const float4*>(part + (size_t)w * part_stride + (size_t)m * N + 4 * c4);
-    s[0] += v.x;
-    s[1] += v.y;
-    s[2] += v.z;
-    s[3] += v.w;
+  const float* src = part + (size_t)m * N + 4 * c4;
+  if constexpr (KS > 0) {   // all parts' loads in flight at once, summed in part order
+    float4 v[KS];
+#pragma unroll
+    for (int w = 0; w < KS; ++w) v[w] = *reinterpret_cast<const float4*>(src + (size_t)w * part_stride);
+#pragma unroll
+    for (int w = 0; w < KS; ++w) {
+      s[0] += v[w].x;
+      s[1] += v[w].y;
+      s[2] += v[w].z;
+      s[3] += v[w].w;
+    }
+  } else {
+    for (int w = 0; w < nw; ++w) {
+      const float4 v = *reinterpret_cast<const float4*>(src + (size_t)w * part_stride);
+      s[0] += v.x;
+      s[1] += v.y;
+      s[2] += v.z;
+      s[3] += v.w;
+    }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -938,8 +967,14 @@ bool range_split_applies(int epi, int M, int ntiles, int ksplit) {
 template <typename T, int EPI, bool NORM>
 static hipError_t launch_range_reduce(const GemmParams& p, size_t part_stride, int nw, int N, hipStream_t st) {
   const dim3 grid((N / 4 + 255) / 256, p.M);
-  hipLaunchKernelGGL((range_reduce_kernel<T, EPI, NORM>), grid, dim3(256), 0, st, p, p.part_ws, part_stride, nw, N);
-  return hipGetLastError();
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, p, p.part_ws, part_stride, nw, N);
+    return hipGetLastError();
+  };
+  if (nw == 2) return go(range_reduce_kernel<T, EPI, NORM, 2>);
+  if (nw == 4) return go(range_reduce_kernel<T, EPI, NORM, 4>);
+  if (nw == 8) return go(range_reduce_kernel<T, EPI, NORM, 8>);
+  return go(range_reduce_kernel<T, EPI, NORM, 0>);
 }
 
 template <typename T>
