@@ -167,7 +167,7 @@ Layout plan(const dflow_dims* d, int* nsplit_out, int* part_items_out, int* lm_g
   const int rows_round = d->max_batch * d->block;
   const int mmax = rows_round > d->max_rows ? rows_round : d->max_rows;
   const int G = d->n_heads / d->n_kv_heads;
-  const int split_keys = split_keys_for(d->dtype == DFLOW_BF16, d->n_kv_heads, d->max_pages * PAGE);
+  const int split_keys = split_keys_for(d->dtype == DFLOW_BF16, d->max_batch, d->n_kv_heads, d->max_pages * PAGE);
   const int nsplit = (d->max_pages * PAGE + split_keys - 1) / split_keys;
   const int rg_round = (d->block * G + 15) / 16, rg_pre = (d->max_rows * G + 15) / 16;
   int items = d->max_batch * rg_round;
@@ -304,7 +304,7 @@ extern "C" int dflow_create(const dflow_dims* dims, const dflow_weights* w, cons
   c->pool_layer_elems = (size_t)dims->num_pages * dims->n_kv_heads * PAGE * dims->head_dim;
 
   Layout L = plan(dims, &c->nsplit, &c->part_items, &c->lm_groups);
-  c->split_keys = split_keys_for(c->bf, dims->n_kv_heads, dims->max_pages * PAGE);
+  c->split_keys = split_keys_for(c->bf, dims->max_batch, dims->n_kv_heads, dims->max_pages * PAGE);
   c->round_chunks = round_chunks_for(dims->max_batch, dims->n_kv_heads, dims->max_pages * PAGE, c->split_keys, c->cus);
   c->ws = workspace;
   c->ws_bytes = L.total;

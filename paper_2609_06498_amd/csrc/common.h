@@ -21,13 +21,16 @@ constexpr int SSQ_LD = 512;       // row stride of the RMSNorm partial sums [row
 // pages fp32, so the staged K+V pages of a split fit the 160 KB LDS of a CU.
 // Split size of a context, from its dimensions only (never from a batch): the
 // largest split (fewest partials to merge, every split re-reads the query
-// rows) unless the kv heads x splits of a full-capacity sequence would leave
-// most compute units idle, then 128 keys (Qwen3-1.7B shape at context 1024:
-// attention 16.5 -> 13.8 us per layer; at context 4096 256-key splits win,
-// 18.7 vs 25.8 us).
-inline int split_keys_for(bool bf16, int n_kv_heads, int max_keys) {
+// rows) unless a full-capacity round launch with it -- max_batch sequences
+// at max_keys, one workgroup per kv head and split -- would leave compute
+// units idle (fewer workgroups than the MI355X's 256 units), then 128 keys
+// (Qwen3-1.7B shape at context 1024: attention 16.5 -> 13.8 us per layer;
+// Qwen3-8B shape at context 4096, b = 1: 19.3 -> 18.7 us; at 8 sequences the
+// 256-key chunks of the multi-chunk splits win).
+constexpr int SPLIT_RULE_CUS = 256;
+inline int split_keys_for(bool bf16, int max_batch, int n_kv_heads, int max_keys) {
   if (!bf16) return 128;
-  return (long long)n_kv_heads * ((max_keys + 255) / 256) >= 128 ? 256 : 128;
+  return (long long)max_batch * n_kv_heads * ((max_keys + 255) / 256) >= SPLIT_RULE_CUS ? 256 : 128;
 }
 
 // Chunks per attention split in the round calls (verify and draft).  One chunk
