@@ -210,6 +210,16 @@ int dflow_destroy(dflow_ctx* ctx);
  * null context. */
 int dflow_qkv_parts(const dflow_ctx* ctx);
 
+/* Attention work split of the round calls (verify and draft): *chunk_keys
+ * receives the keys of one LDS-resident chunk (128 or 256) and *chunks the
+ * chunks per split (a split covers chunks * chunk_keys keys at fixed absolute
+ * positions, the running softmax carried across its chunks; prefill, and a
+ * call whose query rows need more row groups than one workgroup has waves,
+ * use one chunk per split).  Fixed at create from max_batch, the kv heads and the
+ * capacity; for tests and byte accounting.  Returns 0, or DFLOW_EINVAL on a
+ * null argument. */
+int dflow_attention_split(const dflow_ctx* ctx, int* chunk_keys, int* chunks);
+
 /* Prompt processing for sequence slot `seq` (set-up, not part of the round):
  * target KV for positions 0..len-1, fused features and drafter context K/V
  * for the same positions, and first_anchor[0] = the target's greedy token

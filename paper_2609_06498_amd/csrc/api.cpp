@@ -949,6 +949,13 @@ extern "C" int kv_commit(dflow_ctx* c, hipStream_t st, int nseq, const int32_t* 
 
 extern "C" int dflow_qkv_parts(const dflow_ctx* c) { return c ? c->qkv_ks : fail(DFLOW_EINVAL, "qkv_parts: null context"); }
 
+extern "C" int dflow_attention_split(const dflow_ctx* c, int* chunk_keys, int* chunks) {
+  if (!c || !chunk_keys || !chunks) return fail(DFLOW_EINVAL, "attention_split: null argument");
+  *chunk_keys = c->split_keys;
+  *chunks = c->round_chunks;
+  return DFLOW_OK;
+}
+
 extern "C" int dflow_move_slot(dflow_ctx* c, hipStream_t st, int from, int to) {
   if (!c) return fail(DFLOW_EINVAL, "move_slot: null context");
   if (from < 0 || from >= c->dm.max_batch || to < 0 || to >= c->dm.max_batch)

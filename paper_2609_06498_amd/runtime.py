@@ -104,6 +104,8 @@ EXPORTS = {
                                         ctypes.c_void_p]),
     "kv_commit": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
     "dflow_qkv_parts": (ctypes.c_int, [ctypes.c_void_p]),
+    "dflow_attention_split": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int),
+                                             ctypes.POINTER(ctypes.c_int)]),
     "dflow_move_slot": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int]),
     "dflow_bench_force_drafts": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
                                                 ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -351,6 +353,14 @@ class Runtime:
     def qkv_parts(self) -> int:
         """K parts of the QKV projection (fp32 partial sums added by its consumers)."""
         return int(self.lib.dflow_qkv_parts(self.ctx))
+
+    @property
+    def attention_split(self) -> tuple:
+        """(keys per LDS chunk, chunks per attention split) of the round calls."""
+        ck, nc = ctypes.c_int(), ctypes.c_int()
+        self._check(self.lib.dflow_attention_split(self.ctx, ctypes.byref(ck), ctypes.byref(nc)),
+                    "dflow_attention_split")
+        return ck.value, nc.value
 
     def move_slot(self, src: int, dst: int):
         self._check(self.lib.dflow_move_slot(self.ctx, _stream(), int(src), int(dst)), "dflow_move_slot")

@@ -55,6 +55,7 @@ def test_validation_errors_without_device(lib):
     assert lib.dflow_create(None, None, None, None, 0, None, None, None) == -1
     assert lib.dflow_move_slot(None, None, 0, 1) == -1
     assert lib.dflow_qkv_parts(None) == -1
+    assert lib.dflow_attention_split(None, None, None) == -1
     assert lib.dflow_sample_draft(None, None, 1, None, None, None, None, None, None) == -1
     assert lib.dflow_accept_sampled(None, None, 1, None, None, None, None, None, None, None, None, None, None) == -1
     assert lib.dflow_trajectory_targets(None, None, 1, None, 8, 8, None, None) == -1

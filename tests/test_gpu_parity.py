@@ -30,7 +30,7 @@ def lib():
     return load_library()
 
 
-def _setup(name, window=None):
+def _setup(name, window=None, capacity=None):
     from oracle import Mode, OracleDFlow, OracleModel
     from paper_2609_06498_amd import Runtime
     wl = get_config(name)
@@ -44,7 +44,10 @@ def _setup(name, window=None):
     sched = make_schedule(wl)
     need = trajectory_length_needed(wl, sched)
     max_ctx = max(need) + wl.block
-    rt = Runtime(dm, wl.block, wl.batch, max_ctx, w, wl.carry_window)
+    max_batch = wl.batch
+    if capacity is not None:   # a larger context capacity than the sequences use
+        max_batch, max_ctx = max(capacity[0], wl.batch), max(capacity[1], max_ctx)
+    rt = Runtime(dm, wl.block, max_batch, max_ctx, w, wl.carry_window)
     return wl, w, o, prompts, sched, need, rt
 
 
@@ -61,13 +64,26 @@ def test_round_parity_carry_windows(lib, name, window):
     _round_parity(name, True, window)
 
 
-def _round_parity(name, carry_on, window=None):
+@pytest.mark.parametrize("name", ["small-f32", "small-bf16"])
+def test_round_parity_multichunk(lib, name):
+    """Attention splits of several LDS chunks (the running softmax carried from
+    chunk to chunk, the last one partial).  The chunk count follows from the
+    capacity (batch x kv heads x chunks spread over the compute units): a
+    capacity of 64 sequences x 2048 positions gives splits of several chunks,
+    and the 356..402-key sequence of these cases spans more than one of them."""
+    _round_parity(name, True, capacity=(64, 2048), min_chunks=2)
+
+
+def _round_parity(name, carry_on, window=None, capacity=None, min_chunks=1):
     from paper_2609_06498_amd.session import Session
-    wl, w, o, prompts, sched, need, rt = _setup(name, window)
+    wl, w, o, prompts, sched, need, rt = _setup(name, window, capacity)
+    chunk_keys, chunks = rt.attention_split
+    assert chunks >= min_chunks, (chunk_keys, chunks)
+    assert max(need) > chunk_keys or min_chunks == 1
     dm, B, K, b, V = wl.dims, wl.block, wl.K, wl.batch, wl.dims.vocab
     tol = TOL[dm.dtype]
-    print(f"[parity] {name} carry_on={carry_on} window={wl.carry_window} b={b} ctx={[len(p) for p in prompts]}",
-          flush=True)
+    print(f"[parity] {name} carry_on={carry_on} window={wl.carry_window} b={b} ctx={[len(p) for p in prompts]} "
+          f"split={chunks}x{chunk_keys}", flush=True)
     sess = Session(rt, b)
     states = [o.prefill(p) for p in prompts]
     sess.prefill(prompts)
