@@ -9,6 +9,8 @@ tolerance (an excused near-tie: the oracle then follows the device's
 decision).  bf16 additionally requires argmax agreement wherever the margin
 exceeds four times the observed logit error of the row.
 """
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -30,12 +32,14 @@ def lib():
     return load_library()
 
 
-def _setup(name, window=None, capacity=None):
+def _setup(name, window=None, capacity=None, n_heads=None):
     from oracle import Mode, OracleDFlow, OracleModel
     from paper_2609_06498_amd import Runtime
     wl = get_config(name)
     if window is not None:
         wl = wl.with_(carry_window=window)
+    if n_heads is not None:   # another GQA group size at the same widths
+        wl = wl.with_(dims=replace(wl.dims, n_heads=n_heads))
     dm = wl.dims
     w = make_weights(dm, wl.seed_w)
     mode = "fp32" if dm.dtype == "f32" else "bf16"
@@ -74,9 +78,18 @@ def test_round_parity_multichunk(lib, name):
     _round_parity(name, True, capacity=(64, 2048), min_chunks=2)
 
 
-def _round_parity(name, carry_on, window=None, capacity=None, min_chunks=1):
+@pytest.mark.parametrize("name", ["small-f32", "small-bf16"])
+def test_round_parity_multichunk_group8(lib, name):
+    """The same with a GQA group of 8 (16 query heads on 2 kv heads): 128 query
+    rows per kv head, so attention takes its unfused eight-wave form (queries
+    normalised and rotated by their own kernel) -- the Qwen3-32B shape's
+    launch -- with multi-chunk splits."""
+    _round_parity(name, True, capacity=(64, 2048), min_chunks=2, n_heads=16)
+
+
+def _round_parity(name, carry_on, window=None, capacity=None, min_chunks=1, n_heads=None):
     from paper_2609_06498_amd.session import Session
-    wl, w, o, prompts, sched, need, rt = _setup(name, window, capacity)
+    wl, w, o, prompts, sched, need, rt = _setup(name, window, capacity, n_heads)
     chunk_keys, chunks = rt.attention_split
     assert chunks >= min_chunks, (chunk_keys, chunks)
     assert max(need) > chunk_keys or min_chunks == 1
