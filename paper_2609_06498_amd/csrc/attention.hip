@@ -544,6 +544,8 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
     __syncthreads();                           // the pages are no longer read
     float* scr = reinterpret_cast<float*>(lk);     // [4][DT][4][64] outputs, then [4][16][2] (m, l)
     float* sml = scr + 4 * DT * 4 * 64;
+    static_assert((4 * DT * 4 * 64 + 4 * 16 * 2) * sizeof(float) <= 2 * NPG * PG * sizeof(T),
+                  "the merge scratch fits in the chunk's key and value pages");
     if (own2 && par == 1) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
