@@ -503,6 +503,18 @@ hipError_t attention(dflow_ctx* c, hipStream_t st, const dflow_layer& L, int nse
     a.split_keys = c->split_keys * a.chunks;
     a.nsplit = (c->dm.max_pages * PAGE + a.split_keys - 1) / a.split_keys;   // <= c->nsplit
   }
+  // Round launches that leave compute units idle pull the O projection's
+  // weights (the next launch's stream) into the memory-side cache meanwhile,
+  // at most ATTN_PF_WG_BYTES per idle unit.
+  if (c->phase != DFLOW_PHASE_PREFILL && L.wo && c->cus > nseq * a.Hkv * a.nsplit) {
+    const int idle = c->cus - nseq * a.Hkv * a.nsplit;
+    const size_t wo_bytes = (size_t)c->dm.d * c->q_dim * c->elt;
+    const size_t cap = (size_t)idle * ATTN_PF_WG_BYTES;
+    a.pf = L.wo;
+    a.pf_bytes = (wo_bytes < cap ? wo_bytes : cap) / 16 * 16;
+    a.pf_per = ((a.pf_bytes + idle - 1) / idle + 15) / 16 * 16;
+    a.pf_wgs = idle;
+  }
   a.num_pages = c->dm.num_pages;
   a.rg = (Bq * c->G + 15) / 16;
   a.part_o = c->part_o;

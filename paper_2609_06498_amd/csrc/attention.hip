@@ -107,6 +107,35 @@ __device__ inline int vfrag_off(int slot, int e) {
 // A row's arithmetic depends only on its own visible keys and the fixed split
 // boundaries (and page order within them), never on the batch it is part of.
 // MC = 0 instantiates single-chunk splits only (no chunk loop).
+
+// Prefetch workgroup wg of an attention launch: plain 16-byte loads of its
+// slice of p.pf (eight in flight per thread), which allocate in the
+// memory-side cache; the loaded values only feed an empty asm statement.
+// These workgroups run on the compute units the attention workgroups leave
+// idle (the launch's LDS size keeps the two kinds off each other's units).
+// They first sleep about 8K clocks (a few microseconds), so the attention
+// workgroups' latency-bound first loads go out ahead of the prefetch stream:
+// without the pause the attention launch grew by 0.6-1.5 us at the 8B shape.
+template <int NT>
+__device__ __forceinline__ void attn_prefetch(const AttnParams& p, int wg) {
+  __builtin_amdgcn_s_sleep(127);
+  const size_t b0 = (size_t)wg * p.pf_per;
+  const size_t b1 = b0 + p.pf_per < p.pf_bytes ? b0 + p.pf_per : p.pf_bytes;
+  const gu4* src = (const gu4*)(p.pf);
+  u32x4_t x = u32x4_t{0u, 0u, 0u, 0u};
+  size_t i = b0 / 16 + threadIdx.x;
+  const size_t e = b1 / 16;
+  for (; i + 7 * NT < e; i += 8 * NT) {
+    u32x4_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[i + (size_t)u * NT];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x ^= v[u];
+  }
+  for (; i < e; i += NT) x ^= src[i];
+  asm volatile("" ::"v"(x[0]), "v"(x[1]), "v"(x[2]), "v"(x[3]));
+}
+
 template <typename T, int DH, int NW, bool FUSED, int NPART, int NPG, bool MC>
 __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   constexpr int KL = TT<T>::KL, KT = TT<T>::KT;
@@ -132,6 +161,10 @@ __global__ void __launch_bounds__(NW * 64) attn_kernel(AttnParams p) {
   T* lk = reinterpret_cast<T*>(smem);         // [NPG][PG] keys, fragment order
   T* lv = lk + (size_t)NPG * PG;              // [NPG][PG] values, fragment order
 
+  if ((int)blockIdx.x >= p.nseq * p.Hkv * p.nsplit) {   // prefetch workgroup (uniform)
+    attn_prefetch<NW * 64>(p, (int)blockIdx.x - p.nseq * p.Hkv * p.nsplit);
+    return;
+  }
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int item = blockIdx.x;                // (seq, kv head, split), split fastest
@@ -675,7 +708,11 @@ static hipError_t launch_kn(const AttnParams& p, hipStream_t st) {
       reinterpret_cast<const void*>(&attn_kernel<T, DH, NW, FUSED, NPART, NPG, MC>),
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)ATTN_LDS_MAX);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART, NPG, MC>), dim3(p.nseq * p.Hkv * p.nsplit), dim3(NW * 64),
+  if (p.pf_wgs < 0 || (p.pf_wgs > 0 && (!p.pf || p.pf_per % 16 || p.pf_bytes % 16 ||
+                                        (size_t)p.pf_wgs * p.pf_per < p.pf_bytes)))
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL((attn_kernel<T, DH, NW, FUSED, NPART, NPG, MC>), dim3(p.nseq * p.Hkv * p.nsplit + p.pf_wgs),
+                     dim3(NW * 64),
                      lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

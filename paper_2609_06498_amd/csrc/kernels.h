@@ -43,7 +43,17 @@ struct AttnParams {
   float* part_ml;            // [nseq][Hkv][rg][nsplit][16][2]
   void* out;                 // [nseq*Bq, Hq*Dh] storage type
   FragOut outf;              // matrix-core-order copy of out for the O projection (skinny launches)
+  // pf_wgs extra workgroups (after the nseq*Hkv*nsplit attention ones) read
+  // bytes [0, pf_bytes) of pf, pf_per bytes each (multiples of 16), with
+  // plain loads that leave them in the memory-side cache for the next
+  // launch's non-temporal weight stream; pf_wgs = 0: none
+  const void* pf; size_t pf_bytes; size_t pf_per; int pf_wgs;
 };
+// Bytes one prefetch workgroup of an attention launch reads: what a compute
+// unit pulls in between the workgroup's pause and the end of a skinny round's
+// attention (8B shape: 192 KB per unit, 21.5 of the O projection's 33.6 MB;
+// 256 KB stretched the launch by 0.5 us for 0.15 us more gain).
+constexpr size_t ATTN_PF_WG_BYTES = 192 * 1024;
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
 // Waves per attention workgroup (each owns one 16-row group; more groups need chunks = 1).
 int attention_waves(bool fused, int Bq, int G);
