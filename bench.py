@@ -76,6 +76,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 TRAFFIC_KERNEL = ("gemm.swiglu N=24576 K=4096 M=16", "_ZN5dflow11gemm_kernelINS_4bf16ELi2ELi1ELi3ELb1EEEvNS_10GemmParamsE",
                   "gemm_kernel<dflow::bf16, 2, 1, 3, true>", 24576 * 4096 * 2 + 16 * 4096 * 2 + 16 * 12288 * 2)
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
+PROF_EVENTS = 16384   # launches the library's per-launch event record holds (dflow_profile)
 NSEG = 4   # timed segments (median and min per-step time besides the whole-run value)
 
 
@@ -419,7 +420,10 @@ def main():
     else:
         gb, nl = gemm_bytes(rt, b, relay=carry_on)
     if not args.no_kernel_timing:
-        kp = min(K, max(1, 64 // rounds_per_step))   # about 64 rounds: within the library's event record
+        # about 64 rounds, and no more than the library's event record holds
+        # (PROF_EVENTS launches: GEMMs plus one attention launch per layer)
+        per_step = nl + (dm.n_layers + dm.n_draft_layers) * rounds_per_step
+        kp = max(1, min(K, 64 // rounds_per_step, PROF_EVENTS // per_step))
         reset()
         torch.cuda.synchronize()
         rt.profile(True)

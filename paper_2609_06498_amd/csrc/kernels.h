@@ -45,14 +45,14 @@ struct AttnParams {
   FragOut outf;              // matrix-core-order copy of out for the O projection (skinny launches)
   // pf_wgs extra workgroups (after the nseq*Hkv*nsplit attention ones) read
   // bytes [0, pf_bytes) of pf, pf_per bytes each (multiples of 16), with
-  // plain loads that leave them in the memory-side cache for the next
+  // plain loads that leave them in the memory-side cache for a following
   // launch's non-temporal weight stream; pf_wgs = 0: none
   const void* pf; size_t pf_bytes; size_t pf_per; int pf_wgs;
 };
 // Bytes one prefetch workgroup of an attention launch reads: what a compute
 // unit pulls in between the workgroup's pause and the end of a skinny round's
-// attention (8B shape: 192 KB per unit, 21.5 of the O projection's 33.6 MB;
-// 256 KB stretched the launch by 0.5 us for 0.15 us more gain).
+// attention (8B shape: 192 KB per unit, 21.5 MB over 112 idle units; 256 KB
+// stretched the launch by 0.5-0.9 us for less than that gained).
 constexpr size_t ATTN_PF_WG_BYTES = 192 * 1024;
 hipError_t launch_attention(bool bf16, const AttnParams& p, hipStream_t s);
 // Waves per attention workgroup (each owns one 16-row group; more groups need chunks = 1).
