@@ -101,6 +101,14 @@ def measured_traffic(kernel_name):
     return int(rec["fetch_bytes"] + rec["write_bytes"])
 
 
+def profiled_steps(steps, rounds_per_step, gemm_launches, attn_layers):
+    """Steps of the per-launch event pass: about 64 rounds, at most `steps`,
+    and no more than the library's event record holds (PROF_EVENTS launches:
+    the step's GEMM launches plus one attention launch per layer and round)."""
+    per_step = gemm_launches + attn_layers * rounds_per_step
+    return max(1, min(steps, 64 // rounds_per_step, PROF_EVENTS // per_step))
+
+
 def write_traffic_record(fetch_csv, write_csv, copy_mib=256):
     """HBM bytes per launch of the dominant kernel from two rocprofv3 counter
     passes of `bench.py --counter-pass --calib-copy-mib 256`: each counter's
@@ -420,10 +428,7 @@ def main():
     else:
         gb, nl = gemm_bytes(rt, b, relay=carry_on)
     if not args.no_kernel_timing:
-        # about 64 rounds, and no more than the library's event record holds
-        # (PROF_EVENTS launches: GEMMs plus one attention launch per layer)
-        per_step = nl + (dm.n_layers + dm.n_draft_layers) * rounds_per_step
-        kp = max(1, min(K, 64 // rounds_per_step, PROF_EVENTS // per_step))
+        kp = profiled_steps(K, rounds_per_step, nl, dm.n_layers + dm.n_draft_layers)
         reset()
         torch.cuda.synchronize()
         rt.profile(True)

@@ -79,3 +79,19 @@ def test_traffic_record_arithmetic(tmp_path, monkeypatch):
     assert rec["kernel"] == name and rec["symbol"] == symbol and rec["code_sha256"] == "d" * 64
     assert rec["fetch_factor"] == 0.5 and rec["write_factor"] == 1.0 and rec["dispatches"] == 2
     assert rec["fetch_bytes"] == 1001 * 1024 * 2 and rec["write_bytes"] == 768 * 1024
+
+
+def test_profiled_steps_fit_the_event_record():
+    """The per-launch event pass never records more launches than the
+    library holds (the 32B shape at 64 steps once overflowed it)."""
+    import bench
+    # 8B shape, b = 1: ~170 GEMM launches and 41 attention launches per round
+    assert bench.profiled_steps(128, 1, 170, 41) == 64
+    # 32B shape: 64 + 5 layers -> 45 rounds fit
+    k = bench.profiled_steps(64, 1, 290, 69)
+    assert k * (290 + 69) <= bench.PROF_EVENTS < (k + 1) * (290 + 69)
+    # rollouts: rounds per step divide the 64-round target
+    assert bench.profiled_steps(10, 3, 3 * 100, 20) == 10
+    assert bench.profiled_steps(100, 3, 3 * 100, 20) == 21
+    # never zero
+    assert bench.profiled_steps(8, 1, 10 ** 6, 10) == 1
